@@ -1,0 +1,336 @@
+/* rc.h - C ABI of the schedule-parameterised contraction library (librc).
+ *
+ * The paper (Sec. 2, Eq. 1) states compiler optimisation as: an input
+ * program P0 that is one layer of a network, a set M of semantics-preserving
+ * transformations, a sequence of at most T of them, and an objective f
+ * measured on the target.  This library is that statement for MI355X
+ * (gfx950):
+ *   - P0 is an operator descriptor (rc_op_desc): one of five dense
+ *     contractions with fused epilogues, the layer kinds of Sec. 4.1
+ *     (attention, MoE, convolution, gated MLP) plus the fp32 contraction of
+ *     the App. A example module;
+ *   - a program variant is a schedule (rc_schedule): one integer per knob;
+ *   - a transformation (rc_transform) sets one knob, named after the
+ *     transformation classes of App. A (TileSize, Parallel,
+ *     ComputeLocation, Unroll) plus Vectorize and Layout (Sec. 1);
+ *   - f is the measured throughput of the HIP kernels the schedule
+ *     instantiates (rc_time), and the search of Sec. 3.2 runs over it
+ *     (rc_search_*).
+ *
+ * Conventions for every call:
+ *   - Functions return rc_status; RC_OK is 0.  On failure a thread-local
+ *     message is available from rc_last_error().  No C++ exception and no
+ *     abort crosses this interface.
+ *   - Structs start with uint32_t struct_size, which callers set to
+ *     sizeof(the struct) (rc_*_init helpers do it).
+ *   - The library never allocates, frees or retains caller tensors.  Device
+ *     pointers are caller-owned, must stay valid until the work queued on the
+ *     stream has finished, must be 16-byte aligned and contiguous in the
+ *     layout stated for the operator.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Launch calls only enqueue work; they never synchronise the host.
+ *   - Illegal schedules are rejected on the host before any compilation or
+ *     GPU work.
+ */
+#ifndef RC_H
+#define RC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum rc_status {
+    RC_OK = 0,
+    RC_ERR_INVALID_ARGUMENT = 1,
+    RC_ERR_ILLEGAL_SCHEDULE = 2,
+    RC_ERR_UNSUPPORTED = 3,
+    RC_ERR_COMPILE = 4,
+    RC_ERR_HIP = 5,
+    RC_ERR_OUT_OF_MEMORY = 6,
+    RC_ERR_MISALIGNED = 7,
+    RC_ERR_BUDGET = 8
+} rc_status;
+
+/* Human-readable name of a status code (static storage). */
+const char *rc_status_str(rc_status s);
+/* Detail text of the last failing call on this thread (empty if none). */
+const char *rc_last_error(void);
+
+/* ------------------------------------------------------------------ */
+/* Operators: the input program P0 (Sec. 2; App. A)                    */
+/* ------------------------------------------------------------------ */
+
+typedef enum rc_op_kind {
+    /* C[M][N] = A[M][K] B[K][N], fp32 in and out (the App. A contraction).
+     * dim = {M, N, K}.  Inputs: in[0] = A [M][K]; in[1] = B stored [K][N]
+     * (layout 0) or [N][K] (layout 1).  Output: out[0] = C [M][N]. */
+    RC_OP_GEMM_F32 = 1,
+    /* Softmax attention, bf16 Q/K/V/O [B][H][S][D], scale 1/sqrt(D), fp32
+     * scores and softmax (the self-attention layers of Sec. 4.1).
+     * dim = {B, H, S, D}; flags & RC_FLAG_CAUSAL selects the top-left aligned
+     * causal mask (key j visible to query i iff j <= i).
+     * in[0] = Q, in[1] = K, in[2] = V; out[0] = O. */
+    RC_OP_ATTENTION = 2,
+    /* Gated MLP (the MLP layer of Sec. 4.1):
+     *   out = bf16( bf16( SiLU(X Wg) * (X Wu) ) Wd ), fp32 accumulation.
+     * dim = {T, Hd, I}.  in[0] = X [T][Hd]; in[1] = Wg, in[2] = Wu stored
+     * [Hd][I] (up.layout 0) or [I][Hd] (up.layout 1); in[3] = Wd stored
+     * [I][Hd] (down.layout 0) or [Hd][I] (down.layout 1); out[0] = [T][Hd]. */
+    RC_OP_GATED_MLP = 3,
+    /* Routed mixture of gated-MLP experts (the MoE layer of Sec. 4.1):
+     *   out[t] = bf16( sum_s w[t][s] * expert_{ids[t][s]}(X[t]) ),
+     *   expert_e(x) = bf16( SiLU(x Wg[e]) * (x Wu[e]) ) Wd[e].
+     * dim = {T, Hd, E, I, topk}.  in[0] = X [T][Hd] bf16; in[1] = ids
+     * [T][topk] int32 in [0, E); in[2] = w [T][topk] fp32; in[3] = Wg,
+     * in[4] = Wu stored [E][Hd][I] (up.layout 0) or [E][I][Hd] (1);
+     * in[5] = Wd stored [E][I][Hd] (down.layout 0) or [E][Hd][I] (1);
+     * out[0] = [T][Hd] bf16.  Routing (ids, w) is an input. */
+    RC_OP_MOE = 4,
+    /* 2-D convolution, stride 1, zero padding, bias and SiLU (the
+     * convolution layer of Sec. 4.1), as an implicit GEMM:
+     *   y = bf16( SiLU( conv(x, w) + bias ) ).
+     * dim = {N, H, W, C, K, R, S, pad}.  in[0] = x [N][H][W][C] bf16;
+     * in[1] = w stored [K][R][S][C] (layout 1) or [R][S][C][K] (layout 0)
+     * bf16; in[2] = bias [K] fp32; out[0] = y [N][P][Q][K] bf16 with
+     * P = H + 2 pad - R + 1, Q = W + 2 pad - S + 1. */
+    RC_OP_CONV2D = 5
+} rc_op_kind;
+
+#define RC_FLAG_CAUSAL 1
+#define RC_MAX_DIMS 8
+
+typedef struct rc_op_desc {
+    uint32_t struct_size;
+    int32_t kind;              /* rc_op_kind */
+    int64_t dim[RC_MAX_DIMS];  /* meaning per kind, unused entries 0 */
+    int32_t flags;
+    int32_t reserved;
+} rc_op_desc;
+
+/* Fill *d for `kind` with `ndims` dimensions.  Checks the kind, the number
+ * of dimensions and that every dimension is positive (pad may be 0). */
+rc_status rc_op_init(rc_op_desc *d, int32_t kind, const int64_t *dims, int32_t ndims,
+                     int32_t flags);
+
+/* Algorithmic work of one execution of the operator.
+ * FLOPs count 2 per multiply-add of the contraction only (for causal
+ * attention only visible query/key pairs; for MoE only routed rows);
+ * bytes count compulsory HBM traffic: each input read once and each output
+ * written once.  Negative on an invalid descriptor. */
+double rc_op_flops(const rc_op_desc *d);
+double rc_op_bytes(const rc_op_desc *d);
+/* Published MI355X peak that bounds the operator: fp32 MFMA (157.3 TFLOP/s)
+ * for RC_OP_GEMM_F32, bf16 MFMA (2516.6 TFLOP/s) otherwise, in FLOP/s;
+ * and HBM bandwidth (8.0e12 B/s). */
+double rc_peak_flops(const rc_op_desc *d);
+double rc_peak_bytes_per_s(void);
+
+/* ------------------------------------------------------------------ */
+/* Schedules and transformations (Sec. 2, Eq. 1; App. A)              */
+/* ------------------------------------------------------------------ */
+
+#define RC_MAX_KNOBS 24
+
+typedef struct rc_schedule {
+    uint32_t struct_size;
+    int32_t nknobs;
+    int32_t knob[RC_MAX_KNOBS];
+} rc_schedule;
+
+/* One transformation: set knob `knob` to `value`. */
+typedef struct rc_transform {
+    int32_t knob;
+    int32_t value;
+} rc_transform;
+
+/* Knob table of an operator: the count, each knob's name ("tile_m",
+ * "up.tile_n", ...), its transformation class ("TileSize", "Parallel",
+ * "Vectorize", "Unroll", "ComputeLocation", "Layout") and its allowed
+ * values.  Names point to static storage. */
+int32_t rc_knob_count(const rc_op_desc *d);
+const char *rc_knob_name(const rc_op_desc *d, int32_t knob);
+const char *rc_knob_class(const rc_op_desc *d, int32_t knob);
+rc_status rc_knob_values(const rc_op_desc *d, int32_t knob, int32_t *vals, int32_t cap,
+                         int32_t *n);
+
+/* The untransformed program P0: smallest tiles, one wave, one stage,
+ * narrowest vectors, no unrolling, unfused epilogue, canonical layout.  It is
+ * legal for every operator this library accepts, and it is the denominator
+ * of reported speedups (Sec. 4.2). */
+rc_status rc_default_schedule(const rc_op_desc *d, rc_schedule *out);
+
+/* Legality check, host only.  Returns RC_OK or RC_ERR_ILLEGAL_SCHEDULE with
+ * the first violated rule written to `why` (may be NULL). */
+rc_status rc_validate(const rc_op_desc *d, const rc_schedule *s, char *why, size_t why_len);
+
+/* Apply one transformation: out = t(in).  If the result is illegal, returns
+ * RC_ERR_ILLEGAL_SCHEDULE and leaves *out untouched.  in == out allowed. */
+rc_status rc_apply(const rc_op_desc *d, const rc_schedule *in, const rc_transform *t,
+                   rc_schedule *out);
+
+/* The action set at a state: every transformation whose result is legal and
+ * differs from `at`.  Writes min(count, cap) entries and the full count. */
+rc_status rc_enumerate(const rc_op_desc *d, const rc_schedule *at, rc_transform *buf,
+                       size_t cap, size_t *n);
+
+/* Parse a textual transformation proposal such as "TileSize(up.tile_m=128)"
+ * or "Unroll(unroll=2)".  Only a known class with one of its own knobs and
+ * an allowed value is accepted (Sec. 3.1, proposal validation); anything
+ * else returns RC_ERR_INVALID_ARGUMENT. */
+rc_status rc_parse_transform(const rc_op_desc *d, const char *text, rc_transform *out);
+
+/* "name=value,name=value,..." for logs; from_string accepts the same form
+ * (missing knobs keep their default). */
+rc_status rc_schedule_to_string(const rc_op_desc *d, const rc_schedule *s, char *buf,
+                                size_t len);
+rc_status rc_schedule_from_string(const rc_op_desc *d, const char *text, rc_schedule *out);
+uint64_t rc_schedule_hash(const rc_schedule *s);
+
+/* ------------------------------------------------------------------ */
+/* Plans: a compiled program variant                                  */
+/* ------------------------------------------------------------------ */
+
+typedef struct rc_plan rc_plan;
+
+/* Validate, generate the kernels' source for this schedule, compile them for
+ * gfx950 with hipRTC (or load the cached code object) and load them on the
+ * current device.  A variant whose kernels need scratch memory (register
+ * spills) is rejected as RC_ERR_ILLEGAL_SCHEDULE ("spill").  The plan is
+ * immutable and may be launched concurrently on different streams. */
+rc_status rc_plan_create(const rc_op_desc *d, const rc_schedule *s, rc_plan **out);
+void rc_plan_destroy(rc_plan *p);
+
+/* Compile (without loading) the variants of n schedules into the code-object
+ * cache using `nthreads` host threads; needs no GPU.  status[i] receives each
+ * result (may be NULL). */
+rc_status rc_precompile(const rc_op_desc *d, const rc_schedule *s, int32_t n, int32_t nthreads,
+                        rc_status *status);
+
+/* Directory of the on-disk code-object cache (set before the first compile;
+ * NULL restores the default: $RC_CACHE_DIR, else the package's jit_cache). */
+rc_status rc_set_cache_dir(const char *dir);
+
+/* Bytes of device workspace a launch needs (0 if none).  The caller
+ * allocates it; its contents need not be initialised. */
+rc_status rc_plan_workspace(const rc_plan *p, size_t *bytes);
+/* Number of kernels one launch enqueues, and the index of the one doing
+ * most of the FLOPs (the contraction). */
+rc_status rc_plan_kernels(const rc_plan *p, int32_t *nkernels, int32_t *dominant);
+
+typedef struct rc_args {
+    uint32_t struct_size;
+    const void *in[8];
+    void *out[2];
+} rc_args;
+
+/* Enqueue one execution of the operator on `stream`.  Checks pointers
+ * (non-NULL, 16-byte aligned) and the workspace size; never synchronises. */
+rc_status rc_launch(const rc_plan *p, const rc_args *a, void *workspace, size_t ws_bytes,
+                    void *stream);
+
+/* Enqueue one execution with a HIP event recorded before and after each
+ * kernel: events[0..nkernels] (caller-created hipEvent_t, passed as void*).
+ * The duration of kernel i is elapsed(events[i], events[i+1]). */
+rc_status rc_launch_timed(const rc_plan *p, const rc_args *a, void *workspace,
+                          size_t ws_bytes, void *stream, void **events, int32_t nevents);
+
+typedef struct rc_time_opts {
+    uint32_t struct_size;
+    int32_t warmup;   /* untimed launches first (default 3) */
+    int32_t repeat;   /* timed launches (default 20) */
+    int32_t flush;    /* 1: overwrite a 512 MiB buffer before each timed
+                         launch so no operand is cache-resident */
+    int32_t reserved;
+} rc_time_opts;
+
+typedef struct rc_timing {
+    uint32_t struct_size;
+    int32_t nkernels;
+    double median_ms, min_ms, mean_ms, q1_ms, q3_ms;
+    double tflops;        /* rc_op_flops / median */
+    double gbps;          /* rc_op_bytes / median */
+    double frac_flops;    /* tflops / peak */
+    double frac_bytes;    /* gbps / HBM peak */
+    double kernel_ms[4];  /* median duration of each kernel */
+} rc_timing;
+
+void rc_time_opts_init(rc_time_opts *o);
+
+/* Time a plan: warm-ups, then `repeat` launches each bracketed by HIP
+ * events on `stream` (flush outside the brackets).  Synchronises the
+ * stream. */
+rc_status rc_time(const rc_plan *p, const rc_args *a, void *workspace, size_t ws_bytes,
+                  void *stream, const rc_time_opts *o, rc_timing *out);
+
+/* ------------------------------------------------------------------ */
+/* Search (Sec. 3.2): UCT tree search, random sampling, exhaustive     */
+/* ------------------------------------------------------------------ */
+
+typedef enum rc_policy {
+    RC_POLICY_RANDOM = 0,      /* random legal transformation sequences */
+    RC_POLICY_UCT = 1,         /* MCTS with UCT selection (Sec. 3.2) */
+    RC_POLICY_EXHAUSTIVE = 2   /* every legal schedule of the listed space */
+} rc_policy;
+
+/* Evaluate one schedule (the objective f).  Return 0 and set *reward (>= 0,
+ * larger is better) for a valid sample; nonzero marks the schedule invalid
+ * (compile failure, spill, launch error), which costs no budget. */
+typedef int32_t (*rc_eval_fn)(void *user, const rc_schedule *s, double *reward);
+
+/* Optional transformation proposer for expansion (Sec. 3.1): writes a
+ * proposal text for the node `at` (whose ancestors' schedules are
+ * parent/grandparent, NULL at the root).  Proposals are parsed with
+ * rc_parse_transform; when none is valid the search samples a random legal
+ * transformation instead. */
+typedef int32_t (*rc_propose_fn)(void *user, const rc_schedule *at, const rc_schedule *parent,
+                                 const rc_schedule *grandparent, char *buf, size_t len);
+
+typedef struct rc_search_opts {
+    uint32_t struct_size;
+    int32_t policy;       /* rc_policy */
+    int32_t budget;       /* valid samples to measure */
+    int32_t horizon;      /* maximum sequence length T (default 12) */
+    int32_t branching;    /* maximum children per node B (default 2) */
+    double c;             /* UCT exploration constant (default sqrt(2)) */
+    uint64_t seed;
+    int32_t max_invalid;  /* stop after this many invalid samples (default 10 * budget) */
+    int32_t reserved;
+} rc_search_opts;
+
+typedef struct rc_sample {
+    rc_schedule schedule;
+    double reward;
+    int32_t valid;
+    int32_t index;        /* valid-sample index (-1 if invalid) */
+    double best_so_far;
+} rc_sample;
+
+typedef struct rc_search rc_search;
+
+void rc_search_opts_init(rc_search_opts *o);
+rc_status rc_search_create(const rc_op_desc *d, const rc_search_opts *o, rc_eval_fn eval,
+                           void *eval_user, rc_search **out);
+rc_status rc_search_set_proposer(rc_search *s, rc_propose_fn fn, void *user);
+/* One iteration: select, expand, roll out, evaluate, back-propagate.
+ * *done = 1 once the budget (or the space) is exhausted. */
+rc_status rc_search_step(rc_search *s, int32_t *done);
+rc_status rc_search_run(rc_search *s);
+rc_status rc_search_best(const rc_search *s, rc_schedule *best, double *reward,
+                         int32_t *sample_index);
+/* All evaluations in order (valid and invalid). */
+rc_status rc_search_history(const rc_search *s, rc_sample *buf, int32_t cap, int32_t *n);
+/* Tree statistics of the root's children for tests: visits and cumulative
+ * reward W of the node reached by applying t at the root (0s if absent). */
+rc_status rc_search_node_stats(const rc_search *s, const rc_transform *path, int32_t len,
+                               int32_t *visits, double *W);
+/* Count of proposals that fell back to a random legal transformation. */
+rc_status rc_search_fallbacks(const rc_search *s, int32_t *n);
+void rc_search_destroy(rc_search *s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* RC_H */

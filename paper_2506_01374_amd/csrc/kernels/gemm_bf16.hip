@@ -1,0 +1,350 @@
+// bf16 x bf16 -> fp32 MFMA GEMM for gfx950 with fused epilogues.  One
+// template serves the gated MLP (dual weight operand + SiLU(g)*u), its down
+// projection, the MoE expert GEMMs (gathered / grouped rows) and the
+// implicit-GEMM convolution (bias + SiLU).
+//
+// Compile-time schedule (generated prologue):
+//   TM TN TK     workgroup tile (TileSize)
+//   WM WN        waves along M and N (Parallel); NT = 64 * WM * WN threads
+//   MF           MFMA shape: 16 -> v_mfma_f32_16x16x32_bf16,
+//                             32 -> v_mfma_f32_32x32x16_bf16
+//   STAGES       1: load, store, compute; 2: LDS double buffer with register
+//                prefetch of the next K tile (ComputeLocation)
+//   VEC          bf16 elements per global load: 2, 4 or 8 (Vectorize)
+//   UNROLL       unroll factor of the K-tile loop (Unroll)
+//   LAYOUT       weights stored 0: [K][N], 1: [N][K] (Layout)
+//   GRID         0: tile n fastest; 1: tile m fastest, with workgroups
+//                regrouped so each XCD owns a contiguous range of tiles
+//   NB           weight operands sharing the A tile (1, or 2 for gate/up)
+//   AMODE        A rows: 0 dense [GM][GK]; 1 MoE gather (row p of expert e
+//                reads X[perm[p] / TOPK]); 2 implicit im2col of an NHWC
+//                image; 3 MoE grouped dense rows (row p of the permuted
+//                hidden matrix)
+//   EPI          0 store bf16; 1 + bias, SiLU, store bf16; 2 SiLU(acc0) *
+//                acc1, store bf16; 3 store fp32 accumulators (unfused)
+//   GM GN GK     GEMM sizes (GM = rows for AMODE 0/2, total routed rows for
+//                AMODE 1/3)
+//
+// LDS holds both operands as rows of TK bf16 (K contiguous).  16-byte
+// chunks are XOR-swizzled with the row so that the 16 lanes that share a
+// 128-bit LDS access cycle hit distinct banks, for fragment reads and for
+// row-major tile writes alike.
+//
+// The MFMA is issued with the weight fragment as its first operand and the
+// activation fragment as its second, so the accumulator holds C^T: each
+// lane owns one output row m and runs of 4 consecutive output columns n,
+// which the epilogue writes as one 8-byte (bf16) or 16-byte (fp32) store.
+
+#define NT (64 * WM * WN)
+#define WTM (TM / WM)
+#define WTN (TN / WN)
+#define FM (WTM / MF)
+#define FN (WTN / MF)
+#define CPR (TK / 8)
+#define RPL ((16 / CPR) > 0 ? (16 / CPR) : 1)
+#define KTILES (GK / TK)
+#define A_LOADS ((TM * TK) / (VEC * NT))
+#define B_LOADS ((TN * TK) / (VEC * NT))
+#define NTN (GN / TN)
+
+typedef unsigned short bf16_t;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+#if MF == 16
+typedef f32x4 accT;
+#define ACCN 4
+#define KSTEP 32
+#else
+typedef f32x16 accT;
+#define ACCN 16
+#define KSTEP 16
+#endif
+
+template <int V> struct BVec;
+template <> struct BVec<2> { typedef unsigned int T; };
+template <> struct BVec<4> { typedef u32x2 T; };
+template <> struct BVec<8> { typedef u32x4 T; };
+typedef typename BVec<VEC>::T vecT;
+
+struct GemmBf16Args {
+    const bf16_t *A;
+    const bf16_t *B0;
+    const bf16_t *B1;
+    void *C;
+    void *C1;
+    const float *bias;
+    const int *perm;        // MoE: permuted row -> token * TOPK + slot
+    const int *offsets;     // MoE: first permuted row of each expert [NEXP + 1]
+    const int *tile_start;  // MoE: first M tile of each expert [NEXP + 1]
+};
+
+__device__ __forceinline__ int swz(int row, int chunk) {
+    return row * TK + ((chunk ^ ((row / RPL) % CPR)) << 3);
+}
+
+__device__ __forceinline__ bf16_t f2bf(float x) { return __builtin_bit_cast(bf16_t, (__bf16)x); }
+
+__device__ __forceinline__ float silu(float x) {
+    // x * sigmoid(x); exp(-x) as 2^(-x log2 e) on the hardware exp2 unit.
+    return x / (1.0f + __builtin_amdgcn_exp2f(-x * 1.4426950408889634f));
+}
+
+__device__ __forceinline__ accT mfma(const bf16x8 &a, const bf16x8 &b, const accT &c) {
+#if MF == 16
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+#else
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+#endif
+}
+
+// Store VEC bf16 held in a register vector into LDS at element offset `off`.
+__device__ __forceinline__ void lds_store_vec(bf16_t *lds, int off, const vecT &v) {
+    *(vecT *)(lds + off) = v;
+}
+
+__device__ __forceinline__ bf16_t vec_elem(const vecT &v, int j) {
+#if VEC == 2
+    return (bf16_t)(v >> (16 * j));
+#else
+    return (bf16_t)(v[j >> 1] >> (16 * (j & 1)));
+#endif
+}
+
+extern "C" __global__ __launch_bounds__(NT) void rc_gemm_bf16(GemmBf16Args args) {
+    __shared__ __attribute__((aligned(16))) bf16_t As[STAGES][TM * TK];
+    __shared__ __attribute__((aligned(16))) bf16_t Bs[STAGES][NB][TN * TK];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave / WN, wn = wave % WN;
+
+    // ---- workgroup -> tile --------------------------------------------
+    int bid = blockIdx.x;
+    const int nblk = gridDim.x;
+#if GRID == 1
+    if ((nblk & 7) == 0) bid = (bid & 7) * (nblk >> 3) + (bid >> 3);
+    const int ntm_grid = nblk / NTN;
+    int mt = bid % ntm_grid, nt = bid / ntm_grid;
+#else
+    int mt = bid / NTN, nt = bid % NTN;
+#endif
+    const int n0 = nt * TN;
+
+#if AMODE == 1 || AMODE == 3
+    // Ragged expert groups: find the expert owning M tile `mt`.
+    if (mt >= args.tile_start[NEXP]) return;
+    int e = 0;
+    {
+        int lo = 0, hi = NEXP - 1;
+        while (lo < hi) {
+            int mid = (lo + hi + 1) >> 1;
+            if (args.tile_start[mid] <= mt) lo = mid; else hi = mid - 1;
+        }
+        e = lo;
+    }
+    const int mrow0 = (mt - args.tile_start[e]) * TM;
+    const int row_base = args.offsets[e] + mrow0;                  // first permuted row
+    const int rows_valid = min(TM, args.offsets[e + 1] - row_base);
+    const size_t wstride = (size_t)GK * GN;
+    const bf16_t *B0 = args.B0 + (size_t)e * wstride;
+#if NB == 2
+    const bf16_t *B1 = args.B1 + (size_t)e * wstride;
+#endif
+#else
+    const int row_base = mt * TM;
+    const int rows_valid = TM;
+    const bf16_t *B0 = args.B0;
+#if NB == 2
+    const bf16_t *B1 = args.B1;
+#endif
+#endif
+
+    // ---- per-thread A row sources (fixed over the K loop) ---------------
+    const bf16_t *arow[A_LOADS];
+    bool aval[A_LOADS];
+#if AMODE == 2
+    int a_n[A_LOADS], a_p[A_LOADS], a_q[A_LOADS];
+#endif
+#pragma unroll
+    for (int i = 0; i < A_LOADS; ++i) {
+        int v = tid + i * NT;
+        int r = v / (TK / VEC);
+        aval[i] = r < rows_valid;
+#if AMODE == 0
+        arow[i] = args.A + (size_t)(row_base + r) * GK;
+#elif AMODE == 1
+        int tok = aval[i] ? args.perm[row_base + r] / TOPK : 0;
+        arow[i] = args.A + (size_t)tok * GK;
+#elif AMODE == 3
+        arow[i] = args.A + (size_t)(aval[i] ? row_base + r : 0) * GK;
+#else
+        int m = row_base + r;
+        a_n[i] = m / (CV_P * CV_Q);
+        a_p[i] = (m / CV_Q) % CV_P;
+        a_q[i] = m % CV_Q;
+        arow[i] = args.A;
+#endif
+    }
+
+    accT acc[NB][FM][FN];
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int r = 0; r < ACCN; ++r) acc[b][i][j][r] = 0.f;
+
+    vecT ra[A_LOADS];
+    vecT rb[NB][B_LOADS];
+
+    auto gload = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < A_LOADS; ++i) {
+            int v = tid + i * NT;
+            int c = (v % (TK / VEC)) * VEC;
+#if AMODE == 2
+            // K index k0 + c lies in filter tap (r, s) = divmod(k0 / C, S).
+            int tap = k0 / CV_C, ch = k0 % CV_C + c;
+            int ih = a_p[i] + tap / CV_S - CV_PAD, iw = a_q[i] + tap % CV_S - CV_PAD;
+            bool ok = aval[i] && ih >= 0 && ih < CV_H && iw >= 0 && iw < CV_W;
+            const bf16_t *src = args.A + (((size_t)a_n[i] * CV_H + (ok ? ih : 0)) * CV_W + (ok ? iw : 0)) * CV_C + ch;
+            ra[i] = ok ? *(const vecT *)src : (vecT)0;
+#else
+            ra[i] = aval[i] ? *(const vecT *)(arow[i] + k0 + c) : (vecT)0;
+#endif
+        }
+#pragma unroll
+        for (int i = 0; i < B_LOADS; ++i) {
+            int v = tid + i * NT;
+#if LAYOUT == 1
+            int r = v / (TK / VEC), c = (v % (TK / VEC)) * VEC;
+            size_t off = (size_t)(n0 + r) * GK + k0 + c;
+#else
+            int r = v / (TN / VEC), c = (v % (TN / VEC)) * VEC;
+            size_t off = (size_t)(k0 + r) * GN + n0 + c;
+#endif
+            rb[0][i] = *(const vecT *)(B0 + off);
+#if NB == 2
+            rb[1][i] = *(const vecT *)(B1 + off);
+#endif
+        }
+    };
+
+    auto swrite = [&](int s) {
+#pragma unroll
+        for (int i = 0; i < A_LOADS; ++i) {
+            int v = tid + i * NT;
+            int r = v / (TK / VEC), c = (v % (TK / VEC)) * VEC;
+            lds_store_vec(As[s], swz(r, c >> 3) + (c & 7), ra[i]);
+        }
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int i = 0; i < B_LOADS; ++i) {
+                int v = tid + i * NT;
+#if LAYOUT == 1
+                int r = v / (TK / VEC), c = (v % (TK / VEC)) * VEC;
+                lds_store_vec(Bs[s][b], swz(r, c >> 3) + (c & 7), rb[b][i]);
+#else
+                int kr = v / (TN / VEC), c = (v % (TN / VEC)) * VEC;
+#pragma unroll
+                for (int j = 0; j < VEC; ++j)
+                    Bs[s][b][swz(c + j, kr >> 3) + (kr & 7)] = vec_elem(rb[b][i], j);
+#endif
+            }
+    };
+
+    auto compute = [&](int s) {
+#pragma unroll
+        for (int ks = 0; ks < TK / KSTEP; ++ks) {
+            const int chunk = ks * (KSTEP / 8) + lane / MF;
+            bf16x8 af[FM], bfr[NB][FN];
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+                af[i] = *(const bf16x8 *)(As[s] + swz(wm * WTM + i * MF + lane % MF, chunk));
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    bfr[b][j] = *(const bf16x8 *)(Bs[s][b] + swz(wn * WTN + j * MF + lane % MF, chunk));
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < FN; ++j) acc[b][i][j] = mfma(bfr[b][j], af[i], acc[b][i][j]);
+        }
+    };
+
+#if STAGES == 1
+#pragma unroll UNROLL
+    for (int kt = 0; kt < KTILES; ++kt) {
+        gload(kt * TK);
+        swrite(0);
+        __syncthreads();
+        compute(0);
+        __syncthreads();
+    }
+#else
+    gload(0);
+    swrite(0);
+    __syncthreads();
+#pragma unroll UNROLL
+    for (int kt = 0; kt < KTILES; ++kt) {
+        if (kt + 1 < KTILES) gload((kt + 1) * TK);
+        compute(kt & 1);
+        if (kt + 1 < KTILES) swrite((kt + 1) & 1);
+        __syncthreads();
+    }
+#endif
+
+    // ---- epilogue --------------------------------------------------------
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int mloc = wm * WTM + i * MF + lane % MF;
+        if (mloc >= rows_valid) continue;
+        const size_t orow = (size_t)(row_base + mloc) * GN;
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+#pragma unroll
+            for (int g = 0; g < ACCN / 4; ++g) {
+                // columns n .. n+3 of this lane's row
+#if MF == 16
+                const int n = n0 + wn * WTN + j * MF + 4 * (lane >> 4);
+#else
+                const int n = n0 + wn * WTN + j * MF + g * 8 + 4 * (lane >> 5);
+#endif
+                float v[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] = acc[0][i][j][g * 4 + r];
+#if EPI == 3
+                *(f32x4 *)((float *)args.C + orow + n) = f32x4{v[0], v[1], v[2], v[3]};
+#if NB == 2
+                *(f32x4 *)((float *)args.C1 + orow + n) =
+                    f32x4{acc[1][i][j][g * 4 + 0], acc[1][i][j][g * 4 + 1], acc[1][i][j][g * 4 + 2],
+                          acc[1][i][j][g * 4 + 3]};
+#endif
+#else
+#if EPI == 1
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] = silu(v[r] + args.bias[n + r]);
+#elif EPI == 2
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] = silu(v[r]) * acc[1][i][j][g * 4 + r];
+#endif
+                u32x2 packed;
+                packed[0] = (unsigned)f2bf(v[0]) | ((unsigned)f2bf(v[1]) << 16);
+                packed[1] = (unsigned)f2bf(v[2]) | ((unsigned)f2bf(v[3]) << 16);
+                *(u32x2 *)((bf16_t *)args.C + orow + n) = packed;
+#endif
+            }
+        }
+    }
+}

@@ -1,0 +1,539 @@
+// Operator descriptors, knob tables, legality, transformations and the
+// FLOP / byte model.  Host-only code; no GPU access.
+//
+// The search space follows the paper's formulation (Sec. 2, Eq. 1): a
+// program variant is reached from P0 by a sequence of transformations, each
+// of which preserves semantics.  Here a variant is a vector of knob values
+// and a transformation sets one knob.  The knob classes are the
+// transformation names of App. A (TileSize, Parallel, ComputeLocation,
+// Unroll) plus the vectorisation and layout changes named in Sec. 1.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "rc_internal.h"
+
+namespace rc {
+
+static thread_local std::string g_err;
+
+rc_status fail(rc_status s, const std::string &msg) {
+    g_err = msg;
+    return s;
+}
+void clear_error() { g_err.clear(); }
+
+static std::vector<KnobDef> gemm_f32_knobs() {
+    return {
+        {"tile_m", "TileSize", {16, 32, 64}, 16},
+        {"tile_n", "TileSize", {16, 32, 64}, 16},
+        {"tile_k", "TileSize", {4, 8, 16, 32}, 4},
+        {"waves_m", "Parallel", {1, 2}, 1},
+        {"waves_n", "Parallel", {1, 2}, 1},
+        {"vec", "Vectorize", {1, 4}, 1},
+        {"stages", "ComputeLocation", {1, 2}, 1},
+        {"unroll", "Unroll", {1, 2, 4}, 1},
+        {"layout", "Layout", {0, 1}, 0},
+    };
+}
+
+// One bf16 GEMM stage's knobs, names prefixed ("" / "up." / "down.").
+static void add_gemm_block(std::vector<KnobDef> &v, const char *const names[11],
+                           std::vector<int32_t> tile_n_vals, std::vector<int32_t> tile_k_vals) {
+    v.push_back({names[0], "TileSize", {16, 32, 64, 128, 256}, 16});
+    v.push_back({names[1], "TileSize", tile_n_vals, 16});
+    v.push_back({names[2], "TileSize", tile_k_vals, 32});
+    v.push_back({names[3], "Parallel", {1, 2, 4}, 1});
+    v.push_back({names[4], "Parallel", {1, 2, 4}, 1});
+    v.push_back({names[5], "TileSize", {16, 32}, 16});          // MFMA instruction shape
+    v.push_back({names[6], "ComputeLocation", {1, 2}, 1});      // LDS stages
+    v.push_back({names[7], "Vectorize", {2, 4, 8}, 2});         // bf16 per global load
+    v.push_back({names[8], "Unroll", {1, 2}, 1});
+    v.push_back({names[9], "Layout", {0, 1}, 0});               // weight stored KxN / NxK
+    v.push_back({names[10], "Parallel", {0, 1}, 0});            // tile order: plain / XCD-grouped
+}
+
+static const char *const PLAIN[11] = {"tile_m", "tile_n", "tile_k", "waves_m", "waves_n", "mfma",
+                                      "stages", "vec", "unroll", "layout", "grid"};
+static const char *const UP[11] = {"up.tile_m", "up.tile_n", "up.tile_k", "up.waves_m",
+                                   "up.waves_n", "up.mfma", "up.stages", "up.vec", "up.unroll",
+                                   "up.layout", "up.grid"};
+static const char *const DOWN[11] = {"down.tile_m", "down.tile_n", "down.tile_k", "down.waves_m",
+                                     "down.waves_n", "down.mfma", "down.stages", "down.vec",
+                                     "down.unroll", "down.layout", "down.grid"};
+
+static std::vector<KnobDef> mlp_knobs() {
+    std::vector<KnobDef> v;
+    add_gemm_block(v, UP, {16, 32, 64, 128, 256}, {32, 64, 128});
+    add_gemm_block(v, DOWN, {16, 32, 64, 128, 256}, {32, 64, 128});
+    v.push_back({"fuse", "ComputeLocation", {0, 1}, 0});
+    return v;
+}
+
+static std::vector<KnobDef> moe_knobs() { return mlp_knobs(); }
+
+static std::vector<KnobDef> conv_knobs() {
+    std::vector<KnobDef> v;
+    add_gemm_block(v, PLAIN, {16, 32, 64, 80, 128, 160, 256, 320}, {32, 64, 128});
+    v.push_back({"fuse", "ComputeLocation", {0, 1}, 0});
+    return v;
+}
+
+static std::vector<KnobDef> attention_knobs() {
+    return {
+        {"block_m", "TileSize", {16, 32, 64, 128, 256}, 16},
+        {"block_n", "TileSize", {32, 64, 128}, 32},
+        {"waves", "Parallel", {1, 2, 4, 8}, 1},
+        {"mfma", "TileSize", {16, 32}, 16},
+        {"stages", "ComputeLocation", {1, 2}, 1},
+        {"vec", "Vectorize", {2, 4, 8}, 2},
+        {"unroll", "Unroll", {1, 2}, 1},
+        {"order", "Parallel", {0, 1}, 0},
+    };
+}
+
+const std::vector<KnobDef> &knobs_for(int32_t kind) {
+    static const std::vector<KnobDef> empty;
+    static const std::vector<KnobDef> g = gemm_f32_knobs();
+    static const std::vector<KnobDef> a = attention_knobs();
+    static const std::vector<KnobDef> m = mlp_knobs();
+    static const std::vector<KnobDef> e = moe_knobs();
+    static const std::vector<KnobDef> c = conv_knobs();
+    switch (kind) {
+        case RC_OP_GEMM_F32: return g;
+        case RC_OP_ATTENTION: return a;
+        case RC_OP_GATED_MLP: return m;
+        case RC_OP_MOE: return e;
+        case RC_OP_CONV2D: return c;
+        default: return empty;
+    }
+}
+
+int knob_index(int32_t kind, const char *name) {
+    const auto &k = knobs_for(kind);
+    for (size_t i = 0; i < k.size(); ++i)
+        if (std::strcmp(k[i].name, name) == 0) return (int)i;
+    return -1;
+}
+
+static int expected_dims(int32_t kind) {
+    switch (kind) {
+        case RC_OP_GEMM_F32: return 3;
+        case RC_OP_ATTENTION: return 4;
+        case RC_OP_GATED_MLP: return 3;
+        case RC_OP_MOE: return 5;
+        case RC_OP_CONV2D: return 8;
+        default: return -1;
+    }
+}
+
+bool desc_ok(const rc_op_desc *d) {
+    if (!d || d->struct_size < sizeof(rc_op_desc)) return false;
+    int nd = expected_dims(d->kind);
+    if (nd < 0) return false;
+    for (int i = 0; i < nd; ++i) {
+        bool pad = (d->kind == RC_OP_CONV2D && i == 7);
+        if (pad ? d->dim[i] < 0 : d->dim[i] <= 0) return false;
+    }
+    return true;
+}
+
+int32_t kv(const rc_op_desc *d, const rc_schedule *s, const char *name) {
+    int i = knob_index(d->kind, name);
+    return i < 0 ? -1 : s->knob[i];
+}
+
+static std::string fmt(const char *f, ...) {
+    char buf[256];
+    va_list ap;
+    va_start(ap, f);
+    vsnprintf(buf, sizeof buf, f, ap);
+    va_end(ap);
+    return buf;
+}
+
+static const int64_t LDS_LIMIT = 163840;   // bytes one workgroup may allocate on gfx950
+
+// Rules for one bf16 GEMM stage of shape M x N x K (M < 0: ragged rows,
+// predicated), NB weight operands sharing the A tile.
+static std::string check_bf16_block(const rc_op_desc *d, const rc_schedule *s,
+                                    const char *const names[11], int64_t M, int64_t N, int64_t K,
+                                    int NB, const char *tag) {
+    int tm = kv(d, s, names[0]), tn = kv(d, s, names[1]), tk = kv(d, s, names[2]);
+    int wm = kv(d, s, names[3]), wn = kv(d, s, names[4]), mf = kv(d, s, names[5]);
+    int st = kv(d, s, names[6]), vec = kv(d, s, names[7]), un = kv(d, s, names[8]);
+    int lay = kv(d, s, names[9]);
+    (void)st;
+    int nt = 64 * wm * wn;
+    if (tm % wm || (tm / wm) % mf)
+        return fmt("%s: tile_m/waves_m = %d/%d is not a multiple of the %dx%d MFMA", tag, tm, wm,
+                   mf, mf);
+    if (tn % wn || (tn / wn) % mf)
+        return fmt("%s: tile_n/waves_n = %d/%d is not a multiple of the %dx%d MFMA", tag, tn, wn,
+                   mf, mf);
+    if (tk % 32) return fmt("%s: tile_k %d is not a multiple of 32", tag, tk);
+    if (M > 0 && M % tm) return fmt("%s: tile_m %d does not divide M = %lld", tag, tm, (long long)M);
+    if (N % tn) return fmt("%s: tile_n %d does not divide N = %lld", tag, tn, (long long)N);
+    if (K % tk) return fmt("%s: tile_k %d does not divide K = %lld", tag, tk, (long long)K);
+    if ((int64_t)tm * tk % ((int64_t)vec * nt))
+        return fmt("%s: A tile %dx%d does not split into %d threads x %d-wide loads", tag, tm, tk,
+                   nt, vec);
+    if ((int64_t)tn * tk % ((int64_t)vec * nt))
+        return fmt("%s: B tile %dx%d does not split into %d threads x %d-wide loads", tag, tk, tn,
+                   nt, vec);
+    if (lay == 0 && tn % vec) return fmt("%s: vec %d does not divide tile_n %d", tag, vec, tn);
+    int64_t lds = (int64_t)st * ((int64_t)tm * tk + (int64_t)NB * tn * tk) * 2;
+    if (lds > LDS_LIMIT)
+        return fmt("%s: LDS %lld B exceeds %lld B", tag, (long long)lds, (long long)LDS_LIMIT);
+    int64_t acc = (int64_t)NB * tm * tn / nt;
+    if (acc > 256) return fmt("%s: %lld accumulators per lane exceed 256", tag, (long long)acc);
+    int64_t stage_regs = st > 1 ? ((int64_t)tm * tk + (int64_t)NB * tn * tk) / (2 * nt) : 0;
+    if (acc + stage_regs > 384)
+        return fmt("%s: %lld accumulator + %lld staging registers per lane exceed 384", tag,
+                   (long long)acc, (long long)stage_regs);
+    if ((K / tk) % un) return fmt("%s: unroll %d does not divide %lld K tiles", tag, un,
+                                  (long long)(K / tk));
+    return "";
+}
+
+std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
+    const auto &kt = knobs_for(d->kind);
+    if (s->struct_size < sizeof(rc_schedule)) return "schedule struct_size too small";
+    if (s->nknobs != (int32_t)kt.size()) return fmt("schedule has %d knobs, operator has %d",
+                                                    s->nknobs, (int)kt.size());
+    for (size_t i = 0; i < kt.size(); ++i) {
+        bool found = false;
+        for (int32_t v : kt[i].values) found |= (v == s->knob[i]);
+        if (!found) return fmt("knob %s = %d is not an allowed value", kt[i].name, s->knob[i]);
+    }
+    const int64_t *D = d->dim;
+    switch (d->kind) {
+        case RC_OP_GEMM_F32: {
+            int tm = kv(d, s, "tile_m"), tn = kv(d, s, "tile_n"), tk = kv(d, s, "tile_k");
+            int wm = kv(d, s, "waves_m"), wn = kv(d, s, "waves_n"), vec = kv(d, s, "vec");
+            int st = kv(d, s, "stages"), un = kv(d, s, "unroll"), lay = kv(d, s, "layout");
+            int64_t M = D[0], N = D[1], K = D[2];
+            int nt = 64 * wm * wn;
+            if ((tm / wm) % 16 || tm % wm) return fmt("tile_m/waves_m = %d/%d is not a multiple of 16", tm, wm);
+            if ((tn / wn) % 16 || tn % wn) return fmt("tile_n/waves_n = %d/%d is not a multiple of 16", tn, wn);
+            if (M % tm) return fmt("tile_m %d does not divide M = %lld", tm, (long long)M);
+            if (N % tn) return fmt("tile_n %d does not divide N = %lld", tn, (long long)N);
+            if (K % tk) return fmt("tile_k %d does not divide K = %lld", tk, (long long)K);
+            if ((tm * tk) % (vec * nt))
+                return fmt("A tile %dx%d does not split into %d threads x %d-wide loads", tm, tk, nt, vec);
+            if ((tk * tn) % (vec * nt))
+                return fmt("B tile %dx%d does not split into %d threads x %d-wide loads", tk, tn, nt, vec);
+            if (tk % vec) return fmt("vec %d does not divide tile_k %d", vec, tk);
+            if (lay == 0 && tn % vec) return fmt("vec %d does not divide tile_n %d", vec, tn);
+            if ((K / tk) % un) return fmt("unroll %d does not divide the %lld K tiles", un, (long long)(K / tk));
+            int64_t lds = (int64_t)st * (tm * (tk + 1) + tk * (tn + 1)) * 4;
+            if (lds > LDS_LIMIT) return fmt("LDS %lld B exceeds limit", (long long)lds);
+            return "";
+        }
+        case RC_OP_ATTENTION: {
+            int bm = kv(d, s, "block_m"), bn = kv(d, s, "block_n"), w = kv(d, s, "waves");
+            int mf = kv(d, s, "mfma"), st = kv(d, s, "stages");
+            int64_t S = D[2], Dh = D[3];
+            if (bm % w) return fmt("block_m %d is not divisible by waves %d", bm, w);
+            int rpw = bm / w;
+            if (rpw % mf) return fmt("rows per wave %d is not a multiple of the %dx%d MFMA", rpw, mf, mf);
+            if (rpw / mf > 2) return fmt("rows per wave %d exceeds two MFMA blocks", rpw);
+            if (bn % 32) return fmt("block_n %d is not a multiple of 32", bn);
+            if (S % bm) return fmt("block_m %d does not divide S = %lld", bm, (long long)S);
+            if (S % bn) return fmt("block_n %d does not divide S = %lld", bn, (long long)S);
+            // the K tile's LDS swizzle XORs 16-byte chunk indices, so a row
+            // must hold a power-of-two number of chunks
+            if (Dh != 32 && Dh != 64 && Dh != 128 && Dh != 256)
+                return fmt("head dim %lld must be 32, 64, 128 or 256", (long long)Dh);
+            int64_t lds = (int64_t)st * (2 * bn * (Dh + 8) * 2);
+            if (lds > LDS_LIMIT) return fmt("LDS %lld B exceeds limit", (long long)lds);
+            int64_t regs = (int64_t)rpw * Dh / 64 + (int64_t)bn * rpw / 64 + (int64_t)rpw * Dh / 128;
+            if (regs > 320) return fmt("%lld registers per lane for O, S and Q exceed 320", (long long)regs);
+            return "";
+        }
+        case RC_OP_GATED_MLP: {
+            int64_t T = D[0], Hd = D[1], I = D[2];
+            std::string r = check_bf16_block(d, s, UP, T, I, Hd, 2, "up");
+            if (!r.empty()) return r;
+            return check_bf16_block(d, s, DOWN, T, Hd, I, 1, "down");
+        }
+        case RC_OP_MOE: {
+            int64_t Hd = D[1], E = D[2], I = D[3], topk = D[4];
+            if (topk > E) return "topk exceeds the number of experts";
+            std::string r = check_bf16_block(d, s, UP, -1, I, Hd, 2, "up");
+            if (!r.empty()) return r;
+            return check_bf16_block(d, s, DOWN, -1, Hd, I, 1, "down");
+        }
+        case RC_OP_CONV2D: {
+            int64_t N = D[0], H = D[1], W = D[2], C = D[3], K = D[4], R = D[5], S = D[6], pad = D[7];
+            int64_t P = H + 2 * pad - R + 1, Q = W + 2 * pad - S + 1;
+            if (P <= 0 || Q <= 0) return "empty output";
+            int tk = kv(d, s, "tile_k");
+            if (C % tk) return fmt("tile_k %d does not divide C = %lld (a K tile must stay in one filter tap)", tk, (long long)C);
+            return check_bf16_block(d, s, PLAIN, N * P * Q, K, R * S * C, 1, "conv");
+        }
+    }
+    return "unknown operator kind";
+}
+
+}  // namespace rc
+
+using namespace rc;
+
+extern "C" {
+
+const char *rc_status_str(rc_status s) {
+    switch (s) {
+        case RC_OK: return "RC_OK";
+        case RC_ERR_INVALID_ARGUMENT: return "RC_ERR_INVALID_ARGUMENT";
+        case RC_ERR_ILLEGAL_SCHEDULE: return "RC_ERR_ILLEGAL_SCHEDULE";
+        case RC_ERR_UNSUPPORTED: return "RC_ERR_UNSUPPORTED";
+        case RC_ERR_COMPILE: return "RC_ERR_COMPILE";
+        case RC_ERR_HIP: return "RC_ERR_HIP";
+        case RC_ERR_OUT_OF_MEMORY: return "RC_ERR_OUT_OF_MEMORY";
+        case RC_ERR_MISALIGNED: return "RC_ERR_MISALIGNED";
+        case RC_ERR_BUDGET: return "RC_ERR_BUDGET";
+    }
+    return "RC_ERR_UNKNOWN";
+}
+
+const char *rc_last_error(void) { return g_err.c_str(); }
+
+rc_status rc_op_init(rc_op_desc *d, int32_t kind, const int64_t *dims, int32_t ndims,
+                     int32_t flags) {
+    if (!d || !dims) return fail(RC_ERR_INVALID_ARGUMENT, "null descriptor or dims");
+    int nd = expected_dims(kind);
+    if (nd < 0) return fail(RC_ERR_UNSUPPORTED, "unknown operator kind");
+    if (ndims != nd) return fail(RC_ERR_INVALID_ARGUMENT, fmt("kind %d takes %d dims, got %d", kind, nd, ndims));
+    rc_op_desc t;
+    std::memset(&t, 0, sizeof t);
+    t.struct_size = sizeof(rc_op_desc);
+    t.kind = kind;
+    for (int i = 0; i < nd; ++i) t.dim[i] = dims[i];
+    t.flags = flags;
+    if (!desc_ok(&t)) return fail(RC_ERR_INVALID_ARGUMENT, "dimensions must be positive");
+    if (kind == RC_OP_MOE && t.dim[4] > t.dim[2])
+        return fail(RC_ERR_INVALID_ARGUMENT, "topk exceeds the number of experts");
+    *d = t;
+    clear_error();
+    return RC_OK;
+}
+
+double rc_op_flops(const rc_op_desc *d) {
+    if (!desc_ok(d)) return -1.0;
+    const int64_t *D = d->dim;
+    switch (d->kind) {
+        case RC_OP_GEMM_F32: return 2.0 * D[0] * D[1] * D[2];
+        case RC_OP_ATTENTION: {
+            double S = (double)D[2];
+            double pairs = (d->flags & RC_FLAG_CAUSAL) ? S * (S + 1) / 2 : S * S;
+            return 4.0 * D[3] * D[0] * D[1] * pairs;
+        }
+        case RC_OP_GATED_MLP: return 6.0 * D[0] * D[1] * D[2];
+        case RC_OP_MOE: return 6.0 * D[0] * D[4] * D[1] * D[3];
+        case RC_OP_CONV2D: {
+            double P = D[1] + 2 * D[7] - D[5] + 1, Q = D[2] + 2 * D[7] - D[6] + 1;
+            return 2.0 * D[0] * P * Q * D[4] * D[5] * D[6] * D[3];
+        }
+    }
+    return -1.0;
+}
+
+double rc_op_bytes(const rc_op_desc *d) {
+    if (!desc_ok(d)) return -1.0;
+    const int64_t *D = d->dim;
+    switch (d->kind) {
+        case RC_OP_GEMM_F32: return 4.0 * (D[0] * D[2] + D[2] * D[1] + D[0] * D[1]);
+        case RC_OP_ATTENTION: return 2.0 * 4 * D[0] * D[1] * D[2] * D[3];
+        case RC_OP_GATED_MLP: return 2.0 * (2 * D[0] * D[1] + 3 * D[1] * D[2]);
+        case RC_OP_MOE:
+            return 2.0 * (2 * D[0] * D[1] + 3 * D[2] * D[1] * D[3]) + 8.0 * D[0] * D[4];
+        case RC_OP_CONV2D: {
+            double P = D[1] + 2 * D[7] - D[5] + 1, Q = D[2] + 2 * D[7] - D[6] + 1;
+            return 2.0 * D[0] * D[1] * D[2] * D[3] + 2.0 * D[4] * D[5] * D[6] * D[3] + 4.0 * D[4] +
+                   2.0 * D[0] * P * Q * D[4];
+        }
+    }
+    return -1.0;
+}
+
+double rc_peak_flops(const rc_op_desc *d) {
+    if (!desc_ok(d)) return -1.0;
+    return d->kind == RC_OP_GEMM_F32 ? 157.3e12 : 2516.6e12;
+}
+
+double rc_peak_bytes_per_s(void) { return 8.0e12; }
+
+int32_t rc_knob_count(const rc_op_desc *d) {
+    if (!desc_ok(d)) return -1;
+    return (int32_t)knobs_for(d->kind).size();
+}
+
+const char *rc_knob_name(const rc_op_desc *d, int32_t knob) {
+    if (!desc_ok(d)) return nullptr;
+    const auto &k = knobs_for(d->kind);
+    return (knob >= 0 && knob < (int32_t)k.size()) ? k[knob].name : nullptr;
+}
+
+const char *rc_knob_class(const rc_op_desc *d, int32_t knob) {
+    if (!desc_ok(d)) return nullptr;
+    const auto &k = knobs_for(d->kind);
+    return (knob >= 0 && knob < (int32_t)k.size()) ? k[knob].xform : nullptr;
+}
+
+rc_status rc_knob_values(const rc_op_desc *d, int32_t knob, int32_t *vals, int32_t cap,
+                         int32_t *n) {
+    if (!desc_ok(d) || !n) return fail(RC_ERR_INVALID_ARGUMENT, "bad descriptor");
+    const auto &k = knobs_for(d->kind);
+    if (knob < 0 || knob >= (int32_t)k.size()) return fail(RC_ERR_INVALID_ARGUMENT, "bad knob");
+    *n = (int32_t)k[knob].values.size();
+    for (int32_t i = 0; i < *n && i < cap && vals; ++i) vals[i] = k[knob].values[i];
+    return RC_OK;
+}
+
+rc_status rc_default_schedule(const rc_op_desc *d, rc_schedule *out) {
+    if (!desc_ok(d) || !out) return fail(RC_ERR_INVALID_ARGUMENT, "bad descriptor");
+    rc_schedule s;
+    std::memset(&s, 0, sizeof s);
+    s.struct_size = sizeof(rc_schedule);
+    const auto &k = knobs_for(d->kind);
+    s.nknobs = (int32_t)k.size();
+    for (size_t i = 0; i < k.size(); ++i) s.knob[i] = k[i].def;
+    std::string why = check_schedule(d, &s);
+    if (!why.empty()) return fail(RC_ERR_UNSUPPORTED, "operator shape admits no default schedule: " + why);
+    *out = s;
+    return RC_OK;
+}
+
+rc_status rc_validate(const rc_op_desc *d, const rc_schedule *s, char *why, size_t why_len) {
+    if (!desc_ok(d) || !s) return fail(RC_ERR_INVALID_ARGUMENT, "bad descriptor or schedule");
+    std::string r = check_schedule(d, s);
+    if (why && why_len) {
+        std::strncpy(why, r.c_str(), why_len - 1);
+        why[why_len - 1] = 0;
+    }
+    if (!r.empty()) return fail(RC_ERR_ILLEGAL_SCHEDULE, r);
+    return RC_OK;
+}
+
+rc_status rc_apply(const rc_op_desc *d, const rc_schedule *in, const rc_transform *t,
+                   rc_schedule *out) {
+    if (!desc_ok(d) || !in || !t || !out) return fail(RC_ERR_INVALID_ARGUMENT, "null argument");
+    if (t->knob < 0 || t->knob >= in->nknobs || in->nknobs > RC_MAX_KNOBS)
+        return fail(RC_ERR_INVALID_ARGUMENT, "knob index out of range");
+    rc_schedule s = *in;
+    s.knob[t->knob] = t->value;
+    std::string r = check_schedule(d, &s);
+    if (!r.empty()) return fail(RC_ERR_ILLEGAL_SCHEDULE, r);
+    *out = s;
+    return RC_OK;
+}
+
+rc_status rc_enumerate(const rc_op_desc *d, const rc_schedule *at, rc_transform *buf, size_t cap,
+                       size_t *n) {
+    if (!desc_ok(d) || !at || !n) return fail(RC_ERR_INVALID_ARGUMENT, "null argument");
+    const auto &k = knobs_for(d->kind);
+    if (at->nknobs != (int32_t)k.size()) return fail(RC_ERR_INVALID_ARGUMENT, "knob count mismatch");
+    size_t cnt = 0;
+    for (size_t i = 0; i < k.size(); ++i) {
+        for (int32_t v : k[i].values) {
+            if (v == at->knob[i]) continue;
+            rc_schedule s = *at;
+            s.knob[i] = v;
+            if (!check_schedule(d, &s).empty()) continue;
+            if (buf && cnt < cap) buf[cnt] = rc_transform{(int32_t)i, v};
+            ++cnt;
+        }
+    }
+    *n = cnt;
+    return RC_OK;
+}
+
+rc_status rc_parse_transform(const rc_op_desc *d, const char *text, rc_transform *out) {
+    if (!desc_ok(d) || !text || !out) return fail(RC_ERR_INVALID_ARGUMENT, "null argument");
+    // Form: Class(knob=value), whitespace tolerated.
+    std::string s;
+    for (const char *p = text; *p; ++p)
+        if (*p != ' ' && *p != '\t' && *p != '\n' && *p != '\r') s += *p;
+    size_t lp = s.find('('), eq = s.find('='), rp = s.find(')');
+    if (lp == std::string::npos || eq == std::string::npos || rp == std::string::npos || !(lp < eq && eq < rp) ||
+        rp != s.size() - 1)
+        return fail(RC_ERR_INVALID_ARGUMENT, "expected Class(knob=value)");
+    std::string cls = s.substr(0, lp), name = s.substr(lp + 1, eq - lp - 1),
+                val = s.substr(eq + 1, rp - eq - 1);
+    int ki = knob_index(d->kind, name.c_str());
+    if (ki < 0) return fail(RC_ERR_INVALID_ARGUMENT, "unknown knob " + name);
+    const KnobDef &kd = knobs_for(d->kind)[ki];
+    if (cls != kd.xform) return fail(RC_ERR_INVALID_ARGUMENT, "knob " + name + " is not a " + cls + " knob");
+    if (val.empty()) return fail(RC_ERR_INVALID_ARGUMENT, "missing value");
+    char *end = nullptr;
+    long v = std::strtol(val.c_str(), &end, 10);
+    if (*end) return fail(RC_ERR_INVALID_ARGUMENT, "value is not an integer");
+    bool allowed = false;
+    for (int32_t a : kd.values) allowed |= (a == v);
+    if (!allowed) return fail(RC_ERR_INVALID_ARGUMENT, "value not allowed for " + name);
+    *out = rc_transform{ki, (int32_t)v};
+    return RC_OK;
+}
+
+rc_status rc_schedule_to_string(const rc_op_desc *d, const rc_schedule *s, char *buf, size_t len) {
+    if (!desc_ok(d) || !s || !buf || !len) return fail(RC_ERR_INVALID_ARGUMENT, "null argument");
+    const auto &k = knobs_for(d->kind);
+    if (s->nknobs != (int32_t)k.size()) return fail(RC_ERR_INVALID_ARGUMENT, "knob count mismatch");
+    std::string r;
+    for (size_t i = 0; i < k.size(); ++i) {
+        if (i) r += ',';
+        r += k[i].name;
+        r += '=';
+        r += std::to_string(s->knob[i]);
+    }
+    if (r.size() + 1 > len) return fail(RC_ERR_INVALID_ARGUMENT, "buffer too small");
+    std::memcpy(buf, r.c_str(), r.size() + 1);
+    return RC_OK;
+}
+
+rc_status rc_schedule_from_string(const rc_op_desc *d, const char *text, rc_schedule *out) {
+    if (!desc_ok(d) || !text || !out) return fail(RC_ERR_INVALID_ARGUMENT, "null argument");
+    rc_schedule s;
+    std::memset(&s, 0, sizeof s);
+    s.struct_size = sizeof s;
+    const auto &k = knobs_for(d->kind);
+    s.nknobs = (int32_t)k.size();
+    for (size_t i = 0; i < k.size(); ++i) s.knob[i] = k[i].def;
+    std::string t(text);
+    size_t pos = 0;
+    while (pos < t.size()) {
+        size_t comma = t.find(',', pos);
+        if (comma == std::string::npos) comma = t.size();
+        std::string item = t.substr(pos, comma - pos);
+        pos = comma + 1;
+        if (item.empty()) continue;
+        size_t eq = item.find('=');
+        if (eq == std::string::npos) return fail(RC_ERR_INVALID_ARGUMENT, "expected name=value");
+        int ki = knob_index(d->kind, item.substr(0, eq).c_str());
+        if (ki < 0) return fail(RC_ERR_INVALID_ARGUMENT, "unknown knob " + item.substr(0, eq));
+        char *end = nullptr;
+        long v = std::strtol(item.c_str() + eq + 1, &end, 10);
+        if (*end || end == item.c_str() + eq + 1) return fail(RC_ERR_INVALID_ARGUMENT, "bad value in " + item);
+        s.knob[ki] = (int32_t)v;
+    }
+    *out = s;
+    return RC_OK;
+}
+
+uint64_t rc_schedule_hash(const rc_schedule *s) {
+    if (!s) return 0;
+    uint64_t h = 1469598103934665603ULL;   // FNV-1a over the knob values
+    for (int32_t i = 0; i < s->nknobs && i < RC_MAX_KNOBS; ++i) {
+        uint32_t v = (uint32_t)s->knob[i];
+        for (int b = 0; b < 4; ++b) {
+            h ^= (v >> (8 * b)) & 0xFF;
+            h *= 1099511628211ULL;
+        }
+    }
+    return h;
+}
+
+}  // extern "C"

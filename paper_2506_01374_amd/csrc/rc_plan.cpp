@@ -1,0 +1,723 @@
+// Plans: source generation for a schedule, hipRTC compilation with an
+// on-disk code-object cache, module loading, launch and event timing.
+#include <dlfcn.h>
+#include <hip/hip_runtime_api.h>
+#include <hip/hiprtc.h>
+#include <sys/stat.h>
+#include <unistd.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <fstream>
+#include <functional>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <sstream>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "rc_internal.h"
+
+namespace rc {
+#include "kernels_src.inc"   // generated: kernel sources as string literals
+}
+
+using namespace rc;
+
+namespace {
+
+// ---------------------------------------------------------------------
+// Kernel argument blocks; each mirrors the struct its kernel takes by value.
+// ---------------------------------------------------------------------
+struct GemmF32Args {
+    const void *A, *B;
+    void *C;
+};
+struct GemmBf16Args {
+    const void *A, *B0, *B1;
+    void *C, *C1;
+    const void *bias, *perm, *offsets, *tile_start;
+};
+struct EwArgs {
+    const void *G, *U, *bias;
+    void *out;
+};
+struct MoePrepArgs {
+    const void *ids;
+    void *offsets, *perm, *pos, *tile_up, *tile_down;
+};
+struct MoeCombineArgs {
+    const void *Y, *pos, *w;
+    void *out;
+};
+struct AttnArgs {
+    const void *Q, *K, *V;
+    void *O;
+};
+
+struct Source {
+    const char *file;     // kernel source text
+    const char *entry;    // kernel function name
+    std::string defines;  // generated prologue
+};
+
+std::mutex g_mu;
+std::string g_cache_dir;
+std::map<std::string, hipModule_t> g_modules;   // cache-key -> loaded module
+
+uint64_t fnv1a(const std::string &s, uint64_t h = 1469598103934665603ULL) {
+    for (unsigned char c : s) {
+        h ^= c;
+        h *= 1099511628211ULL;
+    }
+    return h;
+}
+
+std::string lib_dir() {
+    Dl_info info;
+    if (dladdr((void *)&fnv1a, &info) && info.dli_fname) {
+        std::string p(info.dli_fname);
+        size_t k = p.rfind('/');
+        if (k != std::string::npos) return p.substr(0, k);
+    }
+    return ".";
+}
+
+const std::vector<std::string> &compile_options() {
+    static const std::vector<std::string> opts = {
+        "--offload-arch=gfx950", "-O3", "-std=c++17",
+        // keep the compiler from forming packed fp32 instructions
+        "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"};
+    return opts;
+}
+
+std::string full_source(const Source &s) { return s.defines + "\n" + s.file; }
+
+std::string cache_key(const Source &s) {
+    std::string k = full_source(s);
+    for (auto &o : compile_options()) k += "\x1f" + o;
+    int maj = 0, min = 0;
+    hiprtcVersion(&maj, &min);
+    k += "\x1fhiprtc" + std::to_string(maj) + "." + std::to_string(min);
+    char hex[32];
+    snprintf(hex, sizeof hex, "%016llx", (unsigned long long)fnv1a(k));
+    return std::string(s.entry) + "_" + hex;
+}
+
+bool read_file(const std::string &path, std::vector<char> &out) {
+    std::ifstream f(path, std::ios::binary);
+    if (!f) return false;
+    out.assign(std::istreambuf_iterator<char>(f), std::istreambuf_iterator<char>());
+    return !out.empty();
+}
+
+void mkdirs(const std::string &dir) {
+    std::string cur;
+    for (size_t i = 0; i < dir.size(); ++i) {
+        cur += dir[i];
+        if (dir[i] == '/' || i + 1 == dir.size()) mkdir(cur.c_str(), 0755);
+    }
+}
+
+// Compile (or fetch from the cache) one kernel source.
+rc_status compile(const Source &s, std::vector<char> &code, std::string &key) {
+    key = cache_key(s);
+    std::string dir = cache_dir();
+    std::string path = dir + "/" + key + ".hsaco";
+    if (read_file(path, code)) return RC_OK;
+    std::string src = full_source(s);
+    hiprtcProgram prog;
+    if (hiprtcCreateProgram(&prog, src.c_str(), (std::string(s.entry) + ".hip").c_str(), 0, nullptr,
+                            nullptr) != HIPRTC_SUCCESS)
+        return fail(RC_ERR_COMPILE, "hiprtcCreateProgram failed");
+    std::vector<const char *> opts;
+    for (auto &o : compile_options()) opts.push_back(o.c_str());
+    hiprtcResult r = hiprtcCompileProgram(prog, (int)opts.size(), opts.data());
+    if (r != HIPRTC_SUCCESS) {
+        size_t n = 0;
+        hiprtcGetProgramLogSize(prog, &n);
+        std::string log(n, '\0');
+        if (n) hiprtcGetProgramLog(prog, &log[0]);
+        hiprtcDestroyProgram(&prog);
+        return fail(RC_ERR_COMPILE, std::string("hipRTC: ") + s.entry + ": " + log.substr(0, 4000));
+    }
+    size_t n = 0;
+    hiprtcGetCodeSize(prog, &n);
+    code.resize(n);
+    hiprtcGetCode(prog, code.data());
+    hiprtcDestroyProgram(&prog);
+    mkdirs(dir);
+    std::string tmp = path + ".tmp" + std::to_string(getpid()) + "_" +
+                      std::to_string(std::hash<std::thread::id>()(std::this_thread::get_id()));
+    {
+        std::ofstream f(tmp, std::ios::binary);
+        f.write(code.data(), (std::streamsize)code.size());
+    }
+    rename(tmp.c_str(), path.c_str());
+    return RC_OK;
+}
+
+// Integer value following a metadata key in the code object's msgpack note.
+long meta_int(const std::vector<char> &code, const char *key) {
+    size_t kl = strlen(key);
+    for (size_t i = 0; i + kl + 1 < code.size(); ++i) {
+        if ((unsigned char)code[i] != (0xa0 | kl) || memcmp(&code[i + 1], key, kl) != 0) continue;
+        size_t j = i + 1 + kl;
+        unsigned char t = (unsigned char)code[j];
+        if (t <= 0x7f) return t;
+        if (t == 0xcc) return (unsigned char)code[j + 1];
+        if (t == 0xcd) return ((unsigned char)code[j + 1] << 8) | (unsigned char)code[j + 2];
+        if (t == 0xce)
+            return ((long)(unsigned char)code[j + 1] << 24) | ((unsigned char)code[j + 2] << 16) |
+                   ((unsigned char)code[j + 3] << 8) | (unsigned char)code[j + 4];
+        return -1;
+    }
+    return -1;
+}
+
+std::string def(const char *name, long long v) {
+    return std::string("#define ") + name + " " + std::to_string(v) + "\n";
+}
+
+// ---------------------------------------------------------------------
+// Plan description: the kernels of one operator execution.
+// ---------------------------------------------------------------------
+struct Kern {
+    Source src;
+    dim3 grid, block;
+    // fills the argument block from the caller's buffers and the workspace
+    std::function<void(const rc_args *, char *ws, std::vector<char> &blob)> bind;
+    hipFunction_t fn = nullptr;
+};
+
+struct WsLayout {
+    size_t total = 0;
+    size_t add(size_t bytes) {
+        size_t off = total;
+        total += (bytes + 255) & ~(size_t)255;
+        return off;
+    }
+};
+
+struct GemmCfg {
+    int tm, tn, tk, wm, wn, mf, st, vec, un, lay, grid;
+};
+
+GemmCfg read_block(const rc_op_desc *d, const rc_schedule *s, const char *prefix) {
+    auto k = [&](const char *n) { return kv(d, s, (std::string(prefix) + n).c_str()); };
+    return GemmCfg{k("tile_m"), k("tile_n"), k("tile_k"), k("waves_m"), k("waves_n"), k("mfma"),
+                   k("stages"), k("vec"), k("unroll"), k("layout"), k("grid")};
+}
+
+std::string gemm_defs(const GemmCfg &g, int nb, int amode, int epi, long gm, long gn, long gk) {
+    std::string s;
+    s += def("TM", g.tm) + def("TN", g.tn) + def("TK", g.tk) + def("WM", g.wm) + def("WN", g.wn);
+    s += def("MF", g.mf) + def("STAGES", g.st) + def("VEC", g.vec) + def("UNROLL", g.un);
+    s += def("LAYOUT", g.lay) + def("GRID", g.grid) + def("NB", nb) + def("AMODE", amode);
+    s += def("EPI", epi) + def("GM", gm) + def("GN", gn) + def("GK", gk);
+    return s;
+}
+
+template <class T>
+void put(std::vector<char> &blob, const T &v) {
+    blob.resize(sizeof(T));
+    memcpy(blob.data(), &v, sizeof(T));
+}
+
+}  // namespace
+
+struct rc_plan {
+    rc_op_desc desc;
+    rc_schedule sched;
+    std::vector<Kern> kerns;
+    size_t workspace = 0;
+    int dominant = 0;
+};
+
+namespace rc {
+
+std::string cache_dir() {
+    std::lock_guard<std::mutex> g(g_mu);
+    if (!g_cache_dir.empty()) return g_cache_dir;
+    const char *e = getenv("RC_CACHE_DIR");
+    if (e && *e) return e;
+    return lib_dir() + "/jit_cache";
+}
+
+}  // namespace rc
+
+namespace {
+
+// Build the kernel list of a plan (no compilation, no GPU).
+rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
+    const int64_t *D = d->dim;
+    WsLayout ws;
+    switch (d->kind) {
+        case RC_OP_GEMM_F32: {
+            int tm = kv(d, s, "tile_m"), tn = kv(d, s, "tile_n");
+            int nt = 64 * kv(d, s, "waves_m") * kv(d, s, "waves_n");
+            Kern k;
+            k.src = Source{SRC_gemm_f32, "rc_gemm_f32", ""};
+            k.src.defines = def("TM", tm) + def("TN", tn) + def("TK", kv(d, s, "tile_k")) +
+                            def("WM", kv(d, s, "waves_m")) + def("WN", kv(d, s, "waves_n")) +
+                            def("VEC", kv(d, s, "vec")) + def("STAGES", kv(d, s, "stages")) +
+                            def("UNROLL", kv(d, s, "unroll")) + def("LAYOUT", kv(d, s, "layout")) +
+                            def("GM", D[0]) + def("GN", D[1]) + def("GK", D[2]);
+            k.grid = dim3((unsigned)(D[1] / tn), (unsigned)(D[0] / tm), 1);
+            k.block = dim3(nt, 1, 1);
+            k.bind = [](const rc_args *a, char *, std::vector<char> &b) {
+                put(b, GemmF32Args{a->in[0], a->in[1], a->out[0]});
+            };
+            p.kerns.push_back(k);
+            p.dominant = 0;
+            break;
+        }
+        case RC_OP_GATED_MLP: {
+            long T = D[0], Hd = D[1], I = D[2];
+            GemmCfg up = read_block(d, s, "up."), dn = read_block(d, s, "down.");
+            int fuse = kv(d, s, "fuse");
+            size_t offH = ws.add((size_t)T * I * 2);
+            size_t offG = 0, offU = 0;
+            if (!fuse) {
+                offG = ws.add((size_t)T * I * 4);
+                offU = ws.add((size_t)T * I * 4);
+            }
+            Kern k1;
+            k1.src = Source{SRC_gemm_bf16, "rc_gemm_bf16", gemm_defs(up, 2, 0, fuse ? 2 : 3, T, I, Hd)};
+            k1.grid = dim3((unsigned)((T / up.tm) * (I / up.tn)), 1, 1);
+            k1.block = dim3(64 * up.wm * up.wn, 1, 1);
+            k1.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
+                if (fuse)
+                    put(b, GemmBf16Args{a->in[0], a->in[1], a->in[2], w + offH, nullptr, nullptr,
+                                        nullptr, nullptr, nullptr});
+                else
+                    put(b, GemmBf16Args{a->in[0], a->in[1], a->in[2], w + offG, w + offU, nullptr,
+                                        nullptr, nullptr, nullptr});
+            };
+            p.kerns.push_back(k1);
+            if (!fuse) {
+                Kern ke;
+                ke.src = Source{SRC_aux, "rc_swiglu_f32", def("EW_N", T * I) + def("EW_COLS", I)};
+                ke.grid = dim3((unsigned)((T * I / 4 + 255) / 256), 1, 1);
+                ke.block = dim3(256, 1, 1);
+                ke.bind = [=](const rc_args *, char *w, std::vector<char> &b) {
+                    put(b, EwArgs{w + offG, w + offU, nullptr, w + offH});
+                };
+                p.kerns.push_back(ke);
+            }
+            Kern k2;
+            k2.src = Source{SRC_gemm_bf16, "rc_gemm_bf16", gemm_defs(dn, 1, 0, 0, T, Hd, I)};
+            k2.grid = dim3((unsigned)((T / dn.tm) * (Hd / dn.tn)), 1, 1);
+            k2.block = dim3(64 * dn.wm * dn.wn, 1, 1);
+            k2.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
+                put(b, GemmBf16Args{w + offH, a->in[3], nullptr, a->out[0], nullptr, nullptr,
+                                    nullptr, nullptr, nullptr});
+            };
+            p.kerns.push_back(k2);
+            p.dominant = 0;
+            break;
+        }
+        case RC_OP_MOE: {
+            long T = D[0], Hd = D[1], E = D[2], I = D[3], topk = D[4], R = T * topk;
+            GemmCfg up = read_block(d, s, "up."), dn = read_block(d, s, "down.");
+            int fuse = kv(d, s, "fuse");
+            size_t offOff = ws.add((E + 1) * 4), offPerm = ws.add(R * 4), offPos = ws.add(R * 4);
+            size_t offTu = ws.add((E + 1) * 4), offTd = ws.add((E + 1) * 4);
+            size_t offH = ws.add((size_t)R * I * 2), offY = ws.add((size_t)R * Hd * 2);
+            size_t offG = 0, offU = 0;
+            if (!fuse) {
+                offG = ws.add((size_t)R * I * 4);
+                offU = ws.add((size_t)R * I * 4);
+            }
+            std::string moe = def("MOE_T", T) + def("MOE_TOPK", topk) + def("MOE_E", E) +
+                              def("MOE_H", Hd) + def("MOE_TM_UP", up.tm) + def("MOE_TM_DOWN", dn.tm);
+            Kern k0;
+            k0.src = Source{SRC_aux, "rc_moe_prep", moe};
+            k0.grid = dim3((unsigned)E, 1, 1);
+            k0.block = dim3(256, 1, 1);
+            k0.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
+                put(b, MoePrepArgs{a->in[1], w + offOff, w + offPerm, w + offPos, w + offTu, w + offTd});
+            };
+            p.kerns.push_back(k0);
+            std::string mdefs = def("TOPK", topk) + def("NEXP", E);
+            Kern k1;
+            k1.src = Source{SRC_gemm_bf16, "rc_gemm_bf16",
+                            gemm_defs(up, 2, 1, fuse ? 2 : 3, R, I, Hd) + mdefs};
+            long ntm_up = (R + up.tm - 1) / up.tm + E;
+            k1.grid = dim3((unsigned)(ntm_up * (I / up.tn)), 1, 1);
+            k1.block = dim3(64 * up.wm * up.wn, 1, 1);
+            k1.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
+                put(b, GemmBf16Args{a->in[0], a->in[3], a->in[4], w + (fuse ? offH : offG),
+                                    fuse ? nullptr : w + offU, nullptr, w + offPerm, w + offOff,
+                                    w + offTu});
+            };
+            p.kerns.push_back(k1);
+            p.dominant = 1;
+            if (!fuse) {
+                Kern ke;
+                ke.src = Source{SRC_aux, "rc_swiglu_f32", def("EW_N", R * I) + def("EW_COLS", I)};
+                ke.grid = dim3((unsigned)((R * I / 4 + 255) / 256), 1, 1);
+                ke.block = dim3(256, 1, 1);
+                ke.bind = [=](const rc_args *, char *w, std::vector<char> &b) {
+                    put(b, EwArgs{w + offG, w + offU, nullptr, w + offH});
+                };
+                p.kerns.push_back(ke);
+            }
+            Kern k2;
+            k2.src = Source{SRC_gemm_bf16, "rc_gemm_bf16", gemm_defs(dn, 1, 3, 0, R, Hd, I) + mdefs};
+            long ntm_dn = (R + dn.tm - 1) / dn.tm + E;
+            k2.grid = dim3((unsigned)(ntm_dn * (Hd / dn.tn)), 1, 1);
+            k2.block = dim3(64 * dn.wm * dn.wn, 1, 1);
+            k2.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
+                put(b, GemmBf16Args{w + offH, a->in[5], nullptr, w + offY, nullptr, nullptr,
+                                    w + offPerm, w + offOff, w + offTd});
+            };
+            p.kerns.push_back(k2);
+            Kern k3;
+            k3.src = Source{SRC_aux, "rc_moe_combine", moe};
+            k3.grid = dim3((unsigned)((T * (Hd / 8) + 255) / 256), 1, 1);
+            k3.block = dim3(256, 1, 1);
+            k3.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
+                put(b, MoeCombineArgs{w + offY, w + offPos, a->in[2], a->out[0]});
+            };
+            p.kerns.push_back(k3);
+            break;
+        }
+        case RC_OP_CONV2D: {
+            long N = D[0], H = D[1], W = D[2], C = D[3], K = D[4], R = D[5], S = D[6], pad = D[7];
+            long P = H + 2 * pad - R + 1, Q = W + 2 * pad - S + 1, M = N * P * Q;
+            GemmCfg g = read_block(d, s, "");
+            int fuse = kv(d, s, "fuse");
+            size_t offPre = fuse ? 0 : ws.add((size_t)M * K * 4);
+            std::string cv = def("CV_H", H) + def("CV_W", W) + def("CV_C", C) + def("CV_P", P) +
+                             def("CV_Q", Q) + def("CV_S", S) + def("CV_PAD", pad);
+            Kern k1;
+            k1.src = Source{SRC_gemm_bf16, "rc_gemm_bf16",
+                            gemm_defs(g, 1, 2, fuse ? 1 : 3, M, K, R * S * C) + cv};
+            k1.grid = dim3((unsigned)((M / g.tm) * (K / g.tn)), 1, 1);
+            k1.block = dim3(64 * g.wm * g.wn, 1, 1);
+            k1.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
+                if (fuse)
+                    put(b, GemmBf16Args{a->in[0], a->in[1], nullptr, a->out[0], nullptr, a->in[2],
+                                        nullptr, nullptr, nullptr});
+                else
+                    put(b, GemmBf16Args{a->in[0], a->in[1], nullptr, w + offPre, nullptr, nullptr,
+                                        nullptr, nullptr, nullptr});
+            };
+            p.kerns.push_back(k1);
+            if (!fuse) {
+                Kern ke;
+                ke.src = Source{SRC_aux, "rc_bias_silu_f32", def("EW_N", M * K) + def("EW_COLS", K)};
+                ke.grid = dim3((unsigned)((M * K / 4 + 255) / 256), 1, 1);
+                ke.block = dim3(256, 1, 1);
+                ke.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
+                    put(b, EwArgs{w + offPre, nullptr, a->in[2], a->out[0]});
+                };
+                p.kerns.push_back(ke);
+            }
+            p.dominant = 0;
+            break;
+        }
+        case RC_OP_ATTENTION: {
+            long B = D[0], Hh = D[1], S = D[2], Dh = D[3];
+            int bm = kv(d, s, "block_m"), w = kv(d, s, "waves");
+            Kern k;
+            double scale_log2 = 1.4426950408889634 / std::sqrt((double)Dh);
+            char sbuf[64];
+            snprintf(sbuf, sizeof sbuf, "#define SCALE_LOG2 %.17gf\n", scale_log2);
+            k.src = Source{SRC_attention, "rc_attention",
+                           def("BM", bm) + def("BN", kv(d, s, "block_n")) + def("NW", w) +
+                               def("MF", kv(d, s, "mfma")) + def("STAGES", kv(d, s, "stages")) +
+                               def("VEC", kv(d, s, "vec")) + def("UNROLL", kv(d, s, "unroll")) +
+                               def("ORDER", kv(d, s, "order")) + def("AB", B) + def("AH", Hh) +
+                               def("AS", S) + def("AD", Dh) +
+                               def("CAUSAL", (d->flags & RC_FLAG_CAUSAL) ? 1 : 0) + sbuf};
+            k.grid = dim3((unsigned)(B * Hh * (S / bm)), 1, 1);
+            k.block = dim3(64 * w, 1, 1);
+            k.bind = [](const rc_args *a, char *, std::vector<char> &b) {
+                put(b, AttnArgs{a->in[0], a->in[1], a->in[2], a->out[0]});
+            };
+            p.kerns.push_back(k);
+            p.dominant = 0;
+            break;
+        }
+        default: return fail(RC_ERR_UNSUPPORTED, "unknown operator kind");
+    }
+    p.workspace = ws.total;
+    return RC_OK;
+}
+
+int n_inputs(int kind) {
+    switch (kind) {
+        case RC_OP_GEMM_F32: return 2;
+        case RC_OP_ATTENTION: return 3;
+        case RC_OP_GATED_MLP: return 4;
+        case RC_OP_MOE: return 6;
+        case RC_OP_CONV2D: return 3;
+    }
+    return 0;
+}
+
+rc_status hip_fail(hipError_t e, const char *what) {
+    return fail(RC_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+void *g_flush = nullptr;
+const size_t FLUSH_BYTES = (size_t)512 << 20;
+
+}  // namespace
+
+extern "C" {
+
+rc_status rc_set_cache_dir(const char *dir) {
+    std::lock_guard<std::mutex> g(g_mu);
+    g_cache_dir = dir ? dir : "";
+    return RC_OK;
+}
+
+rc_status rc_precompile(const rc_op_desc *d, const rc_schedule *s, int32_t n, int32_t nthreads,
+                        rc_status *status) {
+    if (!desc_ok(d) || (!s && n > 0) || n < 0) return fail(RC_ERR_INVALID_ARGUMENT, "bad arguments");
+    std::atomic<int> next(0);
+    std::atomic<int> nfail(0);
+    std::vector<rc_status> st(n, RC_OK);
+    auto work = [&]() {
+        for (;;) {
+            int i = next.fetch_add(1);
+            if (i >= n) return;
+            std::string why = check_schedule(d, &s[i]);
+            if (!why.empty()) {
+                st[i] = RC_ERR_ILLEGAL_SCHEDULE;
+                ++nfail;
+                continue;
+            }
+            rc_plan p;
+            rc_status r = describe(d, &s[i], p);
+            for (auto &k : p.kerns) {
+                if (r != RC_OK) break;
+                std::vector<char> code;
+                std::string key;
+                r = compile(k.src, code, key);
+                if (r == RC_OK && meta_int(code, ".private_segment_fixed_size") > 0)
+                    r = RC_ERR_ILLEGAL_SCHEDULE;
+            }
+            st[i] = r;
+            if (r != RC_OK) ++nfail;
+        }
+    };
+    int nt = std::max(1, std::min<int>(nthreads, n));
+    std::vector<std::thread> pool;
+    for (int t = 0; t < nt; ++t) pool.emplace_back(work);
+    for (auto &t : pool) t.join();
+    if (status)
+        for (int i = 0; i < n; ++i) status[i] = st[i];
+    if (nfail) return fail(RC_ERR_COMPILE, std::to_string(nfail.load()) + " of " + std::to_string(n) +
+                                               " schedules failed to compile or are illegal");
+    return RC_OK;
+}
+
+rc_status rc_plan_create(const rc_op_desc *d, const rc_schedule *s, rc_plan **out) {
+    if (!desc_ok(d) || !s || !out) return fail(RC_ERR_INVALID_ARGUMENT, "bad arguments");
+    *out = nullptr;
+    std::string why = check_schedule(d, s);
+    if (!why.empty()) return fail(RC_ERR_ILLEGAL_SCHEDULE, why);
+    std::unique_ptr<rc_plan> p(new rc_plan());
+    p->desc = *d;
+    p->sched = *s;
+    rc_status r = describe(d, s, *p);
+    if (r != RC_OK) return r;
+    for (auto &k : p->kerns) {
+        std::vector<char> code;
+        std::string key;
+        r = compile(k.src, code, key);
+        if (r != RC_OK) return r;
+        if (meta_int(code, ".private_segment_fixed_size") > 0)
+            return fail(RC_ERR_ILLEGAL_SCHEDULE, std::string("spill: ") + k.src.entry +
+                                                     " needs scratch memory");
+        hipModule_t mod;
+        {
+            std::lock_guard<std::mutex> g(g_mu);
+            int dev = 0;
+            if (hipGetDevice(&dev) != hipSuccess) dev = -1;
+            std::string mkey = key + "@" + std::to_string(dev);
+            auto it = g_modules.find(mkey);
+            if (it == g_modules.end()) {
+                hipError_t e = hipModuleLoadData(&mod, code.data());
+                if (e != hipSuccess) return hip_fail(e, "hipModuleLoadData");
+                g_modules[mkey] = mod;
+            } else {
+                mod = it->second;
+            }
+        }
+        hipError_t e = hipModuleGetFunction(&k.fn, mod, k.src.entry);
+        if (e != hipSuccess) return hip_fail(e, "hipModuleGetFunction");
+    }
+    *out = p.release();
+    clear_error();
+    return RC_OK;
+}
+
+void rc_plan_destroy(rc_plan *p) { delete p; }
+
+rc_status rc_plan_workspace(const rc_plan *p, size_t *bytes) {
+    if (!p || !bytes) return fail(RC_ERR_INVALID_ARGUMENT, "null argument");
+    *bytes = p->workspace;
+    return RC_OK;
+}
+
+rc_status rc_plan_kernels(const rc_plan *p, int32_t *nkernels, int32_t *dominant) {
+    if (!p) return fail(RC_ERR_INVALID_ARGUMENT, "null plan");
+    if (nkernels) *nkernels = (int32_t)p->kerns.size();
+    if (dominant) *dominant = p->dominant;
+    return RC_OK;
+}
+
+static rc_status check_args(const rc_plan *p, const rc_args *a, void *ws, size_t ws_bytes) {
+    if (!p || !a || a->struct_size < sizeof(rc_args)) return fail(RC_ERR_INVALID_ARGUMENT, "null plan or args");
+    int ni = n_inputs(p->desc.kind);
+    for (int i = 0; i < ni; ++i) {
+        if (!a->in[i]) return fail(RC_ERR_INVALID_ARGUMENT, "input " + std::to_string(i) + " is NULL");
+        if ((uintptr_t)a->in[i] & 15) return fail(RC_ERR_MISALIGNED, "input " + std::to_string(i) + " is not 16-byte aligned");
+    }
+    if (!a->out[0]) return fail(RC_ERR_INVALID_ARGUMENT, "output is NULL");
+    if ((uintptr_t)a->out[0] & 15) return fail(RC_ERR_MISALIGNED, "output is not 16-byte aligned");
+    if (p->workspace) {
+        if (!ws || ws_bytes < p->workspace)
+            return fail(RC_ERR_INVALID_ARGUMENT, "workspace of " + std::to_string(p->workspace) + " bytes required");
+        if ((uintptr_t)ws & 255) return fail(RC_ERR_MISALIGNED, "workspace is not 256-byte aligned");
+    }
+    return RC_OK;
+}
+
+static rc_status launch_impl(const rc_plan *p, const rc_args *a, void *ws, size_t ws_bytes,
+                             void *stream, void **events, int32_t nevents) {
+    rc_status r = check_args(p, a, ws, ws_bytes);
+    if (r != RC_OK) return r;
+    if (events && nevents < (int32_t)p->kerns.size() + 1)
+        return fail(RC_ERR_INVALID_ARGUMENT, "need nkernels + 1 events");
+    hipStream_t st = (hipStream_t)stream;
+    std::vector<char> blob;
+    for (size_t i = 0; i < p->kerns.size(); ++i) {
+        const Kern &k = p->kerns[i];
+        k.bind(a, (char *)ws, blob);
+        size_t sz = blob.size();
+        void *cfg[] = {HIP_LAUNCH_PARAM_BUFFER_POINTER, blob.data(), HIP_LAUNCH_PARAM_BUFFER_SIZE, &sz,
+                       HIP_LAUNCH_PARAM_END};
+        if (events) {
+            hipError_t e = hipEventRecord((hipEvent_t)events[i], st);
+            if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+        }
+        hipError_t e = hipModuleLaunchKernel(k.fn, k.grid.x, k.grid.y, k.grid.z, k.block.x,
+                                             k.block.y, k.block.z, 0, st, nullptr, cfg);
+        if (e != hipSuccess) return hip_fail(e, (std::string("launch ") + k.src.entry).c_str());
+    }
+    if (events) {
+        hipError_t e = hipEventRecord((hipEvent_t)events[p->kerns.size()], st);
+        if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+    }
+    return RC_OK;
+}
+
+rc_status rc_launch(const rc_plan *p, const rc_args *a, void *workspace, size_t ws_bytes,
+                    void *stream) {
+    return launch_impl(p, a, workspace, ws_bytes, stream, nullptr, 0);
+}
+
+rc_status rc_launch_timed(const rc_plan *p, const rc_args *a, void *workspace, size_t ws_bytes,
+                          void *stream, void **events, int32_t nevents) {
+    if (!events) return fail(RC_ERR_INVALID_ARGUMENT, "events is NULL");
+    return launch_impl(p, a, workspace, ws_bytes, stream, events, nevents);
+}
+
+void rc_time_opts_init(rc_time_opts *o) {
+    if (!o) return;
+    o->struct_size = sizeof(rc_time_opts);
+    o->warmup = 3;
+    o->repeat = 20;
+    o->flush = 1;
+    o->reserved = 0;
+}
+
+static double quantile(std::vector<double> v, double q) {
+    std::sort(v.begin(), v.end());
+    if (v.empty()) return 0.0;
+    double pos = q * (v.size() - 1);
+    size_t lo = (size_t)pos;
+    size_t hi = std::min(lo + 1, v.size() - 1);
+    return v[lo] + (pos - lo) * (v[hi] - v[lo]);
+}
+
+rc_status rc_time(const rc_plan *p, const rc_args *a, void *ws, size_t ws_bytes, void *stream,
+                  const rc_time_opts *o, rc_timing *out) {
+    if (!p || !a || !out) return fail(RC_ERR_INVALID_ARGUMENT, "null argument");
+    rc_time_opts opt;
+    rc_time_opts_init(&opt);
+    if (o) opt = *o;
+    if (opt.repeat < 1 || opt.warmup < 0) return fail(RC_ERR_INVALID_ARGUMENT, "repeat must be >= 1");
+    hipStream_t st = (hipStream_t)stream;
+    if (opt.flush && !g_flush) {
+        hipError_t e = hipMalloc(&g_flush, FLUSH_BYTES);
+        if (e != hipSuccess) return hip_fail(e, "hipMalloc(flush buffer)");
+    }
+    for (int i = 0; i < opt.warmup; ++i) {
+        rc_status r = rc_launch(p, a, ws, ws_bytes, stream);
+        if (r != RC_OK) return r;
+    }
+    int nk = (int)p->kerns.size();
+    std::vector<hipEvent_t> ev((size_t)opt.repeat * (nk + 1));
+    for (auto &e : ev) {
+        hipError_t he = hipEventCreate(&e);
+        if (he != hipSuccess) return hip_fail(he, "hipEventCreate");
+    }
+    rc_status r = RC_OK;
+    for (int i = 0; i < opt.repeat && r == RC_OK; ++i) {
+        if (opt.flush) {
+            hipError_t e = hipMemsetAsync(g_flush, i & 0xFF, FLUSH_BYTES, st);
+            if (e != hipSuccess) r = hip_fail(e, "flush");
+        }
+        if (r == RC_OK) r = launch_impl(p, a, ws, ws_bytes, stream, (void **)&ev[(size_t)i * (nk + 1)], nk + 1);
+    }
+    hipError_t se = hipStreamSynchronize(st);
+    if (r == RC_OK && se != hipSuccess) r = hip_fail(se, "hipStreamSynchronize");
+    if (r == RC_OK) {
+        std::vector<double> tot, per[4];
+        for (int i = 0; i < opt.repeat; ++i) {
+            hipEvent_t *e = &ev[(size_t)i * (nk + 1)];
+            float ms = 0.f;
+            if (hipEventElapsedTime(&ms, e[0], e[nk]) != hipSuccess) r = fail(RC_ERR_HIP, "hipEventElapsedTime");
+            tot.push_back(ms);
+            for (int k = 0; k < nk && k < 4; ++k) {
+                float km = 0.f;
+                if (hipEventElapsedTime(&km, e[k], e[k + 1]) != hipSuccess) r = fail(RC_ERR_HIP, "hipEventElapsedTime");
+                per[k].push_back(km);
+            }
+        }
+        rc_timing t;
+        memset(&t, 0, sizeof t);
+        t.struct_size = sizeof t;
+        t.nkernels = nk;
+        t.median_ms = quantile(tot, 0.5);
+        t.q1_ms = quantile(tot, 0.25);
+        t.q3_ms = quantile(tot, 0.75);
+        t.min_ms = *std::min_element(tot.begin(), tot.end());
+        double sum = 0;
+        for (double x : tot) sum += x;
+        t.mean_ms = sum / tot.size();
+        double sec = t.median_ms * 1e-3;
+        t.tflops = rc_op_flops(&p->desc) / sec / 1e12;
+        t.gbps = rc_op_bytes(&p->desc) / sec / 1e9;
+        t.frac_flops = t.tflops * 1e12 / rc_peak_flops(&p->desc);
+        t.frac_bytes = t.gbps * 1e9 / rc_peak_bytes_per_s();
+        for (int k = 0; k < nk && k < 4; ++k) t.kernel_ms[k] = quantile(per[k], 0.5);
+        *out = t;
+    }
+    for (auto &e : ev) (void)hipEventDestroy(e);
+    return r;
+}
+
+}  // extern "C"

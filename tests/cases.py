@@ -1,0 +1,113 @@
+"""Operator shapes and schedules exercised by the GPU parity tests.
+
+Small shapes span several tiles (and ragged expert groups for the MoE) so
+the oracle finishes in seconds; the full-size workloads are checked on
+sampled outputs in the schedules the benchmark times.
+"""
+import json
+import os
+
+from paper_2506_01374_amd import rc, workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+TUNED = json.load(open(os.path.join(ROOT, "paper_2506_01374_amd", "tuned.json")))
+
+SMALL = {
+    "gemm": (rc.RC_OP_GEMM_F32, (128, 128, 128), 0),
+    "attn_causal": (rc.RC_OP_ATTENTION, (1, 2, 256, 128), rc.RC_FLAG_CAUSAL),
+    "attn_full": (rc.RC_OP_ATTENTION, (1, 2, 256, 128), 0),
+    "attn_d64": (rc.RC_OP_ATTENTION, (2, 1, 128, 64), rc.RC_FLAG_CAUSAL),
+    "mlp": (rc.RC_OP_GATED_MLP, (256, 256, 512), 0),
+    "moe": (rc.RC_OP_MOE, (256, 256, 8, 128, 2), 0),
+    "conv": (rc.RC_OP_CONV2D, (2, 16, 12, 64, 64, 3, 3, 1), 0),
+}
+
+_GEMM_BLOCK = ("tile_m", "tile_n", "tile_k", "waves_m", "waves_n", "mfma", "stages", "vec",
+               "unroll", "layout", "grid")
+
+
+def _block(prefix, tm, tn, tk, wm, wn, mf, st, vec, un, lay, grid):
+    vals = (tm, tn, tk, wm, wn, mf, st, vec, un, lay, grid)
+    return ",".join(f"{prefix}{k}={v}" for k, v in zip(_GEMM_BLOCK, vals))
+
+
+def gemm_sweep():
+    """The 18-point fp32 sweep: tile 16/32/64 (M and N) x vector width 1/4."""
+    out = []
+    for tm in (16, 32, 64):
+        for tn in (16, 32, 64):
+            for vec in (1, 4):
+                out.append(f"tile_m={tm},tile_n={tn},tile_k=16,waves_m=1,waves_n=1,vec={vec},"
+                           f"stages=2,unroll=1,layout=0")
+    return out
+
+
+SCHEDULES = {
+    "gemm": gemm_sweep() + [
+        "",   # P0
+        "tile_m=64,tile_n=64,tile_k=32,waves_m=2,waves_n=2,vec=4,stages=2,unroll=2,layout=1",
+        "tile_m=32,tile_n=64,tile_k=8,waves_m=2,waves_n=1,vec=1,stages=1,unroll=4,layout=1",
+        "tile_m=64,tile_n=32,tile_k=4,waves_m=1,waves_n=2,vec=1,stages=2,unroll=1,layout=0",
+    ],
+    "attn_causal": [
+        "",
+        "block_m=128,block_n=64,waves=4,mfma=32,stages=2,vec=8,unroll=1,order=1",
+        "block_m=64,block_n=128,waves=4,mfma=16,stages=1,vec=4,unroll=2,order=0",
+        "block_m=256,block_n=32,waves=8,mfma=32,stages=2,vec=8,unroll=1,order=1",
+        "block_m=64,block_n=64,waves=2,mfma=32,stages=1,vec=8,unroll=1,order=0",
+        "block_m=32,block_n=128,waves=2,mfma=16,stages=2,vec=2,unroll=1,order=1",
+    ],
+    "attn_full": [
+        "",
+        "block_m=128,block_n=64,waves=4,mfma=32,stages=2,vec=8,unroll=1,order=1",
+        "block_m=64,block_n=128,waves=4,mfma=16,stages=1,vec=4,unroll=2,order=0",
+    ],
+    "attn_d64": [
+        "block_m=64,block_n=32,waves=2,mfma=32,stages=2,vec=8,unroll=1,order=0",
+        "block_m=32,block_n=64,waves=2,mfma=16,stages=1,vec=4,unroll=1,order=1",
+    ],
+    "mlp": [
+        "",
+        _block("up.", 128, 128, 64, 2, 2, 32, 2, 8, 1, 1, 1) + "," +
+        _block("down.", 128, 128, 64, 2, 2, 32, 2, 8, 1, 1, 1) + ",fuse=1",
+        _block("up.", 64, 64, 32, 2, 2, 16, 1, 4, 2, 0, 0) + "," +
+        _block("down.", 64, 128, 128, 1, 2, 16, 2, 8, 2, 0, 1) + ",fuse=0",
+        _block("up.", 256, 64, 64, 4, 1, 32, 2, 8, 1, 1, 0) + "," +
+        _block("down.", 32, 256, 32, 1, 4, 32, 1, 2, 1, 1, 0) + ",fuse=1",
+        _block("up.", 32, 32, 128, 1, 1, 16, 2, 8, 2, 1, 1) + "," +
+        _block("down.", 256, 256, 32, 4, 4, 16, 2, 8, 1, 0, 1) + ",fuse=0",
+    ],
+    "moe": [
+        "",
+        _block("up.", 128, 128, 64, 2, 2, 32, 2, 8, 1, 1, 1) + "," +
+        _block("down.", 128, 128, 64, 2, 2, 32, 2, 8, 1, 1, 1) + ",fuse=1",
+        _block("up.", 64, 64, 32, 2, 2, 16, 1, 4, 1, 0, 0) + "," +
+        _block("down.", 32, 128, 128, 1, 2, 16, 2, 8, 1, 0, 1) + ",fuse=0",
+        _block("up.", 32, 64, 32, 1, 2, 16, 2, 8, 2, 1, 0) + "," +
+        _block("down.", 256, 64, 64, 4, 1, 32, 2, 8, 1, 1, 0) + ",fuse=1",
+    ],
+    "conv": [
+        "",
+        _block("", 128, 64, 64, 2, 1, 16, 2, 8, 1, 1, 0) + ",fuse=1",
+        _block("", 64, 32, 32, 2, 1, 16, 1, 4, 2, 0, 1) + ",fuse=0",
+        _block("", 128, 64, 64, 2, 2, 32, 2, 8, 1, 1, 1) + ",fuse=1",
+        _block("", 32, 64, 64, 1, 2, 16, 2, 2, 1, 0, 0) + ",fuse=1",
+    ],
+}
+
+
+def small_op(key):
+    kind, dims, flags = SMALL[key]
+    return rc.Op(kind, dims, flags)
+
+
+def all_compile_jobs():
+    """(op, [schedules]) pairs for ahead-of-time compilation."""
+    jobs = []
+    for key, lst in SCHEDULES.items():
+        op = small_op(key)
+        jobs.append((op, [op.from_string(s) for s in lst]))
+    for name, s in TUNED.items():
+        op = W.workload_op(name)
+        jobs.append((op, [op.from_string(s), op.default()]))
+    return jobs
