@@ -1,0 +1,199 @@
+#!/usr/bin/env python3
+"""Benchmark: best-found schedule of a contraction workload on one MI355X.
+
+One step is one execution of the workload's operator in its tuned schedule
+(every kernel of the operator: for attention the single fused kernel) over
+inputs already resident in HBM.  W untimed warm-up steps, then exactly K
+steps back to back, bracketed by torch.cuda.synchronize(); value = the
+operator's algorithmic FLOPs x K / elapsed wall time.
+
+roofline: HIP events recorded on the launch stream around every kernel of
+every timed step give the dominant kernel's mean duration; achieved =
+algorithmic bytes (HBM-bound operators) or FLOPs (MFMA-bound) of one launch
+divided by that duration.  traffic: measured HBM bytes per launch from the
+rocprofv3 FETCH_SIZE / WRITE_SIZE summaries in profiles/, when present for
+the same kernel source and schedule, else null.
+
+cpu_baseline: the CPU oracle (test infrastructure) on the same workload, or a
+bounded sample of it, timed on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "best-schedule TFLOP/s and % of MFMA peak per operator; samples to reach it"
+DEFAULT_WORKLOAD = "attention_causal_b1_h32_s1024_d128"
+HBM_PEAK_GBS = 8000.0
+
+# Which roofline binds each operator (arithmetic intensity vs. the ridge
+# point of the MI355X: bf16 2516.6 TFLOP/s / 8 TB/s = 314.6 FLOP/B).
+BOUND = {"gemm_f32_128": "mfma", "attention_causal_b1_h32_s1024_d128": "hbm",
+         "gated_mlp_t2048_h4096_i14336": "mfma", "moe_t4096_h2048_e64_i1408_top6": "mfma",
+         "conv3x3_n2_64x64_c320_k320": "mfma"}
+DTYPE = {"gemm_f32_128": "f32"}
+
+
+def _oracle_baseline(name, op, host, budget_s):
+    """Time the CPU oracle on the workload (whole, or a bounded row sample)."""
+    import oracle
+    kind = op.kind
+    from paper_2506_01374_amd import rc
+    flops_total = op.flops()
+    t0 = time.perf_counter()
+    reps = 0
+    if kind == rc.RC_OP_ATTENTION:
+        sample = "all query rows of all heads (whole workload)"
+        frac = 1.0
+        while True:
+            oracle.attention_bf16(host["Q"], host["K"], host["V"], causal=bool(op.flags & 1))
+            reps += 1
+            if time.perf_counter() - t0 > budget_s:
+                break
+    elif kind == rc.RC_OP_GEMM_F32:
+        sample = "whole workload"
+        frac = 1.0
+        while True:
+            oracle.gemm_f32(host["A"], host["B"])
+            reps += 1
+            if time.perf_counter() - t0 > budget_s:
+                break
+    else:
+        n = {rc.RC_OP_GATED_MLP: 32, rc.RC_OP_MOE: 32, rc.RC_OP_CONV2D: 512}[kind]
+        rows = np.arange(n)
+        total = op.dims[0] if kind != rc.RC_OP_CONV2D else op.dims[0] * op.dims[1] * op.dims[2]
+        frac = n / total
+        sample = f"first {n} of {total} independent output rows"
+        while True:
+            if kind == rc.RC_OP_GATED_MLP:
+                oracle.gated_mlp_bf16(host["X"], host["Wg"], host["Wu"], host["Wd"], rows=rows)
+            elif kind == rc.RC_OP_MOE:
+                oracle.moe_bf16(host["X"], host["ids"], host["w"], host["Wg"], host["Wu"], host["Wd"],
+                                rows=rows)
+            else:
+                oracle.conv2d_bf16(host["x"], host["w"], host["bias"], pad=op.dims[7], pixels=rows)
+            reps += 1
+            if time.perf_counter() - t0 > budget_s:
+                break
+    dt = time.perf_counter() - t0
+    return {"value": flops_total * frac * reps / dt / 1e12, "unit": "TFLOP/s",
+            "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"{sample}, {reps} repetition(s) in {dt:.2f} s"}
+
+
+def _load_traffic(name, plan_key):
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path)).get(name)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("key") != plan_key:
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--schedule", default=None, help="schedule string (default: tuned.json)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle work")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
+              "multi-GPU path.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2506_01374_amd import rc, workloads as W
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    rc.set_cache_dir(os.path.join(ROOT, "paper_2506_01374_amd", "jit_cache"))
+    torch.cuda.set_device(0)
+    name = args.workload
+    op = W.workload_op(name)
+    tuned = json.load(open(os.path.join(ROOT, "paper_2506_01374_amd", "tuned.json")))
+    sched = op.from_string(args.schedule if args.schedule else tuned[name])
+    host = W.host_inputs(op, seed=0)
+    dev = W.to_device(W.stored_inputs(op, sched, host))
+    out = W.empty_output(op)
+    plan = rc.Plan(op, sched)
+    ws = plan.workspace()
+    stream = torch.cuda.current_stream()
+    nk, dom = plan.nkernels, plan.dominant
+
+    for _ in range(args.warmup):
+        plan.launch(dev, out, ws, stream)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(nk + 1)] for _ in range(K)]
+    for row in events:              # torch creates an event on its first record
+        for e in row:
+            e.record(stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        plan.launch_timed(dev, out, events[i], ws, stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    ms_per_step = elapsed * 1e3 / K
+    flops = op.flops()
+    value = flops / (elapsed / K) / 1e12
+    dom_ms = float(np.mean([events[i][dom].elapsed_time(events[i][dom + 1]) for i in range(K)]))
+    kern_ms = [float(np.mean([events[i][k].elapsed_time(events[i][k + 1]) for i in range(K)]))
+               for k in range(nk)]
+    bound = BOUND.get(name, "mfma")
+    if bound == "hbm":
+        achieved = op.bytes() / (dom_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS}
+    else:
+        # the dominant kernel's FLOPs: its share of the operator's contraction
+        share = {rc.RC_OP_GATED_MLP: 2.0 / 3.0, rc.RC_OP_MOE: 2.0 / 3.0}.get(op.kind, 1.0)
+        achieved = flops * share / (dom_ms * 1e-3) / 1e12
+        peak = op.peak_flops() / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                "frac": achieved / peak}
+    roof["traffic"] = _load_traffic(name, str(sched))
+    roof["kernel"] = ["rc_attention"] if op.kind == rc.RC_OP_ATTENTION else None
+    roof["dominant_kernel_ms"] = dom_ms
+    roof["kernel_ms"] = kern_ms
+    roof["mfma_frac"] = (flops / (sum(kern_ms) * 1e-3)) / op.peak_flops()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = _oracle_baseline(name, op, host, args.cpu_budget)
+
+    rec = {
+        "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": DTYPE.get(name, "bf16"),
+        "data": "synthetic (seeded SplitMix64 inputs of the workload's shape and distribution)",
+        "config": {"workload": name, "dims": list(op.dims), "flags": op.flags,
+                   "schedule": str(sched), "parallelism": "single GPU",
+                   "frac_of_mfma_peak": value * 1e12 / op.peak_flops()},
+        "roofline": roof, "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -220,6 +220,26 @@ rc_status rc_plan_workspace(const rc_plan *p, size_t *bytes);
  * most of the FLOPs (the contraction). */
 rc_status rc_plan_kernels(const rc_plan *p, int32_t *nkernels, int32_t *dominant);
 
+/* Resources of one kernel of a variant, read from its gfx950 code object. */
+typedef struct rc_kernel_info {
+    uint32_t struct_size;
+    char name[48];            /* kernel symbol */
+    int32_t grid;             /* workgroups per launch */
+    int32_t block;            /* threads per workgroup */
+    int32_t lds_bytes;        /* static LDS per workgroup */
+    int32_t vgprs;            /* architectural VGPRs per lane */
+    int32_t agprs;            /* accumulation VGPRs per lane */
+    int32_t sgprs;
+    int32_t scratch_bytes;    /* private segment per lane (0 unless spilling) */
+    int32_t waves_per_simd;   /* occupancy bound from registers and LDS */
+} rc_kernel_info;
+
+/* Compile (or fetch from the cache) the kernels of a schedule and report
+ * their launch shape and resources; needs no GPU.  Writes min(count, cap)
+ * entries and the count. */
+rc_status rc_describe(const rc_op_desc *d, const rc_schedule *s, rc_kernel_info *buf,
+                      int32_t cap, int32_t *n);
+
 typedef struct rc_args {
     uint32_t struct_size;
     const void *in[8];

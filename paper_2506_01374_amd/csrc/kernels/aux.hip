@@ -64,67 +64,92 @@ struct MoePrepArgs {
     int *tile_down;        // [E + 1] first M tile of each expert, down GEMM
 };
 
-// Grid: MOE_E workgroups of 256 threads.  Every workgroup builds the full
-// expert histogram in LDS (ids out of range are clamped to expert 0 so that
-// no write can leave its buffer), derives the exclusive prefix offsets and
-// the per-expert tile starts, and then workgroup e writes the rows routed to
-// expert e in token order (a stable counting sort).  Workgroup 0 also
+// Grid: MOE_E workgroups of PREP_T threads.  Every workgroup copies all
+// expert ids into LDS (ids out of range are clamped to expert 0 so that no
+// write can leave its buffer), builds the expert histogram from per-wave
+// sub-histograms, derives the exclusive prefix offsets and the per-expert
+// tile starts, and then workgroup e writes the rows routed to expert e in
+// token order (a stable counting sort): each thread owns a contiguous chunk
+// of entries, counts its hits, and one block-wide exclusive scan of those
+// counts gives every thread its first output row.  Workgroup 0 also
 // publishes offsets and tile starts.
-extern "C" __global__ __launch_bounds__(256) void rc_moe_prep(MoePrepArgs a) {
-    __shared__ int hist[MOE_E];
+#define PREP_T 1024
+#define PREP_W (PREP_T / 64)
+#define PREP_CHUNK ((MOE_ROWS + PREP_T - 1) / PREP_T)
+
+extern "C" __global__ __launch_bounds__(PREP_T) void rc_moe_prep(MoePrepArgs a) {
+    __shared__ int ids[PREP_CHUNK * PREP_T];
+    __shared__ int sub[PREP_W][MOE_E];
     __shared__ int offs[MOE_E + 1];
-    __shared__ int wave_cnt[4];
+    __shared__ int wsum[PREP_W];
     const int tid = threadIdx.x, e = blockIdx.x;
-    for (int i = tid; i < MOE_E; i += 256) hist[i] = 0;
-    __syncthreads();
-    for (int i = tid; i < MOE_ROWS; i += 256) {
-        int x = a.ids[i];
-        x = (x < 0 || x >= MOE_E) ? 0 : x;
-        atomicAdd(&hist[x], 1);
-    }
-    __syncthreads();
-    if (tid == 0) {
-        int s = 0, tu = 0, td = 0;
-        for (int x = 0; x < MOE_E; ++x) {
-            offs[x] = s;
-            if (e == 0) {
-                a.offsets[x] = s;
-                a.tile_up[x] = tu;
-                a.tile_down[x] = td;
-            }
-            s += hist[x];
-            tu += (hist[x] + MOE_TM_UP - 1) / MOE_TM_UP;
-            td += (hist[x] + MOE_TM_DOWN - 1) / MOE_TM_DOWN;
-        }
-        offs[MOE_E] = s;
-        if (e == 0) {
-            a.offsets[MOE_E] = s;
-            a.tile_up[MOE_E] = tu;
-            a.tile_down[MOE_E] = td;
-        }
-    }
-    __syncthreads();
-    int base = offs[e];
     const int lane = tid & 63, wave = tid >> 6;
-    for (int c0 = 0; c0 < MOE_ROWS; c0 += 256) {
-        int i = c0 + tid;
+    for (int i = tid; i < PREP_W * MOE_E; i += PREP_T) (&sub[0][0])[i] = 0;
+    for (int i = tid; i < PREP_CHUNK * PREP_T; i += PREP_T) {
         int x = i < MOE_ROWS ? a.ids[i] : -1;
         if (i < MOE_ROWS && (x < 0 || x >= MOE_E)) x = 0;
-        bool hit = (x == e);
-        unsigned long long ballot = __ballot(hit);
-        int before = __popcll(ballot & ((1ull << lane) - 1ull));
-        if (lane == 0) wave_cnt[wave] = __popcll(ballot);
-        __syncthreads();
-        int wbase = 0;
-        for (int w = 0; w < wave; ++w) wbase += wave_cnt[w];
-        int total = wave_cnt[0] + wave_cnt[1] + wave_cnt[2] + wave_cnt[3];
-        if (hit) {
-            int p = base + wbase + before;
+        ids[i] = x;
+    }
+    __syncthreads();
+    for (int i = tid; i < MOE_ROWS; i += PREP_T) atomicAdd(&sub[wave][ids[i]], 1);
+    __syncthreads();
+    if (wave == 0) {
+        // lane x sums expert x over the sub-histograms; one wave scans 64 bins
+        int run = 0, tu = 0, td = 0;
+        for (int base = 0; base < MOE_E; base += 64) {
+            int x = base + lane;
+            int h = 0;
+            if (x < MOE_E)
+                for (int w = 0; w < PREP_W; ++w) h += sub[w][x];
+            int hu = (h + MOE_TM_UP - 1) / MOE_TM_UP, hd = (h + MOE_TM_DOWN - 1) / MOE_TM_DOWN;
+            int ih = h, iu = hu, id = hd;          // inclusive scans across the wave
+            for (int d = 1; d < 64; d <<= 1) {
+                int th = __shfl_up(ih, d), tu2 = __shfl_up(iu, d), td2 = __shfl_up(id, d);
+                if (lane >= d) { ih += th; iu += tu2; id += td2; }
+            }
+            if (x < MOE_E) {
+                offs[x] = run + ih - h;
+                if (e == 0) {
+                    a.offsets[x] = run + ih - h;
+                    a.tile_up[x] = tu + iu - hu;
+                    a.tile_down[x] = td + id - hd;
+                }
+            }
+            run += __shfl(ih, 63);
+            tu += __shfl(iu, 63);
+            td += __shfl(id, 63);
+        }
+        if (lane == 0) {
+            offs[MOE_E] = run;
+            if (e == 0) {
+                a.offsets[MOE_E] = run;
+                a.tile_up[MOE_E] = tu;
+                a.tile_down[MOE_E] = td;
+            }
+        }
+    }
+    __syncthreads();
+    // stable compaction of the entries routed to expert e
+    const int c0 = tid * PREP_CHUNK;
+    int cnt = 0;
+    for (int j = 0; j < PREP_CHUNK; ++j) cnt += (c0 + j < MOE_ROWS && ids[c0 + j] == e);
+    int inc = cnt;
+    for (int d = 1; d < 64; d <<= 1) {
+        int t = __shfl_up(inc, d);
+        if (lane >= d) inc += t;
+    }
+    if (lane == 63) wsum[wave] = inc;
+    __syncthreads();
+    int before = 0;
+    for (int w = 0; w < wave; ++w) before += wsum[w];
+    int p = offs[e] + before + inc - cnt;
+    for (int j = 0; j < PREP_CHUNK; ++j) {
+        int i = c0 + j;
+        if (i < MOE_ROWS && ids[i] == e) {
             a.perm[p] = i;
             a.pos[i] = p;
+            ++p;
         }
-        base += total;
-        __syncthreads();
     }
 }
 

@@ -174,7 +174,11 @@ extern "C" __global__ __launch_bounds__(NT) void rc_gemm_bf16(GemmBf16Args args)
     for (int i = 0; i < A_LOADS; ++i) {
         int v = tid + i * NT;
         int r = v / (TK / VEC);
+#if AMODE == 1 || AMODE == 3
         aval[i] = r < rows_valid;
+#else
+        aval[i] = true;          // dense rows: every tile is full
+#endif
 #if AMODE == 0
         arow[i] = args.A + (size_t)(row_base + r) * GK;
 #elif AMODE == 1
@@ -261,35 +265,54 @@ extern "C" __global__ __launch_bounds__(NT) void rc_gemm_bf16(GemmBf16Args args)
             }
     };
 
-    auto compute = [&](int s) {
+    // Fragments of one k-step: FM activation and NB x FN weight fragments.
+    struct Frags {
+        bf16x8 a[FM];
+        bf16x8 b[NB][FN];
+    };
+    auto load_frags = [&](int s, int ks, Frags &f) {
+        const int chunk = ks * (KSTEP / 8) + lane / MF;
 #pragma unroll
-        for (int ks = 0; ks < TK / KSTEP; ++ks) {
-            const int chunk = ks * (KSTEP / 8) + lane / MF;
-            bf16x8 af[FM], bfr[NB][FN];
+        for (int i = 0; i < FM; ++i)
+            f.a[i] = *(const bf16x8 *)(As[s] + swz(wm * WTM + i * MF + lane % MF, chunk));
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+                f.b[b][j] = *(const bf16x8 *)(Bs[s][b] + swz(wn * WTN + j * MF + lane % MF, chunk));
+    };
+    auto mfmas = [&](const Frags &f) {
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
 #pragma unroll
             for (int i = 0; i < FM; ++i)
-                af[i] = *(const bf16x8 *)(As[s] + swz(wm * WTM + i * MF + lane % MF, chunk));
 #pragma unroll
-            for (int b = 0; b < NB; ++b)
+                for (int j = 0; j < FN; ++j) acc[b][i][j] = mfma(f.b[b][j], f.a[i], acc[b][i][j]);
+    };
+    // One K tile from LDS buffer s.  The fragments of k-step ks + 1 are read
+    // while the MFMAs of k-step ks issue; `mid` (the LDS store of the next
+    // tile into the other buffer) runs halfway through the MFMAs.
+    auto compute = [&](int s, auto &&mid) {
+        constexpr int KS = TK / KSTEP;
+        Frags f[2];
+        load_frags(s, 0, f[0]);
 #pragma unroll
-                for (int j = 0; j < FN; ++j)
-                    bfr[b][j] = *(const bf16x8 *)(Bs[s][b] + swz(wn * WTN + j * MF + lane % MF, chunk));
-#pragma unroll
-            for (int b = 0; b < NB; ++b)
-#pragma unroll
-                for (int i = 0; i < FM; ++i)
-#pragma unroll
-                    for (int j = 0; j < FN; ++j) acc[b][i][j] = mfma(bfr[b][j], af[i], acc[b][i][j]);
+        for (int ks = 0; ks < KS; ++ks) {
+            if (ks + 1 < KS) load_frags(s, ks + 1, f[(ks + 1) & 1]);
+            if (ks == KS / 2) mid();
+            mfmas(f[ks & 1]);
         }
+        if (KS == 1) mid();
     };
 
+    auto nothing = [] {};
 #if STAGES == 1
 #pragma unroll UNROLL
     for (int kt = 0; kt < KTILES; ++kt) {
         gload(kt * TK);
         swrite(0);
         __syncthreads();
-        compute(0);
+        compute(0, nothing);
         __syncthreads();
     }
 #else
@@ -298,9 +321,14 @@ extern "C" __global__ __launch_bounds__(NT) void rc_gemm_bf16(GemmBf16Args args)
     __syncthreads();
 #pragma unroll UNROLL
     for (int kt = 0; kt < KTILES; ++kt) {
+        // buffer (kt + 1) & 1 was last read in iteration kt - 1, which ended
+        // with a barrier, so it may be overwritten during this tile's MFMAs
         if (kt + 1 < KTILES) gload((kt + 1) * TK);
-        compute(kt & 1);
-        if (kt + 1 < KTILES) swrite((kt + 1) & 1);
+        const int nxt = (kt + 1) & 1;
+        const bool more = kt + 1 < KTILES;
+        compute(kt & 1, [&] {
+            if (more) swrite(nxt);
+        });
         __syncthreads();
     }
 #endif

@@ -262,6 +262,8 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
         case RC_OP_MOE: {
             int64_t Hd = D[1], E = D[2], I = D[3], topk = D[4];
             if (topk > E) return "topk exceeds the number of experts";
+            // the routing kernel stages every expert id in LDS
+            if (D[0] * topk > 32768) return "more than 32768 routed rows";
             std::string r = check_bf16_block(d, s, UP, -1, I, Hd, 2, "up");
             if (!r.empty()) return r;
             return check_bf16_block(d, s, DOWN, -1, Hd, I, 1, "down");

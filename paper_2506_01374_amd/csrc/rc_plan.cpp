@@ -104,6 +104,9 @@ std::string cache_key(const Source &s) {
     int maj = 0, min = 0;
     hiprtcVersion(&maj, &min);
     k += "\x1fhiprtc" + std::to_string(maj) + "." + std::to_string(min);
+    // the compiler behind hipRTC is identified by the library actually loaded
+    Dl_info info;
+    if (dladdr((void *)&hiprtcCompileProgram, &info) && info.dli_fname) k += "\x1f" + std::string(info.dli_fname);
     char hex[32];
     snprintf(hex, sizeof hex, "%016llx", (unsigned long long)fnv1a(k));
     return std::string(s.entry) + "_" + hex;
@@ -339,7 +342,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             Kern k0;
             k0.src = Source{SRC_aux, "rc_moe_prep", moe};
             k0.grid = dim3((unsigned)E, 1, 1);
-            k0.block = dim3(256, 1, 1);
+            k0.block = dim3(1024, 1, 1);
             k0.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
                 put(b, MoePrepArgs{a->in[1], w + offOff, w + offPerm, w + offPos, w + offTu, w + offTd});
             };
@@ -518,6 +521,48 @@ rc_status rc_precompile(const rc_op_desc *d, const rc_schedule *s, int32_t n, in
         for (int i = 0; i < n; ++i) status[i] = st[i];
     if (nfail) return fail(RC_ERR_COMPILE, std::to_string(nfail.load()) + " of " + std::to_string(n) +
                                                " schedules failed to compile or are illegal");
+    return RC_OK;
+}
+
+rc_status rc_describe(const rc_op_desc *d, const rc_schedule *s, rc_kernel_info *buf, int32_t cap,
+                      int32_t *n) {
+    if (!desc_ok(d) || !s || !n) return fail(RC_ERR_INVALID_ARGUMENT, "bad arguments");
+    std::string why = check_schedule(d, s);
+    if (!why.empty()) return fail(RC_ERR_ILLEGAL_SCHEDULE, why);
+    rc_plan p;
+    rc_status r = describe(d, s, p);
+    if (r != RC_OK) return r;
+    *n = (int32_t)p.kerns.size();
+    for (int32_t i = 0; i < *n; ++i) {
+        std::vector<char> code;
+        std::string key;
+        r = compile(p.kerns[i].src, code, key);
+        if (r != RC_OK) return r;
+        if (!buf || i >= cap) continue;
+        rc_kernel_info k;
+        memset(&k, 0, sizeof k);
+        k.struct_size = sizeof k;
+        snprintf(k.name, sizeof k.name, "%s", p.kerns[i].src.entry);
+        const Kern &kk = p.kerns[i];
+        k.grid = (int32_t)(kk.grid.x * kk.grid.y * kk.grid.z);
+        k.block = (int32_t)(kk.block.x * kk.block.y * kk.block.z);
+        k.lds_bytes = (int32_t)meta_int(code, ".group_segment_fixed_size");
+        k.vgprs = (int32_t)meta_int(code, ".vgpr_count");
+        k.agprs = (int32_t)meta_int(code, ".agpr_count");
+        k.sgprs = (int32_t)meta_int(code, ".sgpr_count");
+        k.scratch_bytes = (int32_t)meta_int(code, ".private_segment_fixed_size");
+        // Occupancy on gfx950: 512 registers (VGPR + AGPR, allocated in
+        // blocks of 8) per lane per SIMD, at most 8 waves per SIMD; LDS of
+        // 160 KiB per CU shared by the workgroups resident on it.
+        int regs = std::max(k.vgprs, 0) + std::max(k.agprs, 0);
+        regs = (regs + 7) / 8 * 8;
+        int by_regs = regs > 0 ? std::min(8, 512 / regs) : 8;
+        int waves_per_wg = (k.block + 63) / 64;
+        int wg_per_cu = k.lds_bytes > 0 ? 163840 / k.lds_bytes : 32;
+        int by_lds = std::max(1, wg_per_cu * waves_per_wg / 4);   // 4 SIMDs per CU
+        k.waves_per_simd = std::min(by_regs, by_lds);
+        buf[i] = k;
+    }
     return RC_OK;
 }
 

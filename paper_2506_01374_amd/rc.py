@@ -40,6 +40,13 @@ class rc_transform(ctypes.Structure):
     _fields_ = [("knob", ctypes.c_int32), ("value", ctypes.c_int32)]
 
 
+class rc_kernel_info(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32), ("name", ctypes.c_char * 48),
+                ("grid", ctypes.c_int32), ("block", ctypes.c_int32), ("lds_bytes", ctypes.c_int32),
+                ("vgprs", ctypes.c_int32), ("agprs", ctypes.c_int32), ("sgprs", ctypes.c_int32),
+                ("scratch_bytes", ctypes.c_int32), ("waves_per_simd", ctypes.c_int32)]
+
+
 class rc_args(ctypes.Structure):
     _fields_ = [("struct_size", ctypes.c_uint32), ("in_", ctypes.c_void_p * 8),
                 ("out", ctypes.c_void_p * 2)]
@@ -111,6 +118,9 @@ _SIGS = [
     ("rc_schedule_from_string", ctypes.c_int, [ctypes.POINTER(rc_op_desc), ctypes.c_char_p,
                                                ctypes.POINTER(rc_schedule)]),
     ("rc_schedule_hash", ctypes.c_uint64, [ctypes.POINTER(rc_schedule)]),
+    ("rc_describe", ctypes.c_int, [ctypes.POINTER(rc_op_desc), ctypes.POINTER(rc_schedule),
+                                   ctypes.POINTER(rc_kernel_info), ctypes.c_int32,
+                                   ctypes.POINTER(ctypes.c_int32)]),
     ("rc_plan_create", ctypes.c_int, [ctypes.POINTER(rc_op_desc), ctypes.POINTER(rc_schedule),
                                       ctypes.POINTER(ctypes.c_void_p)]),
     ("rc_plan_destroy", None, [ctypes.c_void_p]),
@@ -150,11 +160,32 @@ EXPORTS = [name for name, _, _ in _SIGS]
 _lib = None
 
 
+def _preload_torch_hip():
+    """Bind librc to PyTorch's bundled HIP runtime and hipRTC.
+
+    PyTorch-ROCm ships its own libamdhip64 / libhiprtc under the same sonames
+    as /opt/rocm's.  Loading them (by path, without importing torch) before
+    librc makes every HIP call in the process go through one runtime; two
+    runtimes in one process cannot both see the GPU.  The code-object cache
+    key names the hipRTC library actually loaded.
+    """
+    import importlib.util
+    spec = importlib.util.find_spec("torch")
+    if not spec or not spec.origin:
+        return
+    d = os.path.join(os.path.dirname(spec.origin), "lib")
+    for name in ("libamdhip64.so", "libhiprtc.so"):
+        path = os.path.join(d, name)
+        if os.path.exists(path):
+            ctypes.CDLL(path, mode=ctypes.RTLD_GLOBAL)
+
+
 def lib():
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"librc.so is not built ({LIB_PATH}); run __graft_entry__.build()")
+        _preload_torch_hip()
         L = ctypes.CDLL(LIB_PATH)
         for name, res, args in _SIGS:
             f = getattr(L, name)
@@ -290,6 +321,33 @@ class Schedule:
         return lib().rc_schedule_hash(ctypes.byref(self.raw))
 
 
+def _precompile_worker(job):
+    kind, dims, flags, texts, cache = job
+    if cache:
+        set_cache_dir(cache)
+    op = Op(kind, dims, flags)
+    return precompile(op, [op.from_string(t) for t in texts], nthreads=1)
+
+
+def precompile_parallel(op: Op, schedules: Sequence[Schedule], nproc: int = 8,
+                        cache_dir: Optional[str] = None) -> List[int]:
+    """rc_precompile spread over worker processes: hipRTC serialises the
+    compilations of one process, so parallel compilation needs processes."""
+    import multiprocessing as mp
+    texts = [str(s) for s in schedules]
+    if nproc <= 1 or len(texts) <= 1:
+        return precompile(op, schedules, 1)
+    chunks = [texts[i::nproc] for i in range(nproc)]
+    jobs = [(op.kind, op.dims, op.flags, c, cache_dir) for c in chunks if c]
+    with mp.get_context("spawn").Pool(len(jobs)) as pool:
+        res = pool.map(_precompile_worker, jobs)
+    out = [0] * len(texts)
+    for ci, r in enumerate(res):
+        for j, st in enumerate(r):
+            out[ci + j * nproc] = st
+    return out
+
+
 def precompile(op: Op, schedules: Sequence[Schedule], nthreads: int = 8) -> List[int]:
     n = len(schedules)
     arr = (rc_schedule * max(1, n))()
@@ -298,6 +356,18 @@ def precompile(op: Op, schedules: Sequence[Schedule], nthreads: int = 8) -> List
     st = (ctypes.c_int * max(1, n))()
     lib().rc_precompile(op.ref, arr, n, nthreads, st)
     return list(st[:n])
+
+
+def describe(op: Op, sched: Schedule) -> List[dict]:
+    """Launch shape and resources of each kernel of a schedule (no GPU)."""
+    n = ctypes.c_int32()
+    buf = (rc_kernel_info * 8)()
+    _check(lib().rc_describe(op.ref, ctypes.byref(sched.raw), buf, 8, ctypes.byref(n)), "rc_describe")
+    out = []
+    for k in buf[: n.value]:
+        out.append({f: (getattr(k, f).decode() if f == "name" else getattr(k, f))
+                    for f, _ in rc_kernel_info._fields_ if f != "struct_size"})
+    return out
 
 
 def set_cache_dir(path: Optional[str]) -> None:
@@ -359,10 +429,14 @@ class Plan:
                "rc_launch")
 
     def launch_timed(self, inputs, output, events, workspace=None, stream=None) -> None:
-        """events: list of nkernels + 1 torch.cuda.Event(enable_timing=True)."""
+        """events: list of nkernels + 1 torch.cuda.Event(enable_timing=True),
+        each already created (recorded once), since torch creates events lazily."""
         a = self._args(inputs, output)
         wsz = 0 if workspace is None else workspace.numel() * workspace.element_size()
-        evs = (ctypes.c_void_p * len(events))(*[int(e.cuda_event) for e in events])
+        handles = [int(e.cuda_event) for e in events]
+        if not all(handles):
+            raise ValueError("launch_timed: record each event once before use (torch creates events lazily)")
+        evs = (ctypes.c_void_p * len(events))(*handles)
         _check(lib().rc_launch_timed(self.h, ctypes.byref(a), _ptr(workspace), wsz,
                                      _stream_ptr(stream), evs, len(events)), "rc_launch_timed")
 

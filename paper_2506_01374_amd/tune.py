@@ -1,0 +1,250 @@
+"""Schedule tuning: run the search of Sec. 3.2 over a workload's knob space
+with the measured throughput on the GPU as the objective.
+
+Each valid sample is one distinct legal schedule compiled and timed
+(warm-ups, then repeated launches bracketed by HIP events, each after an
+overwrite of a 512 MiB buffer so no operand is cache-resident).  Its reward
+is the fraction of the operator's binding roofline reached: MFMA peak for
+contraction-bound operators, HBM bandwidth for attention (arithmetic
+intensity below the MI355X ridge point).
+
+Usage (GPU):
+  python -m paper_2506_01374_amd.tune --workload NAME --policy uct --budget 64 --seeds 0,1
+  python -m paper_2506_01374_amd.tune --workload NAME --policy exhaustive --out results/
+Usage (CPU, no GPU needed):
+  python -m paper_2506_01374_amd.tune --workload NAME --enumerate --precompile
+  python -m paper_2506_01374_amd.tune --workload NAME --replay table.jsonl --policy uct --seeds 0-19
+
+--replay evaluates against a table of measured samples (a previous run's
+JSONL); schedules missing from it count as invalid.  This reruns search
+policies over many seeds without new GPU work.
+"""
+from __future__ import annotations
+
+import argparse
+import itertools
+import json
+import math
+import os
+import sys
+import time
+from typing import Dict, List, Optional
+
+if __package__ in (None, ""):
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    __package__ = "paper_2506_01374_amd"
+
+from . import rc
+from . import workloads as W
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+POLICIES = {"random": rc.RC_POLICY_RANDOM, "uct": rc.RC_POLICY_UCT, "exhaustive": rc.RC_POLICY_EXHAUSTIVE}
+HBM_BOUND = {rc.RC_OP_ATTENTION}
+
+
+def reward_of(op: rc.Op, ms: float) -> float:
+    sec = ms * 1e-3
+    if op.kind in HBM_BOUND:
+        return op.bytes() / sec / rc.lib().rc_peak_bytes_per_s()
+    return op.flops() / sec / op.peak_flops()
+
+
+def legal_space(op: rc.Op, limit: Optional[int] = None) -> List[rc.Schedule]:
+    """Every legal schedule (cartesian product of knob values, filtered)."""
+    names = op.knob_names()
+    values = [op.knob_values(i) for i in range(len(names))]
+    out = []
+    base = op.default()
+    for combo in itertools.product(*values):
+        s = base.copy()
+        for i, v in enumerate(combo):
+            s.raw.knob[i] = v
+        if s.validate() == "":
+            out.append(s)
+            if limit and len(out) >= limit:
+                break
+    return out
+
+
+def random_walk_space(op: rc.Op, n: int, seed: int, horizon: int = 12) -> List[rc.Schedule]:
+    """n distinct schedules from random legal transformation sequences."""
+    import random
+    rng = random.Random(seed)
+    seen, out = set(), []
+    tries = 0
+    while len(out) < n and tries < 50 * n:
+        tries += 1
+        s = op.default()
+        for _ in range(horizon):
+            mv = s.moves()
+            if not mv:
+                break
+            s = s.apply(rng.choice(mv))
+        if s.hash() not in seen:
+            seen.add(s.hash())
+            out.append(s)
+    return out
+
+
+class GpuEvaluator:
+    def __init__(self, op: rc.Op, repeat: int = 10, warmup: int = 2, log=None):
+        import torch
+        self.torch = torch
+        self.op = op
+        self.host = W.host_inputs(op, seed=0)
+        self.repeat, self.warmup = repeat, warmup
+        self.cache: Dict[str, dict] = {}
+        self.log = log
+        self._dev: Dict[str, list] = {}
+        self.out = W.empty_output(op)
+
+    def _inputs(self, sched: rc.Schedule):
+        # inputs depend on the schedule only through the weight layout knobs
+        key = ",".join(f"{k}={v}" for k, v in sched.as_dict().items() if k.endswith("layout"))
+        if key not in self._dev:
+            self._dev[key] = W.to_device(W.stored_inputs(self.op, sched, self.host))
+        return self._dev[key]
+
+    def measure(self, sched: rc.Schedule) -> dict:
+        text = str(sched)
+        if text in self.cache:
+            return self.cache[text]
+        t0 = time.time()
+        rec = {"schedule": text}
+        try:
+            plan = rc.Plan(self.op, sched)
+            ws = plan.workspace()
+            t = plan.time(self._inputs(sched), self.out, ws, warmup=self.warmup, repeat=self.repeat,
+                          flush=True)
+            rec.update(valid=True, ms=t.median_ms, q1_ms=t.q1_ms, q3_ms=t.q3_ms, tflops=t.tflops,
+                       gbps=t.gbps, reward=reward_of(self.op, t.median_ms),
+                       kernel_ms=list(t.kernel_ms)[: t.nkernels])
+            del plan, ws
+        except rc.RCError as e:
+            rec.update(valid=False, error=str(e)[:300])
+        rec["eval_s"] = time.time() - t0
+        self.cache[text] = rec
+        if self.log:
+            self.log.write(json.dumps({"kind": "measure", **rec}) + "\n")
+            self.log.flush()
+        return rec
+
+
+class TableEvaluator:
+    def __init__(self, path: str):
+        self.table: Dict[str, dict] = {}
+        for line in open(path):
+            r = json.loads(line)
+            if "schedule" in r and "valid" in r:
+                self.table[r["schedule"]] = r
+
+    def measure(self, sched: rc.Schedule) -> dict:
+        return self.table.get(str(sched), {"schedule": str(sched), "valid": False, "error": "not in table"})
+
+
+def run_search(op, evaluator, policy: str, budget: int, seed: int, horizon=12, branching=2,
+               c=math.sqrt(2.0)):
+    def ev(s):
+        r = evaluator.measure(s)
+        return r["reward"] if r.get("valid") else None
+
+    srch = rc.Search(op, ev, policy=POLICIES[policy], budget=budget, horizon=horizon,
+                     branching=branching, c=c, seed=seed)
+    srch.run()
+    hist = srch.history()
+    try:
+        best, reward, idx = srch.best()
+        best_text = str(best)
+    except rc.RCError:
+        best_text, reward, idx = None, 0.0, -1
+    curve = [h["best_so_far"] for h in hist if h["valid"]]
+    # samples to reach the run's best (within 1%)
+    to_best = next((i + 1 for i, v in enumerate(curve) if v >= 0.99 * reward), None) if curve else None
+    return {"policy": policy, "seed": seed, "budget": budget, "valid": sum(h["valid"] for h in hist),
+            "invalid": sum(not h["valid"] for h in hist), "best": best_text, "best_reward": reward,
+            "best_index": idx, "samples_to_best": to_best, "curve": curve}
+
+
+def _parse_seeds(text: str) -> List[int]:
+    out = []
+    for part in text.split(","):
+        if "-" in part:
+            a, b = part.split("-")
+            out.extend(range(int(a), int(b) + 1))
+        elif part:
+            out.append(int(part))
+    return out
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--workload", required=True, choices=list(W.WORKLOADS))
+    ap.add_argument("--policy", default="uct", choices=list(POLICIES) + ["list"])
+    ap.add_argument("--budget", type=int, default=64)
+    ap.add_argument("--seeds", default="0")
+    ap.add_argument("--horizon", type=int, default=12)
+    ap.add_argument("--branching", type=int, default=2)
+    ap.add_argument("--c", type=float, default=math.sqrt(2.0))
+    ap.add_argument("--repeat", type=int, default=10)
+    ap.add_argument("--out", default="tune_out")
+    ap.add_argument("--enumerate", action="store_true", help="list the whole legal space")
+    ap.add_argument("--walks", type=int, default=0, help="list N random-walk schedules")
+    ap.add_argument("--precompile", action="store_true", help="compile the listed schedules (CPU)")
+    ap.add_argument("--list-file", default=None, help="measure the schedules in this file (policy list)")
+    ap.add_argument("--replay", default=None, help="evaluate against a measured JSONL table")
+    ap.add_argument("--threads", type=int, default=os.cpu_count() or 8)
+    ap.add_argument("--cache-dir", default=os.path.join(HERE, "jit_cache"))
+    args = ap.parse_args(argv)
+
+    rc.set_cache_dir(args.cache_dir)
+    op = W.workload_op(args.workload)
+    os.makedirs(args.out, exist_ok=True)
+
+    if args.enumerate or args.walks:
+        space = legal_space(op) if args.enumerate else random_walk_space(op, args.walks, 12345)
+        path = os.path.join(args.out, f"{args.workload}.space.txt")
+        with open(path, "w") as f:
+            for s in space:
+                f.write(str(s) + "\n")
+        print(f"{len(space)} legal schedules -> {path}", flush=True)
+        if args.precompile:
+            t0 = time.time()
+            chunk = 256
+            bad = 0
+            for i in range(0, len(space), chunk):
+                st = rc.precompile_parallel(op, space[i:i + chunk], args.threads, args.cache_dir)
+                bad += sum(1 for x in st if x != 0)
+                print(f"compiled {min(i + chunk, len(space))}/{len(space)} ({bad} rejected) "
+                      f"{time.time() - t0:.0f}s", flush=True)
+        return
+
+    log = open(os.path.join(args.out, f"{args.workload}.{args.policy}.jsonl"), "a")
+    if args.replay:
+        evaluator = TableEvaluator(args.replay)
+    else:
+        evaluator = GpuEvaluator(op, repeat=args.repeat, log=log)
+
+    if args.policy == "list":
+        scheds = [op.from_string(line.strip()) for line in open(args.list_file) if line.strip()]
+        t0 = time.time()
+        for i, s in enumerate(scheds):
+            r = evaluator.measure(s)
+            if (i + 1) % 25 == 0 or i + 1 == len(scheds):
+                print(f"measured {i + 1}/{len(scheds)} {time.time() - t0:.0f}s", flush=True)
+        best = max((r for r in evaluator.cache.values() if r.get("valid")), key=lambda r: r["reward"],
+                   default=None)
+        print(json.dumps({"kind": "list_best", "workload": args.workload, **(best or {})}), flush=True)
+        log.write(json.dumps({"kind": "list_best", "workload": args.workload, **(best or {})}) + "\n")
+        return
+
+    for seed in _parse_seeds(args.seeds):
+        t0 = time.time()
+        res = run_search(op, evaluator, args.policy, args.budget, seed, args.horizon, args.branching, args.c)
+        res.update(workload=args.workload, kind="search", wall_s=time.time() - t0)
+        log.write(json.dumps(res) + "\n")
+        log.flush()
+        print(json.dumps({k: v for k, v in res.items() if k != "curve"}), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,186 @@
+"""CPU tests of the search driver (Sec. 3.2) against fake evaluators, and of
+the report metrics against Table 1."""
+import csv
+import math
+import os
+
+import pytest
+
+from paper_2506_01374_amd import rc, report
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+C = math.sqrt(2.0)
+
+
+def tiny_op():
+    # fp32 GEMM 16x16x4: only stages {1,2} x layout {0,1} are legal.
+    return rc.Op(rc.RC_OP_GEMM_F32, (16, 16, 4))
+
+
+def test_tiny_space_has_four_points():
+    op = tiny_op()
+    from paper_2506_01374_amd.tune import legal_space
+    pts = {(s["stages"], s["layout"]) for s in legal_space(op)}
+    assert pts == {(1, 0), (2, 0), (1, 1), (2, 1)}
+
+
+def test_uct_selection_and_backprop_match_hand_computation():
+    op = tiny_op()
+    rewards = {(2, 0): 0.3, (1, 1): 0.5, (2, 1): 0.9, (1, 0): 0.1}
+    evals = []
+
+    def ev(s):
+        evals.append((s["stages"], s["layout"]))
+        return rewards[(s["stages"], s["layout"])]
+
+    # The proposer fixes expansion order: child A = stages 2, child B = layout 1.
+    prop = lambda at, par, gpar: "ComputeLocation(stages=2);Layout(layout=1)"
+    s = rc.Search(op, ev, policy=rc.RC_POLICY_UCT, budget=3, horizon=1, branching=2, c=C, seed=0,
+                  propose=prop)
+    A = [op.parse("ComputeLocation(stages=2)")]
+    B = [op.parse("Layout(layout=1)")]
+    s.step()
+    s.step()
+    assert evals == [(2, 0), (1, 1)]
+    assert s.node_stats(A) == (1, pytest.approx(0.3))
+    assert s.node_stats(B) == (1, pytest.approx(0.5))
+    assert s.node_stats([]) == (2, pytest.approx(0.8))
+    # Iteration 3: both children visited once; UCT = W/N + c sqrt(ln 2 / 1) -> B.
+    s.step()
+    assert s.node_stats(B) == (2, pytest.approx(1.0))
+    # Iteration 4: UCT_A = 0.3 + c sqrt(ln 3 / 1) = 1.782 > UCT_B = 0.5 + c sqrt(ln 3 / 2) = 1.548.
+    ua = 0.3 + C * math.sqrt(math.log(3) / 1)
+    ub = 0.5 + C * math.sqrt(math.log(3) / 2)
+    assert ua > ub
+    s.step()
+    assert s.node_stats(A) == (2, pytest.approx(0.6))
+    # Iteration 5: UCT_A = 0.3 + c sqrt(ln 4 / 2) < UCT_B = 0.5 + c sqrt(ln 4 / 2) -> B.
+    s.step()
+    assert s.node_stats(B) == (3, pytest.approx(1.5))
+    assert s.node_stats([]) == (5, pytest.approx(0.3 + 0.5 + 0.5 + 0.3 + 0.5))
+    # Re-selected leaves are not measured again (dedupe): two evaluations only.
+    assert evals == [(2, 0), (1, 1)]
+    assert s.fallbacks() == 0
+
+
+def test_fallback_when_no_proposal_is_valid():
+    op = tiny_op()
+    calls = []
+    prop = lambda at, par, gpar: "Make it faster please;TileSize(tile_m=48);Unroll(layout=1)"
+    s = rc.Search(op, lambda x: calls.append(1) or 0.5, policy=rc.RC_POLICY_UCT, budget=3,
+                  horizon=2, branching=2, seed=1, propose=prop)
+    s.run()
+    assert s.fallbacks() >= 2          # every expansion fell back to a random legal move
+    best, r, _ = s.best()
+    assert r == 0.5
+
+
+def synthetic_reward(s):
+    # a smooth, single-peaked function of the knobs of the fp32 GEMM
+    d = s.as_dict()
+    return (1.0 / (1 + abs(math.log2(d["tile_m"]) - 5)) * 1.0 / (1 + abs(math.log2(d["tile_n"]) - 6))
+            * (1.2 if d["stages"] == 2 else 1.0) * (1.1 if d["vec"] == 4 else 1.0)
+            * (1.0 + 0.05 * math.log2(d["tile_k"])) / (1 + 0.1 * d["unroll"]))
+
+
+def test_exhaustive_finds_global_best_and_uct_random_approach_it():
+    op = rc.Op(rc.RC_OP_GEMM_F32, (128, 128, 128))
+    ex = rc.Search(op, synthetic_reward, policy=rc.RC_POLICY_EXHAUSTIVE, budget=100000).run()
+    hist = ex.history()
+    assert len(hist) == 1716                      # the whole legal space, once each
+    best, r_ex, _ = ex.best()
+    assert r_ex == pytest.approx(max(h["reward"] for h in hist))
+    for pol in (rc.RC_POLICY_UCT, rc.RC_POLICY_RANDOM):
+        bests = []
+        for seed in range(3):
+            s = rc.Search(op, synthetic_reward, policy=pol, budget=300, seed=seed).run()
+            _, r, _ = s.best()
+            assert r <= r_ex + 1e-12
+            bests.append(r)
+        assert max(bests) >= 0.9 * r_ex
+
+
+def test_uct_reaches_the_optimum_of_a_tiny_space():
+    op = tiny_op()
+    rewards = {(2, 0): 0.3, (1, 1): 0.5, (2, 1): 0.9, (1, 0): 0.1}
+    for seed in range(5):
+        s = rc.Search(op, lambda x: rewards[(x["stages"], x["layout"])], policy=rc.RC_POLICY_UCT,
+                      budget=4, horizon=2, seed=seed).run()
+        _, r, _ = s.best()
+        assert r == 0.9
+
+
+def test_dedupe_monotone_best_and_determinism():
+    op = rc.Op(rc.RC_OP_GEMM_F32, (128, 128, 128))
+    runs = []
+    for seed in (7, 7, 8):
+        s = rc.Search(op, synthetic_reward, policy=rc.RC_POLICY_UCT, budget=60, seed=seed).run()
+        h = s.history()
+        valid = [x for x in h if x["valid"]]
+        assert len(valid) == 60
+        assert len({str(x["schedule"]) for x in valid}) == 60          # no schedule measured twice
+        curve = [x["best_so_far"] for x in valid]
+        assert curve == report.best_so_far([x["reward"] for x in valid])
+        runs.append([str(x["schedule"]) for x in valid])
+    assert runs[0] == runs[1] and runs[0] != runs[2]
+
+
+def test_invalid_samples_cost_no_budget_and_keep_the_tree_consistent():
+    op = rc.Op(rc.RC_OP_GEMM_F32, (128, 128, 128))
+
+    def flaky(s):
+        if s["vec"] == 4:
+            raise RuntimeError("simulated compile failure")
+        if s["layout"] == 1:
+            return None
+        return synthetic_reward(s)
+
+    s = rc.Search(op, flaky, policy=rc.RC_POLICY_UCT, budget=40, seed=3).run()
+    h = s.history()
+    assert sum(x["valid"] for x in h) == 40
+    assert all(x["schedule"]["vec"] != 4 and x["schedule"]["layout"] != 1 for x in h if x["valid"])
+    assert any(not x["valid"] for x in h)
+    assert s.node_stats([])[0] == len([x for x in h]) or s.node_stats([])[0] >= 40
+
+
+def test_all_invalid_space_ends_cleanly():
+    op = rc.Op(rc.RC_OP_GEMM_F32, (128, 128, 128))
+    s = rc.Search(op, lambda x: None, policy=rc.RC_POLICY_RANDOM, budget=10, max_invalid=25).run()
+    h = s.history()
+    assert all(not x["valid"] for x in h) and len(h) == 26
+    with pytest.raises(rc.RCError):
+        s.best()
+
+
+def test_report_metrics_reproduce_table1():
+    rows = []
+    with open(os.path.join(HERE, "golden", "table1_layerwise.csv")) as f:
+        lines = [l for l in f if not l.startswith("#")]
+    for r in csv.DictReader(lines):
+        rows.append(r)
+    body, gm = rows[:-1], rows[-1]
+    assert len(body) == 25
+    off = 0
+    for r in body:
+        red = report.sample_reduction(float(r["tvm_n"]), float(r["rc_n"]))
+        gain = report.efficiency_gain(float(r["rc_s"]), float(r["rc_n"]), float(r["tvm_s"]),
+                                      float(r["tvm_n"]))
+        # printed speedups carry one decimal, so derived columns agree to rounding
+        assert abs(red - float(r["red"])) <= 0.051
+        if abs(gain - float(r["gain"])) > 0.051:
+            off += 1
+            assert abs(gain - float(r["gain"])) <= 0.25
+    assert off <= 4
+    assert round(report.geomean(float(r["tvm_s"]) for r in body), 1) == float(gm["tvm_s"])
+    assert round(report.geomean(float(r["rc_s"]) for r in body), 1) == float(gm["rc_s"])
+    assert round(report.geomean(float(r["red"]) for r in body), 1) == float(gm["red"])
+    assert round(report.geomean(float(r["gain"]) for r in body), 1) == float(gm["gain"])
+
+
+def test_report_helpers():
+    assert report.speedup(10.0, 2.0) == 5.0
+    assert report.sample_efficiency(12.1, 200) == pytest.approx(0.0605)
+    assert report.best_so_far([1, 3, 2, 5, 4]) == [1, 3, 3, 5, 5]
+    assert report.samples_to_reach([1, 3, 3, 5, 5], 4) == 4
+    assert report.samples_to_reach([1, 2], 4) is None
+    assert report.mean_curve([[1, 2, 3], [3, 4]]) == [2, 3]
