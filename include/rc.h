@@ -132,7 +132,7 @@ double rc_peak_bytes_per_s(void);
 /* Schedules and transformations (Sec. 2, Eq. 1; App. A)              */
 /* ------------------------------------------------------------------ */
 
-#define RC_MAX_KNOBS 24
+#define RC_MAX_KNOBS 32
 
 typedef struct rc_schedule {
     uint32_t struct_size;

@@ -11,7 +11,10 @@
 //   VEC          bf16 per global load of K (Vectorize)
 //   UNROLL       unroll factor of the key-tile loop (Unroll)
 //   ORDER        0: query tiles in order; 1: longest (last) query tiles
-//                first, which balances causal work across the grid
+//                first; 2: paired - workgroup b and b + half take query
+//                tiles t and NQT-1-t, so that co-resident pairs carry equal
+//                causal work
+//   OCC          waves per SIMD the register allocation must leave room for
 //   AB AH AS AD  batch, heads, sequence length, head dim
 //   CAUSAL       top-left aligned causal mask (key j visible iff j <= i)
 //   SCALE_LOG2   log2(e) / sqrt(AD): scores are kept in log2 units
@@ -108,7 +111,8 @@ __device__ __forceinline__ float group_sum(float v) {
     return v + __shfl_xor(v, 32);
 }
 
-extern "C" __global__ __launch_bounds__(NT) void rc_attention(AttnArgs args) {
+extern "C" __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
+void rc_attention(AttnArgs args) {
     __shared__ __attribute__((aligned(16))) bf16_t Ks[STAGES][BN * AD];
     __shared__ __attribute__((aligned(16))) bf16_t Vt[STAGES][AD * VTS];
 
@@ -116,6 +120,10 @@ extern "C" __global__ __launch_bounds__(NT) void rc_attention(AttnArgs args) {
     const int bid = blockIdx.x;
 #if ORDER == 1
     const int qt = NQT - 1 - bid / (AB * AH);
+    const int bh = bid % (AB * AH);
+#elif ORDER == 2
+    const int half = (NQT / 2) * AB * AH;
+    const int qt = bid < half ? NQT - 1 - bid / (AB * AH) : (bid - half) / (AB * AH);
     const int bh = bid % (AB * AH);
 #else
     const int qt = bid % NQT;
@@ -206,42 +214,55 @@ extern "C" __global__ __launch_bounds__(NT) void rc_attention(AttnArgs args) {
 #if CAUSAL
         if (kt * BN > q0w + RPW - 1) return;     // every key of the tile is masked for this wave
 #endif
+        // S^T = K Q^T for every query block; each K fragment is read once
+        accT sc[QB][KB];
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
-            accT sc[KB];
-#pragma unroll
-            for (int kb = 0; kb < KB; ++kb) {
-#pragma unroll
-                for (int r = 0; r < ACCN; ++r) sc[kb][r] = 0.f;
-#pragma unroll
-                for (int ks = 0; ks < AD / KSTEP; ++ks) {
-                    bf16x8 kf = *(const bf16x8 *)(Ks[s] + kswz(kb * MF + lane % MF, ks * (KSTEP / 8) + lane / MF));
-                    sc[kb] = mfma(kf, qf[qb][ks], sc[kb]);
-                }
-            }
-            const int q = q0w + qb * MF + lane % MF;
-            float mx = -__builtin_inff();
+        for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
             for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-                for (int r = 0; r < ACCN; ++r) {
-                    float t = sc[kb][r] * SCALE_LOG2;
+                for (int r = 0; r < ACCN; ++r) sc[qb][kb][r] = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+            for (int ks = 0; ks < AD / KSTEP; ++ks) {
+                bf16x8 kf = *(const bf16x8 *)(Ks[s] + kswz(kb * MF + lane % MF, ks * (KSTEP / 8) + lane / MF));
+#pragma unroll
+                for (int qb = 0; qb < QB; ++qb) sc[qb][kb] = mfma(kf, qf[qb][ks], sc[qb][kb]);
+            }
+        // online softmax, one query per lane; m is kept in log2 units and the
+        // scale is folded into the exponent's fused multiply-add
 #if CAUSAL
-                    if (kt * BN + kb * MF + key_of(r, lane) > q) t = -__builtin_inff();
+        // only a tile that crosses this wave's diagonal needs the mask
+        const bool diag = kt * BN + BN - 1 > q0w;
 #endif
-                    sc[kb][r] = t;
-                    mx = fmaxf(mx, t);
-                }
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+            float mx = -__builtin_inff();
+#if CAUSAL
+            if (diag) {
+                const int q = q0w + qb * MF + lane % MF;
+#pragma unroll
+                for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                    for (int r = 0; r < ACCN; ++r)
+                        if (kt * BN + kb * MF + key_of(r, lane) > q) sc[qb][kb][r] = -__builtin_inff();
+            }
+#endif
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int r = 0; r < ACCN; ++r) mx = fmaxf(mx, sc[qb][kb][r]);
             mx = group_max(mx);
-            const float mnew = fmaxf(m[qb], mx);
+            const float mnew = fmaxf(m[qb], mx * SCALE_LOG2);
             const float alpha = __builtin_amdgcn_exp2f(m[qb] - mnew);
             float ps = 0.f;
 #pragma unroll
             for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
                 for (int r = 0; r < ACCN; ++r) {
-                    float p = __builtin_amdgcn_exp2f(sc[kb][r] - mnew);
-                    sc[kb][r] = p;
+                    float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[qb][kb][r], SCALE_LOG2, -mnew));
+                    sc[qb][kb][r] = p;
                     ps += p;
                 }
             ps = group_sum(ps);
@@ -251,35 +272,43 @@ extern "C" __global__ __launch_bounds__(NT) void rc_attention(AttnArgs args) {
             for (int db = 0; db < DB; ++db)
 #pragma unroll
                 for (int r = 0; r < ACCN; ++r) o[qb][db][r] *= alpha;
-            // O^T += V^T P^T, KSTEP keys per MFMA.
+        }
+        // O^T += V^T P^T, KSTEP keys per MFMA; each V^T fragment is read once
 #pragma unroll
-            for (int j = 0; j < BN / KSTEP; ++j) {
-                bf16x8 pf;
+        for (int j = 0; j < BN / KSTEP; ++j) {
+            bf16x8 pf[QB];
+#if MF == 16
+            const int c0 = 32 * j + 4 * (lane >> 4), c1 = c0 + 16;
+#else
+            const int kb = j >> 1, hf = (j & 1) * 8;
+            const int c0 = kb * 32 + (j & 1) * 16 + 4 * (lane >> 5), c1 = c0 + 8;
+#endif
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) {
                 u32x4 pw;
 #if MF == 16
-                pw[0] = pack2(sc[2 * j][0], sc[2 * j][1]);
-                pw[1] = pack2(sc[2 * j][2], sc[2 * j][3]);
-                pw[2] = pack2(sc[2 * j + 1][0], sc[2 * j + 1][1]);
-                pw[3] = pack2(sc[2 * j + 1][2], sc[2 * j + 1][3]);
-                const int c0 = 32 * j + 4 * (lane >> 4), c1 = c0 + 16;
+                pw[0] = pack2(sc[qb][2 * j][0], sc[qb][2 * j][1]);
+                pw[1] = pack2(sc[qb][2 * j][2], sc[qb][2 * j][3]);
+                pw[2] = pack2(sc[qb][2 * j + 1][0], sc[qb][2 * j + 1][1]);
+                pw[3] = pack2(sc[qb][2 * j + 1][2], sc[qb][2 * j + 1][3]);
 #else
-                const int kb = j >> 1, hf = (j & 1) * 8;
-                pw[0] = pack2(sc[kb][hf + 0], sc[kb][hf + 1]);
-                pw[1] = pack2(sc[kb][hf + 2], sc[kb][hf + 3]);
-                pw[2] = pack2(sc[kb][hf + 4], sc[kb][hf + 5]);
-                pw[3] = pack2(sc[kb][hf + 6], sc[kb][hf + 7]);
-                const int c0 = kb * 32 + (j & 1) * 16 + 4 * (lane >> 5), c1 = c0 + 8;
+                pw[0] = pack2(sc[qb][kb][hf + 0], sc[qb][kb][hf + 1]);
+                pw[1] = pack2(sc[qb][kb][hf + 2], sc[qb][kb][hf + 3]);
+                pw[2] = pack2(sc[qb][kb][hf + 4], sc[qb][kb][hf + 5]);
+                pw[3] = pack2(sc[qb][kb][hf + 6], sc[qb][kb][hf + 7]);
 #endif
-                pf = __builtin_bit_cast(bf16x8, pw);
+                pf[qb] = __builtin_bit_cast(bf16x8, pw);
+            }
 #pragma unroll
-                for (int db = 0; db < DB; ++db) {
-                    const int drow = db * MF + lane % MF;
-                    u32x4 vw;
-                    u32x2 a = *(const u32x2 *)(Vt[s] + drow * VTS + c0);
-                    u32x2 b = *(const u32x2 *)(Vt[s] + drow * VTS + c1);
-                    vw[0] = a[0]; vw[1] = a[1]; vw[2] = b[0]; vw[3] = b[1];
-                    o[qb][db] = mfma(__builtin_bit_cast(bf16x8, vw), pf, o[qb][db]);
-                }
+            for (int db = 0; db < DB; ++db) {
+                const int drow = db * MF + lane % MF;
+                u32x4 vw;
+                u32x2 a = *(const u32x2 *)(Vt[s] + drow * VTS + c0);
+                u32x2 b = *(const u32x2 *)(Vt[s] + drow * VTS + c1);
+                vw[0] = a[0]; vw[1] = a[1]; vw[2] = b[0]; vw[3] = b[1];
+                const bf16x8 vf = __builtin_bit_cast(bf16x8, vw);
+#pragma unroll
+                for (int qb = 0; qb < QB; ++qb) o[qb][db] = mfma(vf, pf[qb], o[qb][db]);
             }
         }
     };

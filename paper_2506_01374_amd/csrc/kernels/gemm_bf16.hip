@@ -9,12 +9,15 @@
 //   MF           MFMA shape: 16 -> v_mfma_f32_16x16x32_bf16,
 //                             32 -> v_mfma_f32_32x32x16_bf16
 //   STAGES       1: load, store, compute; 2: LDS double buffer with register
-//                prefetch of the next K tile (ComputeLocation)
+//                prefetch of the next K tile, stored to LDS after the tile's
+//                MFMAs; 3: the same, stored half-way through the MFMAs
+//                (ComputeLocation)
 //   VEC          bf16 elements per global load: 2, 4 or 8 (Vectorize)
 //   UNROLL       unroll factor of the K-tile loop (Unroll)
 //   LAYOUT       weights stored 0: [K][N], 1: [N][K] (Layout)
 //   GRID         0: tile n fastest; 1: tile m fastest, with workgroups
 //                regrouped so each XCD owns a contiguous range of tiles
+//   OCC          waves per SIMD the register allocation must leave room for
 //   NB           weight operands sharing the A tile (1, or 2 for gate/up)
 //   AMODE        A rows: 0 dense [GM][GK]; 1 MoE gather (row p of expert e
 //                reads X[perm[p] / TOPK]); 2 implicit im2col of an NHWC
@@ -114,9 +117,11 @@ __device__ __forceinline__ bf16_t vec_elem(const vecT &v, int j) {
 #endif
 }
 
-extern "C" __global__ __launch_bounds__(NT) void rc_gemm_bf16(GemmBf16Args args) {
-    __shared__ __attribute__((aligned(16))) bf16_t As[STAGES][TM * TK];
-    __shared__ __attribute__((aligned(16))) bf16_t Bs[STAGES][NB][TN * TK];
+extern "C" __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
+void rc_gemm_bf16(GemmBf16Args args) {
+#define NBUF (STAGES > 1 ? 2 : 1)
+    __shared__ __attribute__((aligned(16))) bf16_t As[NBUF][TM * TK];
+    __shared__ __attribute__((aligned(16))) bf16_t Bs[NBUF][NB][TN * TK];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -326,9 +331,14 @@ extern "C" __global__ __launch_bounds__(NT) void rc_gemm_bf16(GemmBf16Args args)
         if (kt + 1 < KTILES) gload((kt + 1) * TK);
         const int nxt = (kt + 1) & 1;
         const bool more = kt + 1 < KTILES;
+#if STAGES == 3
         compute(kt & 1, [&] {
             if (more) swrite(nxt);
         });
+#else
+        compute(kt & 1, nothing);
+        if (more) swrite(nxt);
+#endif
         __syncthreads();
     }
 #endif

@@ -40,7 +40,7 @@ static std::vector<KnobDef> gemm_f32_knobs() {
 }
 
 // One bf16 GEMM stage's knobs, names prefixed ("" / "up." / "down.").
-static void add_gemm_block(std::vector<KnobDef> &v, const char *const names[11],
+static void add_gemm_block(std::vector<KnobDef> &v, const char *const names[12],
                            std::vector<int32_t> tile_n_vals, std::vector<int32_t> tile_k_vals) {
     v.push_back({names[0], "TileSize", {16, 32, 64, 128, 256}, 16});
     v.push_back({names[1], "TileSize", tile_n_vals, 16});
@@ -48,21 +48,22 @@ static void add_gemm_block(std::vector<KnobDef> &v, const char *const names[11],
     v.push_back({names[3], "Parallel", {1, 2, 4}, 1});
     v.push_back({names[4], "Parallel", {1, 2, 4}, 1});
     v.push_back({names[5], "TileSize", {16, 32}, 16});          // MFMA instruction shape
-    v.push_back({names[6], "ComputeLocation", {1, 2}, 1});      // LDS stages
+    v.push_back({names[6], "ComputeLocation", {1, 2, 3}, 1});   // LDS staging of the next K tile
     v.push_back({names[7], "Vectorize", {2, 4, 8}, 2});         // bf16 per global load
     v.push_back({names[8], "Unroll", {1, 2}, 1});
     v.push_back({names[9], "Layout", {0, 1}, 0});               // weight stored KxN / NxK
     v.push_back({names[10], "Parallel", {0, 1}, 0});            // tile order: plain / XCD-grouped
+    v.push_back({names[11], "Parallel", {1, 2}, 1});            // waves per SIMD to budget registers for
 }
 
-static const char *const PLAIN[11] = {"tile_m", "tile_n", "tile_k", "waves_m", "waves_n", "mfma",
-                                      "stages", "vec", "unroll", "layout", "grid"};
-static const char *const UP[11] = {"up.tile_m", "up.tile_n", "up.tile_k", "up.waves_m",
+static const char *const PLAIN[12] = {"tile_m", "tile_n", "tile_k", "waves_m", "waves_n", "mfma",
+                                      "stages", "vec", "unroll", "layout", "grid", "occ"};
+static const char *const UP[12] = {"up.tile_m", "up.tile_n", "up.tile_k", "up.waves_m",
                                    "up.waves_n", "up.mfma", "up.stages", "up.vec", "up.unroll",
-                                   "up.layout", "up.grid"};
-static const char *const DOWN[11] = {"down.tile_m", "down.tile_n", "down.tile_k", "down.waves_m",
+                                   "up.layout", "up.grid", "up.occ"};
+static const char *const DOWN[12] = {"down.tile_m", "down.tile_n", "down.tile_k", "down.waves_m",
                                      "down.waves_n", "down.mfma", "down.stages", "down.vec",
-                                     "down.unroll", "down.layout", "down.grid"};
+                                     "down.unroll", "down.layout", "down.grid", "down.occ"};
 
 static std::vector<KnobDef> mlp_knobs() {
     std::vector<KnobDef> v;
@@ -90,7 +91,8 @@ static std::vector<KnobDef> attention_knobs() {
         {"stages", "ComputeLocation", {1, 2}, 1},
         {"vec", "Vectorize", {2, 4, 8}, 2},
         {"unroll", "Unroll", {1, 2}, 1},
-        {"order", "Parallel", {0, 1}, 0},
+        {"order", "Parallel", {0, 1, 2}, 0},
+        {"occ", "Parallel", {1, 2}, 1},
     };
 }
 
@@ -159,7 +161,7 @@ static const int64_t LDS_LIMIT = 163840;   // bytes one workgroup may allocate o
 // Rules for one bf16 GEMM stage of shape M x N x K (M < 0: ragged rows,
 // predicated), NB weight operands sharing the A tile.
 static std::string check_bf16_block(const rc_op_desc *d, const rc_schedule *s,
-                                    const char *const names[11], int64_t M, int64_t N, int64_t K,
+                                    const char *const names[12], int64_t M, int64_t N, int64_t K,
                                     int NB, const char *tag) {
     int tm = kv(d, s, names[0]), tn = kv(d, s, names[1]), tk = kv(d, s, names[2]);
     int wm = kv(d, s, names[3]), wn = kv(d, s, names[4]), mf = kv(d, s, names[5]);
@@ -184,11 +186,19 @@ static std::string check_bf16_block(const rc_op_desc *d, const rc_schedule *s,
         return fmt("%s: B tile %dx%d does not split into %d threads x %d-wide loads", tag, tk, tn,
                    nt, vec);
     if (lay == 0 && tn % vec) return fmt("%s: vec %d does not divide tile_n %d", tag, vec, tn);
-    int64_t lds = (int64_t)st * ((int64_t)tm * tk + (int64_t)NB * tn * tk) * 2;
+    int64_t lds = (int64_t)(st > 1 ? 2 : 1) * ((int64_t)tm * tk + (int64_t)NB * tn * tk) * 2;
     if (lds > LDS_LIMIT)
         return fmt("%s: LDS %lld B exceeds %lld B", tag, (long long)lds, (long long)LDS_LIMIT);
     int64_t acc = (int64_t)NB * tm * tn / nt;
     if (acc > 256) return fmt("%s: %lld accumulators per lane exceed 256", tag, (long long)acc);
+    int occ = kv(d, s, names[11]);
+    if (occ > 1) {
+        // occ waves per SIMD: the registers of occ waves share 512 per lane,
+        // and enough workgroups must fit in the CU's LDS.
+        if (acc > 512 / occ - 32) return fmt("%s: %lld accumulators leave no registers at %d waves/SIMD", tag, (long long)acc, occ);
+        int64_t waves = (int64_t)wm * wn, wgs = (occ * 4 + waves - 1) / waves;
+        if (wgs * lds > LDS_LIMIT) return fmt("%s: %lld workgroups of %lld B LDS do not fit a CU", tag, (long long)wgs, (long long)lds);
+    }
     int64_t stage_regs = st > 1 ? ((int64_t)tm * tk + (int64_t)NB * tn * tk) / (2 * nt) : 0;
     if (acc + stage_regs > 384)
         return fmt("%s: %lld accumulator + %lld staging registers per lane exceed 384", tag,
@@ -247,10 +257,20 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
             // must hold a power-of-two number of chunks
             if (Dh != 32 && Dh != 64 && Dh != 128 && Dh != 256)
                 return fmt("head dim %lld must be 32, 64, 128 or 256", (long long)Dh);
-            int64_t lds = (int64_t)st * (2 * bn * (Dh + 8) * 2);
+            int64_t lds = (int64_t)st * ((int64_t)bn * Dh + Dh * (bn + 4)) * 2;   // K tile + padded V^T tile
             if (lds > LDS_LIMIT) return fmt("LDS %lld B exceeds limit", (long long)lds);
             int64_t regs = (int64_t)rpw * Dh / 64 + (int64_t)bn * rpw / 64 + (int64_t)rpw * Dh / 128;
             if (regs > 320) return fmt("%lld registers per lane for O, S and Q exceed 320", (long long)regs);
+            int occ = kv(d, s, "occ");
+            if (occ > 1) {
+                if (regs > 512 / occ - 64)
+                    return fmt("%lld registers per lane for O, S and Q leave too few at %d waves/SIMD", (long long)regs, occ);
+                int64_t wgs = (occ * 4 + w - 1) / w;
+                if (wgs * lds > LDS_LIMIT)
+                    return fmt("%lld workgroups of %lld B LDS do not fit a CU", (long long)wgs, (long long)lds);
+            }
+            if (kv(d, s, "order") == 2 && (S / bm) % 2)
+                return "paired tile order needs an even number of query tiles";
             return "";
         }
         case RC_OP_GATED_MLP: {

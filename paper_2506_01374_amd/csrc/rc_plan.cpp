@@ -208,13 +208,13 @@ struct WsLayout {
 };
 
 struct GemmCfg {
-    int tm, tn, tk, wm, wn, mf, st, vec, un, lay, grid;
+    int tm, tn, tk, wm, wn, mf, st, vec, un, lay, grid, occ;
 };
 
 GemmCfg read_block(const rc_op_desc *d, const rc_schedule *s, const char *prefix) {
     auto k = [&](const char *n) { return kv(d, s, (std::string(prefix) + n).c_str()); };
     return GemmCfg{k("tile_m"), k("tile_n"), k("tile_k"), k("waves_m"), k("waves_n"), k("mfma"),
-                   k("stages"), k("vec"), k("unroll"), k("layout"), k("grid")};
+                   k("stages"), k("vec"), k("unroll"), k("layout"), k("grid"), k("occ")};
 }
 
 std::string gemm_defs(const GemmCfg &g, int nb, int amode, int epi, long gm, long gn, long gk) {
@@ -222,7 +222,7 @@ std::string gemm_defs(const GemmCfg &g, int nb, int amode, int epi, long gm, lon
     s += def("TM", g.tm) + def("TN", g.tn) + def("TK", g.tk) + def("WM", g.wm) + def("WN", g.wn);
     s += def("MF", g.mf) + def("STAGES", g.st) + def("VEC", g.vec) + def("UNROLL", g.un);
     s += def("LAYOUT", g.lay) + def("GRID", g.grid) + def("NB", nb) + def("AMODE", amode);
-    s += def("EPI", epi) + def("GM", gm) + def("GN", gn) + def("GK", gk);
+    s += def("EPI", epi) + def("GM", gm) + def("GN", gn) + def("GK", gk) + def("OCC", g.occ);
     return s;
 }
 
@@ -437,7 +437,8 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
                            def("BM", bm) + def("BN", kv(d, s, "block_n")) + def("NW", w) +
                                def("MF", kv(d, s, "mfma")) + def("STAGES", kv(d, s, "stages")) +
                                def("VEC", kv(d, s, "vec")) + def("UNROLL", kv(d, s, "unroll")) +
-                               def("ORDER", kv(d, s, "order")) + def("AB", B) + def("AH", Hh) +
+                               def("ORDER", kv(d, s, "order")) + def("OCC", kv(d, s, "occ")) +
+                               def("AB", B) + def("AH", Hh) +
                                def("AS", S) + def("AD", Dh) +
                                def("CAUSAL", (d->flags & RC_FLAG_CAUSAL) ? 1 : 0) + sbuf};
             k.grid = dim3((unsigned)(B * Hh * (S / bm)), 1, 1);

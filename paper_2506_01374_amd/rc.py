@@ -22,7 +22,7 @@ STATUS = {0: "RC_OK", 1: "RC_ERR_INVALID_ARGUMENT", 2: "RC_ERR_ILLEGAL_SCHEDULE"
 RC_OP_GEMM_F32, RC_OP_ATTENTION, RC_OP_GATED_MLP, RC_OP_MOE, RC_OP_CONV2D = 1, 2, 3, 4, 5
 RC_FLAG_CAUSAL = 1
 RC_POLICY_RANDOM, RC_POLICY_UCT, RC_POLICY_EXHAUSTIVE = 0, 1, 2
-MAX_DIMS, MAX_KNOBS = 8, 24
+MAX_DIMS, MAX_KNOBS = 8, 32
 
 
 class rc_op_desc(ctypes.Structure):

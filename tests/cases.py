@@ -23,11 +23,11 @@ SMALL = {
 }
 
 _GEMM_BLOCK = ("tile_m", "tile_n", "tile_k", "waves_m", "waves_n", "mfma", "stages", "vec",
-               "unroll", "layout", "grid")
+               "unroll", "layout", "grid", "occ")
 
 
-def _block(prefix, tm, tn, tk, wm, wn, mf, st, vec, un, lay, grid):
-    vals = (tm, tn, tk, wm, wn, mf, st, vec, un, lay, grid)
+def _block(prefix, tm, tn, tk, wm, wn, mf, st, vec, un, lay, grid, occ=1):
+    vals = (tm, tn, tk, wm, wn, mf, st, vec, un, lay, grid, occ)
     return ",".join(f"{prefix}{k}={v}" for k, v in zip(_GEMM_BLOCK, vals))
 
 
@@ -56,6 +56,10 @@ SCHEDULES = {
         "block_m=256,block_n=32,waves=8,mfma=32,stages=2,vec=8,unroll=1,order=1",
         "block_m=64,block_n=64,waves=2,mfma=32,stages=1,vec=8,unroll=1,order=0",
         "block_m=32,block_n=128,waves=2,mfma=16,stages=2,vec=2,unroll=1,order=1",
+        "block_m=128,block_n=64,waves=4,mfma=16,stages=2,vec=8,unroll=1,order=2,occ=2",
+        "block_m=64,block_n=64,waves=2,mfma=32,stages=2,vec=8,unroll=1,order=2,occ=1",
+        "block_m=128,block_n=128,waves=8,mfma=16,stages=2,vec=8,unroll=2,order=2,occ=2",
+        "block_m=64,block_n=64,waves=2,mfma=16,stages=1,vec=4,unroll=1,order=2,occ=2",
     ],
     "attn_full": [
         "",
@@ -76,6 +80,8 @@ SCHEDULES = {
         _block("down.", 32, 256, 32, 1, 4, 32, 1, 2, 1, 1, 0) + ",fuse=1",
         _block("up.", 32, 32, 128, 1, 1, 16, 2, 8, 2, 1, 1) + "," +
         _block("down.", 256, 256, 32, 4, 4, 16, 2, 8, 1, 0, 1) + ",fuse=0",
+        _block("up.", 128, 128, 32, 2, 2, 32, 3, 8, 1, 1, 1, 2) + "," +
+        _block("down.", 128, 128, 64, 2, 2, 16, 3, 8, 1, 1, 0, 2) + ",fuse=1",
     ],
     "moe": [
         "",
@@ -85,6 +91,8 @@ SCHEDULES = {
         _block("down.", 32, 128, 128, 1, 2, 16, 2, 8, 1, 0, 1) + ",fuse=0",
         _block("up.", 32, 64, 32, 1, 2, 16, 2, 8, 2, 1, 0) + "," +
         _block("down.", 256, 64, 64, 4, 1, 32, 2, 8, 1, 1, 0) + ",fuse=1",
+        _block("up.", 64, 128, 64, 2, 2, 32, 3, 8, 1, 1, 1, 2) + "," +
+        _block("down.", 64, 128, 32, 2, 2, 16, 3, 8, 1, 1, 1, 2) + ",fuse=1",
     ],
     "conv": [
         "",
@@ -92,6 +100,7 @@ SCHEDULES = {
         _block("", 64, 32, 32, 2, 1, 16, 1, 4, 2, 0, 1) + ",fuse=0",
         _block("", 128, 64, 64, 2, 2, 32, 2, 8, 1, 1, 1) + ",fuse=1",
         _block("", 32, 64, 64, 1, 2, 16, 2, 2, 1, 0, 0) + ",fuse=1",
+        _block("", 128, 64, 64, 2, 2, 16, 3, 8, 1, 1, 0, 2) + ",fuse=1",
     ],
 }
 
