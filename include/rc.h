@@ -227,8 +227,8 @@ typedef struct rc_kernel_info {
     int32_t grid;             /* workgroups per launch */
     int32_t block;            /* threads per workgroup */
     int32_t lds_bytes;        /* static LDS per workgroup */
-    int32_t vgprs;            /* architectural VGPRs per lane */
-    int32_t agprs;            /* accumulation VGPRs per lane */
+    int32_t vgprs;            /* VGPRs per lane, architectural + accumulation */
+    int32_t agprs;            /* of which accumulation VGPRs (AGPRs) */
     int32_t sgprs;
     int32_t scratch_bytes;    /* private segment per lane (0 unless spilling) */
     int32_t waves_per_simd;   /* occupancy bound from registers and LDS */

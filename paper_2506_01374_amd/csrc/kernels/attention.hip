@@ -4,10 +4,18 @@
 // Compile-time schedule (generated prologue):
 //   BM           query rows per workgroup (TileSize)
 //   BN           keys per tile (TileSize)
-//   NW           waves per workgroup; each owns BM / NW query rows (Parallel)
+//   NW           wave row groups; each owns BM / NW query rows (Parallel)
+//   SPLITS       key splits inside the workgroup (Parallel): NW * SPLITS
+//                waves; split s takes key tiles s, s + SPLITS, ... with its
+//                own online-softmax state, and the states of the splits are
+//                merged through LDS at the end (exact: partial outputs and
+//                sums relative to their own maxima are rescaled to the joint
+//                maximum)
 //   MF           MFMA shape 16 (16x16x32) or 32 (32x32x16)
 //   STAGES       1: load tile, compute; 2: double-buffered K/V tiles with
-//                register prefetch of the next tile (ComputeLocation)
+//                register prefetch of the next tile; 3: as 2, plus the
+//                scores of the next tile computed ahead of this tile's
+//                softmax (software pipeline) (ComputeLocation)
 //   VEC          bf16 per global load of K (Vectorize)
 //   UNROLL       unroll factor of the key-tile loop (Unroll)
 //   ORDER        0: query tiles in order; 1: longest (last) query tiles
@@ -31,15 +39,28 @@
 
 #define RPW (BM / NW)
 #define QB (RPW / MF)
-#define NT (64 * NW)
+#define NTS (64 * NW)
+#define NT (NTS * SPLITS)
+#define NBUF (STAGES > 1 ? 2 : 1)
 #define KB (BN / MF)
 #define DB (AD / MF)
 #define NQT (AS / BM)
 #define CPR (AD / 8)
 #define RPL ((16 / CPR) > 0 ? (16 / CPR) : 1)
+#define SWZ (CPR < 16 ? CPR : 16)
+// Lazy rescale: the running max moves (and O, l are rescaled) only when a
+// score exceeds it by more than 2^RESCALE_LOG2; stale maxima keep every
+// probability below 2^RESCALE_LOG2, exact in fp32 and in bf16.
+#define RESCALE_LOG2 8.0f
 #define VTS (BN + 4)
-#define K_LOADS ((BN * AD / VEC + NT - 1) / NT)
-#define V_BLKS ((BN * AD / 32 + NT - 1) / NT)
+#define K_LOADS ((BN * AD / VEC + NTS - 1) / NTS)
+#define V_BLKS ((BN * AD / 32 + NTS - 1) / NTS)
+#define KT_ELEMS (BN * AD)
+#define VT_ELEMS (AD * VTS)
+#define LDS_ELEMS (SPLITS * NBUF * (KT_ELEMS + VT_ELEMS))
+// merge area per partner wave: m and l of its QB * MF queries, then its
+// output accumulators lane by lane
+#define WSLOT (QB * 2 * MF + QB * DB * ACCN * 64)
 
 typedef unsigned short bf16_t;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -71,8 +92,11 @@ struct AttnArgs {
     bf16_t *O;
 };
 
+// XOR swizzle of 16-byte chunks within a K-tile row.  The XOR value depends
+// on the row modulo 16 * RPL only, so rows r and r + 16 k share it and a
+// fragment offset computed once per lane serves every key block.
 __device__ __forceinline__ int kswz(int row, int chunk) {
-    return row * AD + ((chunk ^ ((row / RPL) % CPR)) << 3);
+    return row * AD + ((chunk ^ ((row / RPL) % SWZ)) << 3);
 }
 
 __device__ __forceinline__ accT mfma(const bf16x8 &a, const bf16x8 &b, const accT &c) {
@@ -83,9 +107,12 @@ __device__ __forceinline__ accT mfma(const bf16x8 &a, const bf16x8 &b, const acc
 #endif
 }
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// two floats -> two bf16 (round to nearest even) in one v_cvt_pk_bf16_f32
 __device__ __forceinline__ unsigned pack2(float a, float b) {
-    return (unsigned)__builtin_bit_cast(bf16_t, (__bf16)a) |
-           ((unsigned)__builtin_bit_cast(bf16_t, (__bf16)b) << 16);
+    return __builtin_bit_cast(unsigned, __builtin_convertvector((f32x2){a, b}, bf16x2));
 }
 
 // Key offset (within an MF-key block) of accumulator element r of `lane`.
@@ -97,26 +124,38 @@ __device__ __forceinline__ int key_of(int r, int lane) {
 #endif
 }
 
-__device__ __forceinline__ float group_max(float v) {
-#if MF == 16
-    v = fmaxf(v, __shfl_xor(v, 16));
-#endif
-    return fmaxf(v, __shfl_xor(v, 32));
+// Reductions across the lane groups that hold the other keys of a query:
+// lanes l ^ 16 and l ^ 32 (16x16 MFMA) or l ^ 32 (32x32).  The bpermute
+// byte addresses x16 = (lane ^ 16) * 4 and x32 = (lane ^ 32) * 4 are
+// computed once per kernel.
+__device__ __forceinline__ float xlane(float v, int addr) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(addr, __builtin_bit_cast(int, v)));
 }
 
-__device__ __forceinline__ float group_sum(float v) {
+__device__ __forceinline__ float group_max(float v, int x16, int x32) {
 #if MF == 16
-    v += __shfl_xor(v, 16);
+    v = fmaxf(v, xlane(v, x16));
 #endif
-    return v + __shfl_xor(v, 32);
+    return fmaxf(v, xlane(v, x32));
+}
+
+__device__ __forceinline__ float group_sum(float v, int x16, int x32) {
+#if MF == 16
+    v += xlane(v, x16);
+#endif
+    return v + xlane(v, x32);
 }
 
 extern "C" __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
 void rc_attention(AttnArgs args) {
-    __shared__ __attribute__((aligned(16))) bf16_t Ks[STAGES][BN * AD];
-    __shared__ __attribute__((aligned(16))) bf16_t Vt[STAGES][AD * VTS];
+    // one LDS block: per split, NBUF K tiles then NBUF V^T tiles; reused for
+    // the merge of the splits' states at the end
+    __shared__ __attribute__((aligned(16))) bf16_t smem[LDS_ELEMS];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int rg = wave % NW, sp = wave / NW, tids = tid % NTS;
+    bf16_t *const Kbase = smem + sp * NBUF * (KT_ELEMS + VT_ELEMS);
+    bf16_t *const Vbase = Kbase + NBUF * KT_ELEMS;
     const int bid = blockIdx.x;
 #if ORDER == 1
     const int qt = NQT - 1 - bid / (AB * AH);
@@ -130,7 +169,7 @@ void rc_attention(AttnArgs args) {
     const int bh = bid / NQT;
 #endif
     const int q0 = qt * BM;
-    const int q0w = q0 + wave * RPW;
+    const int q0w = q0 + rg * RPW;
     const size_t base = (size_t)bh * AS * AD;
 
     bf16x8 qf[QB][AD / KSTEP];
@@ -161,19 +200,25 @@ void rc_attention(AttnArgs args) {
 
     vecT rk[K_LOADS];
     u32x4 rv[V_BLKS][4];
+    const int x16 = (lane ^ 16) << 2, x32 = (lane ^ 32) << 2;
+    (void)x16;
+    // per-lane offset of the K fragment of k-step ks in key block 0
+    int koff[AD / KSTEP];
+#pragma unroll
+    for (int ks = 0; ks < AD / KSTEP; ++ks) koff[ks] = kswz(lane % MF, ks * (KSTEP / 8) + lane / MF);
 
     auto gload = [&](int kt) {
         const bf16_t *Kg = args.K + base + (size_t)kt * BN * AD;
         const bf16_t *Vg = args.V + base + (size_t)kt * BN * AD;
 #pragma unroll
         for (int i = 0; i < K_LOADS; ++i) {
-            int idx = tid + i * NT;
-            if (idx < BN * AD / VEC) rk[i] = *(const vecT *)(Kg + (size_t)idx * VEC);
+            int idx = tids + i * NTS;
+            if ((BN * AD / VEC) % NTS == 0 || idx < BN * AD / VEC) rk[i] = *(const vecT *)(Kg + (size_t)idx * VEC);
         }
 #pragma unroll
         for (int i = 0; i < V_BLKS; ++i) {
-            int blk = tid + i * NT;
-            if (blk < BN * AD / 32) {
+            int blk = tids + i * NTS;
+            if ((BN * AD / 32) % NTS == 0 || blk < BN * AD / 32) {
                 int kr = (blk / (AD / 8)) * 4, dc = (blk % (AD / 8)) * 8;
 #pragma unroll
                 for (int j = 0; j < 4; ++j) rv[i][j] = *(const u32x4 *)(Vg + (size_t)(kr + j) * AD + dc);
@@ -182,40 +227,50 @@ void rc_attention(AttnArgs args) {
     };
 
     auto swrite = [&](int s) {
+        bf16_t *const Ks = Kbase + s * KT_ELEMS;
+        bf16_t *const Vt = Vbase + s * VT_ELEMS;
 #pragma unroll
         for (int i = 0; i < K_LOADS; ++i) {
-            int idx = tid + i * NT;
-            if (idx < BN * AD / VEC) {
+            int idx = tids + i * NTS;
+            if ((BN * AD / VEC) % NTS == 0 || idx < BN * AD / VEC) {
                 int row = idx / (AD / VEC), c = (idx % (AD / VEC)) * VEC;
-                *(vecT *)(Ks[s] + kswz(row, c >> 3) + (c & 7)) = rk[i];
+                *(vecT *)(Ks + kswz(row, c >> 3) + (c & 7)) = rk[i];
             }
         }
 #pragma unroll
         for (int i = 0; i < V_BLKS; ++i) {
-            int blk = tid + i * NT;
-            if (blk < BN * AD / 32) {
+            int blk = tids + i * NTS;
+            if ((BN * AD / 32) % NTS == 0 || blk < BN * AD / 32) {
                 int kr = (blk / (AD / 8)) * 4, dc = (blk % (AD / 8)) * 8;
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    // column d = dc + j of keys kr .. kr+3
-                    unsigned h[4];
-#pragma unroll
-                    for (int t = 0; t < 4; ++t) h[t] = (rv[i][t][j >> 1] >> (16 * (j & 1))) & 0xFFFF;
+                    // column d = dc + j of keys kr .. kr+3: one byte permute per
+                    // pair of keys picks the low (j even) or high (j odd) halves
+                    const unsigned sel = (j & 1) ? 0x07060302u : 0x05040100u;
+                    const int c = j >> 1;
                     u32x2 w;
-                    w[0] = h[0] | (h[1] << 16);
-                    w[1] = h[2] | (h[3] << 16);
-                    *(u32x2 *)(Vt[s] + (dc + j) * VTS + kr) = w;
+                    w[0] = __builtin_amdgcn_perm(rv[i][1][c], rv[i][0][c], sel);
+                    w[1] = __builtin_amdgcn_perm(rv[i][3][c], rv[i][2][c], sel);
+                    *(u32x2 *)(Vt + (dc + j) * VTS + kr) = w;
                 }
             }
         }
     };
 
-    auto compute = [&](int kt, int s) {
+    // true when every key of tile kt is masked for this wave's queries
+    auto skipped = [&](int kt) {
 #if CAUSAL
-        if (kt * BN > q0w + RPW - 1) return;     // every key of the tile is masked for this wave
+        return kt * BN > q0w + RPW - 1;
+#else
+        (void)kt;
+        return false;
 #endif
-        // S^T = K Q^T for every query block; each K fragment is read once
-        accT sc[QB][KB];
+    };
+
+    // S^T = K Q^T of tile kt (LDS buffer s) for every query block; each K
+    // fragment is read once
+    auto scores = [&](int s, accT (&sc)[QB][KB]) {
+        const bf16_t *const Ks = Kbase + s * KT_ELEMS;
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
@@ -226,10 +281,15 @@ void rc_attention(AttnArgs args) {
         for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
             for (int ks = 0; ks < AD / KSTEP; ++ks) {
-                bf16x8 kf = *(const bf16x8 *)(Ks[s] + kswz(kb * MF + lane % MF, ks * (KSTEP / 8) + lane / MF));
+                bf16x8 kf = *(const bf16x8 *)(Ks + kb * MF * AD + koff[ks]);
 #pragma unroll
                 for (int qb = 0; qb < QB; ++qb) sc[qb][kb] = mfma(kf, qf[qb][ks], sc[qb][kb]);
             }
+    };
+
+    // online softmax of tile kt's scores and O^T += V^T P^T (V^T from buffer s)
+    auto softmax_pv = [&](int kt, int s, accT (&sc)[QB][KB]) {
+        const bf16_t *const Vt = Vbase + s * VT_ELEMS;
         // online softmax, one query per lane; m is kept in log2 units and the
         // scale is folded into the exponent's fused multiply-add
 #if CAUSAL
@@ -253,9 +313,18 @@ void rc_attention(AttnArgs args) {
             for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
                 for (int r = 0; r < ACCN; ++r) mx = fmaxf(mx, sc[qb][kb][r]);
-            mx = group_max(mx);
-            const float mnew = fmaxf(m[qb], mx * SCALE_LOG2);
-            const float alpha = __builtin_amdgcn_exp2f(m[qb] - mnew);
+            mx = group_max(mx, x16, x32) * SCALE_LOG2;
+            if (__builtin_amdgcn_ballot_w64(mx > m[qb] + RESCALE_LOG2) != 0) {
+                const float mnew = fmaxf(m[qb], mx);
+                const float alpha = __builtin_amdgcn_exp2f(m[qb] - mnew);
+                l[qb] *= alpha;
+#pragma unroll
+                for (int db = 0; db < DB; ++db)
+#pragma unroll
+                    for (int r = 0; r < ACCN; ++r) o[qb][db][r] *= alpha;
+                m[qb] = mnew;
+            }
+            const float mnew = m[qb];
             float ps = 0.f;
 #pragma unroll
             for (int kb = 0; kb < KB; ++kb)
@@ -265,13 +334,7 @@ void rc_attention(AttnArgs args) {
                     sc[qb][kb][r] = p;
                     ps += p;
                 }
-            ps = group_sum(ps);
-            l[qb] = l[qb] * alpha + ps;
-            m[qb] = mnew;
-#pragma unroll
-            for (int db = 0; db < DB; ++db)
-#pragma unroll
-                for (int r = 0; r < ACCN; ++r) o[qb][db][r] *= alpha;
+            l[qb] += group_sum(ps, x16, x32);
         }
         // O^T += V^T P^T, KSTEP keys per MFMA; each V^T fragment is read once
 #pragma unroll
@@ -303,8 +366,8 @@ void rc_attention(AttnArgs args) {
             for (int db = 0; db < DB; ++db) {
                 const int drow = db * MF + lane % MF;
                 u32x4 vw;
-                u32x2 a = *(const u32x2 *)(Vt[s] + drow * VTS + c0);
-                u32x2 b = *(const u32x2 *)(Vt[s] + drow * VTS + c1);
+                u32x2 a = *(const u32x2 *)(Vt + drow * VTS + c0);
+                u32x2 b = *(const u32x2 *)(Vt + drow * VTS + c1);
                 vw[0] = a[0]; vw[1] = a[1]; vw[2] = b[0]; vw[3] = b[1];
                 const bf16x8 vf = __builtin_bit_cast(bf16x8, vw);
 #pragma unroll
@@ -313,25 +376,109 @@ void rc_attention(AttnArgs args) {
         }
     };
 
-#if STAGES == 1
-#pragma unroll UNROLL
-    for (int kt = 0; kt < n_kt; ++kt) {
-        gload(kt);
+    auto compute = [&](int kt, int s) {
+        if (skipped(kt)) return;
+        accT sc[QB][KB];
+        scores(s, sc);
+        softmax_pv(kt, s, sc);
+    };
+
+    // split sp visits key tiles sp, sp + SPLITS, ...; every wave runs the same
+    // number of iterations so the workgroup barriers line up
+    const int n_it = (n_kt + SPLITS - 1) / SPLITS;
+#if STAGES == 3
+    // Software pipeline: iteration i issues the score MFMAs of tile i + 1
+    // (K from the other buffer) ahead of the softmax of tile i, so the matrix
+    // unit works while the vector unit exponentiates; then P V of tile i.
+    // Buffer i & 1 is refilled with tile i + 2 between two barriers.
+    accT sc_a[QB][KB], sc_b[QB][KB];
+    if (sp < n_kt) {
+        gload(sp);
         swrite(0);
+    }
+    if (sp + SPLITS < n_kt) {
+        gload(sp + SPLITS);
+        swrite(1);
+    }
+    __syncthreads();
+    if (sp < n_kt && !skipped(sp)) scores(0, sc_a);
+    auto step = [&](int it, accT (&cur)[QB][KB], accT (&nxt)[QB][KB]) {
+        const int kt = it * SPLITS + sp, kn = kt + SPLITS, k2 = kn + SPLITS;
+        if (k2 < n_kt) gload(k2);
+        if (kn < n_kt && !skipped(kn)) scores((it + 1) & 1, nxt);
+        if (kt < n_kt && !skipped(kt)) softmax_pv(kt, it & 1, cur);
         __syncthreads();
-        compute(kt, 0);
+        if (k2 < n_kt) swrite(it & 1);
+        __syncthreads();
+    };
+    for (int it = 0; it < n_it; it += 2) {
+        step(it, sc_a, sc_b);
+        if (it + 1 < n_it) step(it + 1, sc_b, sc_a);
+    }
+#elif STAGES == 1
+#pragma unroll UNROLL
+    for (int it = 0; it < n_it; ++it) {
+        const int kt = it * SPLITS + sp;
+        if (kt < n_kt) {
+            gload(kt);
+            swrite(0);
+        }
+        __syncthreads();
+        if (kt < n_kt) compute(kt, 0);
         __syncthreads();
     }
 #else
-    gload(0);
-    swrite(0);
+    if (sp < n_kt) {
+        gload(sp);
+        swrite(0);
+    }
     __syncthreads();
 #pragma unroll UNROLL
-    for (int kt = 0; kt < n_kt; ++kt) {
-        if (kt + 1 < n_kt) gload(kt + 1);
-        compute(kt, kt & 1);
-        if (kt + 1 < n_kt) swrite((kt + 1) & 1);
+    for (int it = 0; it < n_it; ++it) {
+        const int kt = it * SPLITS + sp, nk = kt + SPLITS;
+        if (nk < n_kt) gload(nk);
+        if (kt < n_kt) compute(kt, it & 1);
+        if (nk < n_kt) swrite((it + 1) & 1);
         __syncthreads();
+    }
+#endif
+
+#if SPLITS > 1
+    // merge: splits 1.. publish (m, l, O) in LDS, split 0 folds them in
+    float *const cmb = (float *)smem;
+    if (sp > 0) {
+        float *w = cmb + ((sp - 1) * NW + rg) * WSLOT;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+            if (lane < MF) {
+                w[qb * 2 * MF + lane] = m[qb];
+                w[qb * 2 * MF + MF + lane] = l[qb];
+            }
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+                for (int r = 0; r < ACCN; ++r) w[QB * 2 * MF + ((qb * DB + db) * ACCN + r) * 64 + lane] = o[qb][db][r];
+    }
+    __syncthreads();
+    if (sp > 0) return;
+#pragma unroll
+    for (int p = 1; p < SPLITS; ++p) {
+        const float *w = cmb + ((p - 1) * NW + rg) * WSLOT;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+            const float mp = w[qb * 2 * MF + lane % MF], lp = w[qb * 2 * MF + MF + lane % MF];
+            const float mt = fmaxf(m[qb], mp);
+            const float a0 = __builtin_amdgcn_exp2f(m[qb] - mt), a1 = __builtin_amdgcn_exp2f(mp - mt);
+            l[qb] = l[qb] * a0 + lp * a1;
+            m[qb] = mt;
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+                for (int r = 0; r < ACCN; ++r)
+                    o[qb][db][r] = o[qb][db][r] * a0 + w[QB * 2 * MF + ((qb * DB + db) * ACCN + r) * 64 + lane] * a1;
+        }
     }
 #endif
 

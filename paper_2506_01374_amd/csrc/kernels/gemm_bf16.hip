@@ -11,7 +11,10 @@
 //   STAGES       1: load, store, compute; 2: LDS double buffer with register
 //                prefetch of the next K tile, stored to LDS after the tile's
 //                MFMAs; 3: the same, stored half-way through the MFMAs
-//                (ComputeLocation)
+//                (ComputeLocation); 4: direct-to-LDS loads
+//                (global_load_lds_dwordx4) into a ring of three LDS buffers,
+//                two K tiles in flight, no register staging (weights stored
+//                [N][K], 16-byte vectors, non-im2col rows)
 //   VEC          bf16 elements per global load: 2, 4 or 8 (Vectorize)
 //   UNROLL       unroll factor of the K-tile loop (Unroll)
 //   LAYOUT       weights stored 0: [K][N], 1: [N][K] (Layout)
@@ -89,7 +92,13 @@ __device__ __forceinline__ int swz(int row, int chunk) {
     return row * TK + ((chunk ^ ((row / RPL) % CPR)) << 3);
 }
 
-__device__ __forceinline__ bf16_t f2bf(float x) { return __builtin_bit_cast(bf16_t, (__bf16)x); }
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// two floats -> two bf16 (round to nearest even) in one v_cvt_pk_bf16_f32
+__device__ __forceinline__ unsigned pack2(float a, float b) {
+    return __builtin_bit_cast(unsigned, __builtin_convertvector((f32x2){a, b}, bf16x2));
+}
 
 __device__ __forceinline__ float silu(float x) {
     // x * sigmoid(x); exp(-x) as 2^(-x log2 e) on the hardware exp2 unit.
@@ -119,9 +128,19 @@ __device__ __forceinline__ bf16_t vec_elem(const vecT &v, int j) {
 
 extern "C" __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
 void rc_gemm_bf16(GemmBf16Args args) {
+#if STAGES == 4
+    // three distinct LDS objects, so the compiler can tell the buffer being
+    // filled by direct-to-LDS loads from the one being read
+    __shared__ __attribute__((aligned(16))) bf16_t As0[TM * TK], As1[TM * TK], As2[TM * TK];
+    __shared__ __attribute__((aligned(16))) bf16_t Bs0[NB][TN * TK], Bs1[NB][TN * TK], Bs2[NB][TN * TK];
+#define NBUF 2
+    bf16_t (*As)[TM * TK] = nullptr;           // unused with the DMA ring
+    bf16_t (*Bs)[NB][TN * TK] = nullptr;
+#else
 #define NBUF (STAGES > 1 ? 2 : 1)
     __shared__ __attribute__((aligned(16))) bf16_t As[NBUF][TM * TK];
     __shared__ __attribute__((aligned(16))) bf16_t Bs[NBUF][NB][TN * TK];
+#endif
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -275,16 +294,22 @@ void rc_gemm_bf16(GemmBf16Args args) {
         bf16x8 a[FM];
         bf16x8 b[NB][FN];
     };
-    auto load_frags = [&](int s, int ks, Frags &f) {
-        const int chunk = ks * (KSTEP / 8) + lane / MF;
+    // The swizzle's XOR depends on the row modulo MF only (MF / RPL is a
+    // multiple of CPR for every legal tile_k), so each lane's fragment
+    // offset within an MF-row block is computed once per k-step and every
+    // block adds a constant.
+    int foff[TK / KSTEP];
+#pragma unroll
+    for (int ks = 0; ks < TK / KSTEP; ++ks) foff[ks] = swz(lane % MF, ks * (KSTEP / 8) + lane / MF);
+    auto load_frags = [&](const bf16_t *la, const bf16_t (*lb)[TN * TK], int ks, Frags &f) {
 #pragma unroll
         for (int i = 0; i < FM; ++i)
-            f.a[i] = *(const bf16x8 *)(As[s] + swz(wm * WTM + i * MF + lane % MF, chunk));
+            f.a[i] = *(const bf16x8 *)(la + (wm * WTM + i * MF) * TK + foff[ks]);
 #pragma unroll
         for (int b = 0; b < NB; ++b)
 #pragma unroll
             for (int j = 0; j < FN; ++j)
-                f.b[b][j] = *(const bf16x8 *)(Bs[s][b] + swz(wn * WTN + j * MF + lane % MF, chunk));
+                f.b[b][j] = *(const bf16x8 *)(lb[b] + (wn * WTN + j * MF) * TK + foff[ks]);
     };
     auto mfmas = [&](const Frags &f) {
 #pragma unroll
@@ -297,21 +322,111 @@ void rc_gemm_bf16(GemmBf16Args args) {
     // One K tile from LDS buffer s.  The fragments of k-step ks + 1 are read
     // while the MFMAs of k-step ks issue; `mid` (the LDS store of the next
     // tile into the other buffer) runs halfway through the MFMAs.
-    auto compute = [&](int s, auto &&mid) {
+    auto compute_at = [&](const bf16_t *la, const bf16_t (*lb)[TN * TK], auto &&mid) {
         constexpr int KS = TK / KSTEP;
         Frags f[2];
-        load_frags(s, 0, f[0]);
+        load_frags(la, lb, 0, f[0]);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-            if (ks + 1 < KS) load_frags(s, ks + 1, f[(ks + 1) & 1]);
+            if (ks + 1 < KS) load_frags(la, lb, ks + 1, f[(ks + 1) & 1]);
             if (ks == KS / 2) mid();
             mfmas(f[ks & 1]);
         }
         if (KS == 1) mid();
     };
+    auto compute = [&](int s, auto &&mid) { compute_at(As[s], Bs[s], mid); };
 
     auto nothing = [] {};
-#if STAGES == 1
+#if STAGES == 4
+    // Direct-to-LDS loads: one global_load_lds_dwordx4 moves 64 lanes x 16 B
+    // into 1 KiB of LDS at a wave-uniform base, lane i at byte 16 i.  The
+    // swizzle is applied by choosing which global chunk each lane fetches:
+    // LDS chunk c of the tile holds row c / CPR, logical chunk
+    // (c % CPR) ^ ((row / RPL) % CPR) of that row (the XOR is an involution).
+    typedef __attribute__((address_space(3))) void *lds_vp;
+    typedef __attribute__((address_space(1))) void *gbl_vp;
+    constexpr int NWV = WM * WN;
+    constexpr int A_WL = TM * TK / 8 / 64 / NWV;     // wave-loads per wave, A tile
+    constexpr int B_WL = TN * TK / 8 / 64 / NWV;     // per weight operand
+    constexpr int LPT = A_WL + NB * B_WL;            // loads per lane per K tile
+    const bf16_t *a_src[A_WL];
+    const bf16_t *b_src[NB][B_WL];
+#pragma unroll
+    for (int j = 0; j < A_WL; ++j) {
+        const int c = (wave * A_WL + j) * 64 + lane;
+        const int row = c / CPR, lc = (c % CPR) ^ ((row / RPL) % CPR);
+#if AMODE == 0
+        a_src[j] = args.A + (size_t)(row_base + row) * GK + lc * 8;
+#elif AMODE == 1
+        // rows past the group read a valid row; their products are never stored
+        const int tok = args.perm[row_base + (row < rows_valid ? row : 0)] / TOPK;
+        a_src[j] = args.A + (size_t)tok * GK + lc * 8;
+#else
+        a_src[j] = args.A + (size_t)(row_base + (row < rows_valid ? row : 0)) * GK + lc * 8;
+#endif
+    }
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int j = 0; j < B_WL; ++j) {
+            const int c = (wave * B_WL + j) * 64 + lane;
+            const int row = c / CPR, lc = (c % CPR) ^ ((row / RPL) % CPR);
+            b_src[b][j] = (b == 0 ? B0 :
+#if NB == 2
+                           B1
+#else
+                           B0
+#endif
+                           ) + (size_t)(n0 + row) * GK + lc * 8;
+        }
+    auto gload_lds = [&](int k0, bf16_t *la, bf16_t (*lb)[TN * TK]) {
+#pragma unroll
+        for (int j = 0; j < A_WL; ++j)
+            __builtin_amdgcn_global_load_lds((gbl_vp)(a_src[j] + k0),
+                                             (lds_vp)(la + (wave * A_WL + j) * 512), 16, 0, 0);
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int j = 0; j < B_WL; ++j)
+                __builtin_amdgcn_global_load_lds((gbl_vp)(b_src[b][j] + k0),
+                                                 (lds_vp)(lb[b] + (wave * B_WL + j) * 512), 16, 0, 0);
+    };
+    // s_waitcnt with only the vector-memory count constrained (expcnt and
+    // lgkmcnt at their maxima): at most n loads of this wave still in flight
+#define WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | ((((n) >> 4) & 3) << 14) | (7 << 4) | (15 << 8))
+    gload_lds(0, As0, Bs0);
+    if (KTILES > 1) {
+        gload_lds(TK, As1, Bs1);
+        WAIT_VM(LPT);
+    } else {
+        WAIT_VM(0);
+    }
+    __syncthreads();
+    // tile kt sits in buffer kt % 3; buffer (kt + 2) % 3 held tile kt - 1,
+    // finished before the last barrier, and receives tile kt + 2
+    auto body = [&](int kt, bf16_t *cur_a, bf16_t (*cur_b)[TN * TK], bf16_t *fill_a,
+                    bf16_t (*fill_b)[TN * TK]) {
+        if (kt + 2 < KTILES) gload_lds((kt + 2) * TK, fill_a, fill_b);
+        compute_at(cur_a, cur_b, nothing);
+        if (kt + 2 < KTILES) {
+            WAIT_VM(LPT);          // tile kt + 1 has landed; tile kt + 2 may be in flight
+        } else {
+            WAIT_VM(0);
+        }
+        // Barrier without a release fence: __syncthreads() would also wait for
+        // tile kt + 2's loads.  LDS written by this wave's completed loads is
+        // visible to the workgroup once the barrier is passed; the memory
+        // clobber keeps the compiler from moving LDS accesses across it.
+        __builtin_amdgcn_s_waitcnt(0xC07F);      // lgkmcnt(0): this wave's LDS reads are done
+        asm volatile("s_barrier" ::: "memory");
+    };
+    for (int kt = 0; kt < KTILES; kt += 3) {
+        body(kt, As0, Bs0, As2, Bs2);
+        if (kt + 1 < KTILES) body(kt + 1, As1, Bs1, As0, Bs0);
+        if (kt + 2 < KTILES) body(kt + 2, As2, Bs2, As1, Bs1);
+    }
+#undef WAIT_VM
+#elif STAGES == 1
 #pragma unroll UNROLL
     for (int kt = 0; kt < KTILES; ++kt) {
         gload(kt * TK);
@@ -378,8 +493,8 @@ void rc_gemm_bf16(GemmBf16Args args) {
                 for (int r = 0; r < 4; ++r) v[r] = silu(v[r]) * acc[1][i][j][g * 4 + r];
 #endif
                 u32x2 packed;
-                packed[0] = (unsigned)f2bf(v[0]) | ((unsigned)f2bf(v[1]) << 16);
-                packed[1] = (unsigned)f2bf(v[2]) | ((unsigned)f2bf(v[3]) << 16);
+                packed[0] = pack2(v[0], v[1]);
+                packed[1] = pack2(v[2], v[3]);
                 *(u32x2 *)((bf16_t *)args.C + orow + n) = packed;
 #endif
             }

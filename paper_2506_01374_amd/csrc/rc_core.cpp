@@ -48,7 +48,7 @@ static void add_gemm_block(std::vector<KnobDef> &v, const char *const names[12],
     v.push_back({names[3], "Parallel", {1, 2, 4}, 1});
     v.push_back({names[4], "Parallel", {1, 2, 4}, 1});
     v.push_back({names[5], "TileSize", {16, 32}, 16});          // MFMA instruction shape
-    v.push_back({names[6], "ComputeLocation", {1, 2, 3}, 1});   // LDS staging of the next K tile
+    v.push_back({names[6], "ComputeLocation", {1, 2, 3, 4}, 1});   // LDS staging of the next K tile
     v.push_back({names[7], "Vectorize", {2, 4, 8}, 2});         // bf16 per global load
     v.push_back({names[8], "Unroll", {1, 2}, 1});
     v.push_back({names[9], "Layout", {0, 1}, 0});               // weight stored KxN / NxK
@@ -88,11 +88,12 @@ static std::vector<KnobDef> attention_knobs() {
         {"block_n", "TileSize", {32, 64, 128}, 32},
         {"waves", "Parallel", {1, 2, 4, 8}, 1},
         {"mfma", "TileSize", {16, 32}, 16},
-        {"stages", "ComputeLocation", {1, 2}, 1},
+        {"stages", "ComputeLocation", {1, 2, 3}, 1},
         {"vec", "Vectorize", {2, 4, 8}, 2},
         {"unroll", "Unroll", {1, 2}, 1},
         {"order", "Parallel", {0, 1, 2}, 0},
         {"occ", "Parallel", {1, 2}, 1},
+        {"splits", "Parallel", {1, 2, 4}, 1},
     };
 }
 
@@ -162,7 +163,7 @@ static const int64_t LDS_LIMIT = 163840;   // bytes one workgroup may allocate o
 // predicated), NB weight operands sharing the A tile.
 static std::string check_bf16_block(const rc_op_desc *d, const rc_schedule *s,
                                     const char *const names[12], int64_t M, int64_t N, int64_t K,
-                                    int NB, const char *tag) {
+                                    int NB, const char *tag, bool im2col = false) {
     int tm = kv(d, s, names[0]), tn = kv(d, s, names[1]), tk = kv(d, s, names[2]);
     int wm = kv(d, s, names[3]), wn = kv(d, s, names[4]), mf = kv(d, s, names[5]);
     int st = kv(d, s, names[6]), vec = kv(d, s, names[7]), un = kv(d, s, names[8]);
@@ -186,7 +187,17 @@ static std::string check_bf16_block(const rc_op_desc *d, const rc_schedule *s,
         return fmt("%s: B tile %dx%d does not split into %d threads x %d-wide loads", tag, tk, tn,
                    nt, vec);
     if (lay == 0 && tn % vec) return fmt("%s: vec %d does not divide tile_n %d", tag, vec, tn);
-    int64_t lds = (int64_t)(st > 1 ? 2 : 1) * ((int64_t)tm * tk + (int64_t)NB * tn * tk) * 2;
+    if (st == 4) {
+        // direct-to-LDS loads: whole 1 KiB wave-loads of 16-byte chunks
+        if (lay != 1) return fmt("%s: direct-to-LDS staging needs weights stored N x K", tag);
+        if (vec != 8) return fmt("%s: direct-to-LDS staging moves 16-byte vectors (vec 8)", tag);
+        if (im2col) return fmt("%s: direct-to-LDS staging cannot zero-fill padded im2col rows", tag);
+        if (((int64_t)tm * tk / 512) % (wm * wn) || tm * tk < 512 * wm * wn)
+            return fmt("%s: A tile is not a whole number of 1 KiB wave-loads per wave", tag);
+        if (((int64_t)tn * tk / 512) % (wm * wn) || tn * tk < 512 * wm * wn)
+            return fmt("%s: B tile is not a whole number of 1 KiB wave-loads per wave", tag);
+    }
+    int64_t lds = (int64_t)(st == 4 ? 3 : st > 1 ? 2 : 1) * ((int64_t)tm * tk + (int64_t)NB * tn * tk) * 2;
     if (lds > LDS_LIMIT)
         return fmt("%s: LDS %lld B exceeds %lld B", tag, (long long)lds, (long long)LDS_LIMIT);
     int64_t acc = (int64_t)NB * tm * tn / nt;
@@ -199,7 +210,7 @@ static std::string check_bf16_block(const rc_op_desc *d, const rc_schedule *s,
         int64_t waves = (int64_t)wm * wn, wgs = (occ * 4 + waves - 1) / waves;
         if (wgs * lds > LDS_LIMIT) return fmt("%s: %lld workgroups of %lld B LDS do not fit a CU", tag, (long long)wgs, (long long)lds);
     }
-    int64_t stage_regs = st > 1 ? ((int64_t)tm * tk + (int64_t)NB * tn * tk) / (2 * nt) : 0;
+    int64_t stage_regs = (st == 2 || st == 3) ? ((int64_t)tm * tk + (int64_t)NB * tn * tk) / (2 * nt) : 0;
     if (acc + stage_regs > 384)
         return fmt("%s: %lld accumulator + %lld staging registers per lane exceed 384", tag,
                    (long long)acc, (long long)stage_regs);
@@ -257,15 +268,21 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
             // must hold a power-of-two number of chunks
             if (Dh != 32 && Dh != 64 && Dh != 128 && Dh != 256)
                 return fmt("head dim %lld must be 32, 64, 128 or 256", (long long)Dh);
-            int64_t lds = (int64_t)st * ((int64_t)bn * Dh + Dh * (bn + 4)) * 2;   // K tile + padded V^T tile
+            int sp = kv(d, s, "splits");
+            if (w * sp > 16) return fmt("waves x splits = %d exceeds 16 waves per workgroup", w * sp);
+            // K tile + padded V^T tile per stage and split
+            int64_t lds = (int64_t)sp * (st > 1 ? 2 : 1) * ((int64_t)bn * Dh + Dh * (bn + 4)) * 2;
             if (lds > LDS_LIMIT) return fmt("LDS %lld B exceeds limit", (long long)lds);
+            int64_t mf_acc = (mf == 16) ? 4 : 16;
+            int64_t merge = (int64_t)(sp - 1) * w * ((rpw / mf) * 2 * mf + (rpw / mf) * (Dh / mf) * mf_acc * 64) * 4;
+            if (merge > lds) return fmt("merging %d splits needs %lld B of LDS, more than the %lld B tiles", sp, (long long)merge, (long long)lds);
             int64_t regs = (int64_t)rpw * Dh / 64 + (int64_t)bn * rpw / 64 + (int64_t)rpw * Dh / 128;
             if (regs > 320) return fmt("%lld registers per lane for O, S and Q exceed 320", (long long)regs);
             int occ = kv(d, s, "occ");
             if (occ > 1) {
                 if (regs > 512 / occ - 64)
                     return fmt("%lld registers per lane for O, S and Q leave too few at %d waves/SIMD", (long long)regs, occ);
-                int64_t wgs = (occ * 4 + w - 1) / w;
+                int64_t wgs = (occ * 4 + w * sp - 1) / (w * sp);
                 if (wgs * lds > LDS_LIMIT)
                     return fmt("%lld workgroups of %lld B LDS do not fit a CU", (long long)wgs, (long long)lds);
             }
@@ -294,7 +311,7 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
             if (P <= 0 || Q <= 0) return "empty output";
             int tk = kv(d, s, "tile_k");
             if (C % tk) return fmt("tile_k %d does not divide C = %lld (a K tile must stay in one filter tap)", tk, (long long)C);
-            return check_bf16_block(d, s, PLAIN, N * P * Q, K, R * S * C, 1, "conv");
+            return check_bf16_block(d, s, PLAIN, N * P * Q, K, R * S * C, 1, "conv", true);
         }
     }
     return "unknown operator kind";

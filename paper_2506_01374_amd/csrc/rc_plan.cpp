@@ -438,11 +438,12 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
                                def("MF", kv(d, s, "mfma")) + def("STAGES", kv(d, s, "stages")) +
                                def("VEC", kv(d, s, "vec")) + def("UNROLL", kv(d, s, "unroll")) +
                                def("ORDER", kv(d, s, "order")) + def("OCC", kv(d, s, "occ")) +
+                               def("SPLITS", kv(d, s, "splits")) +
                                def("AB", B) + def("AH", Hh) +
                                def("AS", S) + def("AD", Dh) +
                                def("CAUSAL", (d->flags & RC_FLAG_CAUSAL) ? 1 : 0) + sbuf};
             k.grid = dim3((unsigned)(B * Hh * (S / bm)), 1, 1);
-            k.block = dim3(64 * w, 1, 1);
+            k.block = dim3(64 * w * kv(d, s, "splits"), 1, 1);
             k.bind = [](const rc_args *a, char *, std::vector<char> &b) {
                 put(b, AttnArgs{a->in[0], a->in[1], a->in[2], a->out[0]});
             };
@@ -552,10 +553,11 @@ rc_status rc_describe(const rc_op_desc *d, const rc_schedule *s, rc_kernel_info 
         k.agprs = (int32_t)meta_int(code, ".agpr_count");
         k.sgprs = (int32_t)meta_int(code, ".sgpr_count");
         k.scratch_bytes = (int32_t)meta_int(code, ".private_segment_fixed_size");
-        // Occupancy on gfx950: 512 registers (VGPR + AGPR, allocated in
-        // blocks of 8) per lane per SIMD, at most 8 waves per SIMD; LDS of
-        // 160 KiB per CU shared by the workgroups resident on it.
-        int regs = std::max(k.vgprs, 0) + std::max(k.agprs, 0);
+        // Occupancy on gfx950: 512 registers per lane per SIMD shared by the
+        // resident waves (the metadata's vgpr_count is the combined VGPR +
+        // AGPR allocation), allocated in blocks of 8, at most 8 waves per
+        // SIMD; LDS of 160 KiB per CU shared by the resident workgroups.
+        int regs = std::max(k.vgprs, 0);
         regs = (regs + 7) / 8 * 8;
         int by_regs = regs > 0 ? std::min(8, 512 / regs) : 8;
         int waves_per_wg = (k.block + 63) / 64;

@@ -422,6 +422,34 @@ class Plan:
         a.out[0] = _ptr(output)
         return a
 
+    class Prepared:
+        """Argument block, workspace and stream of repeated launches, built once."""
+
+        def __init__(self, plan, inputs, output, workspace, stream):
+            self.plan = plan
+            self.args = plan._args(inputs, output)
+            self.keep = (list(inputs), output, workspace)       # keep tensors alive
+            self.ws = _ptr(workspace)
+            self.wsz = 0 if workspace is None else workspace.numel() * workspace.element_size()
+            self.stream = _stream_ptr(stream)
+
+        def events(self, events):
+            handles = [int(e.cuda_event) for e in events]
+            if not all(handles):
+                raise ValueError("record each event once before use (torch creates events lazily)")
+            return (ctypes.c_void_p * len(handles))(*handles)
+
+        def launch(self) -> None:
+            _check(lib().rc_launch(self.plan.h, ctypes.byref(self.args), self.ws, self.wsz, self.stream),
+                   "rc_launch")
+
+        def launch_timed(self, ev_array) -> None:
+            _check(lib().rc_launch_timed(self.plan.h, ctypes.byref(self.args), self.ws, self.wsz,
+                                         self.stream, ev_array, len(ev_array)), "rc_launch_timed")
+
+    def prepare(self, inputs, output, workspace=None, stream=None) -> "Plan.Prepared":
+        return Plan.Prepared(self, inputs, output, workspace, stream)
+
     def launch(self, inputs, output, workspace=None, stream=None) -> None:
         a = self._args(inputs, output)
         wsz = 0 if workspace is None else workspace.numel() * workspace.element_size()

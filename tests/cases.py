@@ -60,11 +60,19 @@ SCHEDULES = {
         "block_m=64,block_n=64,waves=2,mfma=32,stages=2,vec=8,unroll=1,order=2,occ=1",
         "block_m=128,block_n=128,waves=8,mfma=16,stages=2,vec=8,unroll=2,order=2,occ=2",
         "block_m=64,block_n=64,waves=2,mfma=16,stages=1,vec=4,unroll=1,order=2,occ=2",
+        "block_m=64,block_n=64,waves=4,mfma=16,stages=2,vec=8,unroll=1,order=2,occ=1,splits=2",
+        "block_m=64,block_n=32,waves=2,mfma=32,stages=2,vec=8,unroll=1,order=1,occ=1,splits=4",
+        "block_m=32,block_n=64,waves=2,mfma=16,stages=1,vec=8,unroll=2,order=0,occ=1,splits=4",
+        "block_m=64,block_n=64,waves=4,mfma=16,stages=3,vec=8,unroll=1,order=2,occ=2",
+        "block_m=64,block_n=32,waves=2,mfma=32,stages=3,vec=8,unroll=1,order=1,occ=1,splits=2",
+        "block_m=128,block_n=64,waves=4,mfma=16,stages=3,vec=4,unroll=1,order=0,occ=1",
     ],
     "attn_full": [
         "",
         "block_m=128,block_n=64,waves=4,mfma=32,stages=2,vec=8,unroll=1,order=1",
         "block_m=64,block_n=128,waves=4,mfma=16,stages=1,vec=4,unroll=2,order=0",
+        "block_m=64,block_n=64,waves=4,mfma=16,stages=2,vec=8,unroll=1,order=0,splits=2",
+        "block_m=64,block_n=64,waves=4,mfma=16,stages=3,vec=8,unroll=1,order=0,splits=2",
     ],
     "attn_d64": [
         "block_m=64,block_n=32,waves=2,mfma=32,stages=2,vec=8,unroll=1,order=0",
@@ -82,6 +90,10 @@ SCHEDULES = {
         _block("down.", 256, 256, 32, 4, 4, 16, 2, 8, 1, 0, 1) + ",fuse=0",
         _block("up.", 128, 128, 32, 2, 2, 32, 3, 8, 1, 1, 1, 2) + "," +
         _block("down.", 128, 128, 64, 2, 2, 16, 3, 8, 1, 1, 0, 2) + ",fuse=1",
+        _block("up.", 128, 128, 64, 2, 2, 16, 4, 8, 1, 1, 1) + "," +
+        _block("down.", 128, 128, 64, 2, 2, 16, 4, 8, 1, 1, 1) + ",fuse=1",
+        _block("up.", 64, 128, 32, 2, 2, 32, 4, 8, 1, 1, 0) + "," +
+        _block("down.", 256, 64, 32, 4, 1, 16, 4, 8, 1, 1, 0) + ",fuse=0",
     ],
     "moe": [
         "",
@@ -93,6 +105,10 @@ SCHEDULES = {
         _block("down.", 256, 64, 64, 4, 1, 32, 2, 8, 1, 1, 0) + ",fuse=1",
         _block("up.", 64, 128, 64, 2, 2, 32, 3, 8, 1, 1, 1, 2) + "," +
         _block("down.", 64, 128, 32, 2, 2, 16, 3, 8, 1, 1, 1, 2) + ",fuse=1",
+        _block("up.", 128, 128, 64, 2, 2, 16, 4, 8, 1, 1, 1) + "," +
+        _block("down.", 128, 128, 64, 2, 2, 16, 4, 8, 1, 1, 1) + ",fuse=1",
+        _block("up.", 32, 128, 64, 1, 2, 16, 4, 8, 1, 1, 0) + "," +
+        _block("down.", 64, 64, 64, 2, 1, 32, 4, 8, 1, 1, 0) + ",fuse=0",
     ],
     "conv": [
         "",

@@ -190,3 +190,32 @@ def test_full_size_sampled(name, which):
     rows = None if op.kind == rc.RC_OP_GEMM_F32 else _sample_rows(op, n)
     assert_parity(op, y, host, rows=rows, label=f"{name} {which}")
     assert np.all(np.isfinite(y))
+
+
+@pytest.mark.parametrize("key", ["attn_causal", "mlp", "moe"])
+def test_graph_replay_matches_eager(key):
+    # The benchmark replays captured launches.  Capture one execution on a
+    # side stream, replay it several times with eager work and host
+    # synchronisation in between, and compare every replay with the eager
+    # result bit for bit.
+    op = cases.small_op(key)
+    sched = op.from_string(cases.SCHEDULES[key][1])
+    host = W.host_inputs(op, seed=5)
+    eager, (plan, dev, out, ws) = run(op, sched, host)
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        prep = plan.prepare(dev, out, ws, stream)
+        prep.launch()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        prep.launch()
+    torch.cuda.synchronize()
+    scratch = torch.zeros(1 << 20, device="cuda")
+    for rep in range(3):
+        out.fill_(float("nan"))
+        scratch.add_(1.0)                      # unrelated eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(W.output_to_f64(op, out), eager), f"replay {rep} differs"
