@@ -15,7 +15,10 @@
 //   STAGES       1: load tile, compute; 2: double-buffered K/V tiles with
 //                register prefetch of the next tile; 3: as 2, plus the
 //                scores of the next tile computed ahead of this tile's
-//                softmax (software pipeline) (ComputeLocation)
+//                softmax (software pipeline); 4: direct global-to-LDS loads
+//                into a ring of three K/V buffers, two tiles in flight
+//                while one is computed, V kept key-major and read with the
+//                transposing LDS load (ComputeLocation)
 //   VEC          bf16 per global load of K (Vectorize)
 //   UNROLL       unroll factor of the key-tile loop (Unroll)
 //   ORDER        0: query tiles in order; 1: longest (last) query tiles
@@ -33,15 +36,16 @@
 // (running max m and sum l) are per-lane scalars and the rescale of the
 // output accumulator is a scalar multiply.  The output is accumulated
 // transposed too, O^T = V^T P^T, with V^T fragments from an LDS copy of
-// the V tile stored d-major; the probabilities never leave registers: the
-// MFMA's k index (the key) follows the accumulator layout of S^T, and the
-// V^T fragment is read in that same key order.
+// the V tile stored d-major (or, with STAGES 4, of the key-major V tile
+// through ds_read_b64_tr_b16); the probabilities never leave registers:
+// the MFMA's k index (the key) follows the accumulator layout of S^T, and
+// the V^T fragment is read in that same key order.
 
 #define RPW (BM / NW)
 #define QB (RPW / MF)
 #define NTS (64 * NW)
 #define NT (NTS * SPLITS)
-#define NBUF (STAGES > 1 ? 2 : 1)
+#define NBUF (STAGES == 4 ? 3 : STAGES > 1 ? 2 : 1)
 #define KB (BN / MF)
 #define DB (AD / MF)
 #define NQT (AS / BM)
@@ -52,12 +56,21 @@
 // score exceeds it by more than 2^RESCALE_LOG2; stale maxima keep every
 // probability below 2^RESCALE_LOG2, exact in fp32 and in bf16.
 #define RESCALE_LOG2 8.0f
-#define VTS (BN + 4)
+// V^T tile: d-major rows of BN keys, padded to VTS elements.  Columns hold
+// the keys in the order the P^T fragments use (vcol), so one 16-byte read
+// gives a lane its 8 keys; the padding (16 for the 16x16 MFMA shape, 8 for
+// 32x32) keeps those reads and the 8-byte block stores free of LDS bank
+// conflicts.
+#define VTS (BN + (MF == 16 ? 16 : 8))
 #define K_LOADS ((BN * AD / VEC + NTS - 1) / NTS)
 #define V_BLKS ((BN * AD / 32 + NTS - 1) / NTS)
 #define KT_ELEMS (BN * AD)
 #define VT_ELEMS (AD * VTS)
 #define LDS_ELEMS (SPLITS * NBUF * (KT_ELEMS + VT_ELEMS))
+// Key-major V tile (STAGES 4): 16-byte chunk c of key row r sits at chunk
+// c ^ vswz(r); for 16 consecutive rows the two chunks a transposing read
+// takes from each row land on distinct banks.
+#define VSWZ(r) ((2 * (r)) & (CPR - 1))
 // merge area per partner wave: m and l of its QB * MF queries, then its
 // output accumulators lane by lane
 #define WSLOT (QB * 2 * MF + QB * DB * ACCN * 64)
@@ -115,6 +128,20 @@ __device__ __forceinline__ unsigned pack2(float a, float b) {
     return __builtin_bit_cast(unsigned, __builtin_convertvector((f32x2){a, b}, bf16x2));
 }
 
+// Column of key `key` (a multiple of 4: one group of 4 keys) in the V^T tile.
+// A lane's P^T fragment for one MFMA k-step holds two groups of 4 keys
+// (16 apart for 16x16, 8 apart for 32x32); this interleave makes them
+// adjacent.
+__device__ __forceinline__ int vcol(int key) {
+#if MF == 16
+    const int g4 = (key & 31) >> 2;            // 4h + g
+    return (key & ~31) + 4 * (2 * (g4 & 3) + (g4 >> 2));
+#else
+    const int g4 = (key & 15) >> 2;            // 2t + g
+    return (key & ~15) + 4 * (2 * (g4 & 1) + (g4 >> 1));
+#endif
+}
+
 // Key offset (within an MF-key block) of accumulator element r of `lane`.
 __device__ __forceinline__ int key_of(int r, int lane) {
 #if MF == 16
@@ -125,32 +152,57 @@ __device__ __forceinline__ int key_of(int r, int lane) {
 }
 
 // Reductions across the lane groups that hold the other keys of a query:
-// lanes l ^ 16 and l ^ 32 (16x16 MFMA) or l ^ 32 (32x32).  The bpermute
-// byte addresses x16 = (lane ^ 16) * 4 and x32 = (lane ^ 32) * 4 are
-// computed once per kernel.
-__device__ __forceinline__ float xlane(float v, int addr) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(addr, __builtin_bit_cast(int, v)));
+// lanes l ^ 16 and l ^ 32 (16x16 MFMA) or l ^ 32 (32x32).  v_permlane16_swap
+// and v_permlane32_swap (VALU, no LDS round trip) hand every lane the pair
+// {v[l], v[l ^ 16]} (resp. l ^ 32) in the same order on both lanes, so the
+// reduced value is bit-identical across the lanes of a query.
+__device__ __forceinline__ void pair16(float v, float &a, float &b) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(unsigned, v),
+                                                    __builtin_bit_cast(unsigned, v), false, false);
+    a = __builtin_bit_cast(float, r[0]);
+    b = __builtin_bit_cast(float, r[1]);
 }
 
-__device__ __forceinline__ float group_max(float v, int x16, int x32) {
-#if MF == 16
-    v = fmaxf(v, xlane(v, x16));
-#endif
-    return fmaxf(v, xlane(v, x32));
+__device__ __forceinline__ void pair32(float v, float &a, float &b) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, v),
+                                                    __builtin_bit_cast(unsigned, v), false, false);
+    a = __builtin_bit_cast(float, r[0]);
+    b = __builtin_bit_cast(float, r[1]);
 }
 
-__device__ __forceinline__ float group_sum(float v, int x16, int x32) {
+__device__ __forceinline__ float group_max(float v) {
+    float a, b;
 #if MF == 16
-    v += xlane(v, x16);
+    pair16(v, a, b);
+    v = fmaxf(a, b);
 #endif
-    return v + xlane(v, x32);
+    pair32(v, a, b);
+    return fmaxf(a, b);
+}
+
+__device__ __forceinline__ float group_sum(float v) {
+    float a, b;
+#if MF == 16
+    pair16(v, a, b);
+    v = a + b;
+#endif
+    pair32(v, a, b);
+    return a + b;
 }
 
 extern "C" __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
 void rc_attention(AttnArgs args) {
+#if STAGES == 4
+    // three distinct LDS objects per operand, so the compiler can tell the
+    // buffer being filled by direct-to-LDS loads from the one being read
+    __shared__ __attribute__((aligned(16))) bf16_t K0[KT_ELEMS], K1[KT_ELEMS], K2[KT_ELEMS];
+    __shared__ __attribute__((aligned(16))) bf16_t V0[KT_ELEMS], V1[KT_ELEMS], V2[KT_ELEMS];
+    bf16_t *const smem = K0;                 // unused (no register-staged tiles)
+#else
     // one LDS block: per split, NBUF K tiles then NBUF V^T tiles; reused for
     // the merge of the splits' states at the end
     __shared__ __attribute__((aligned(16))) bf16_t smem[LDS_ELEMS];
+#endif
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int rg = wave % NW, sp = wave / NW, tids = tid % NTS;
@@ -172,6 +224,57 @@ void rc_attention(AttnArgs args) {
     const int q0w = q0 + rg * RPW;
     const size_t base = (size_t)bh * AS * AD;
 
+#if CAUSAL
+    const int n_kt = (q0 + BM - 1) / BN + 1;
+#else
+    const int n_kt = AS / BN;
+#endif
+#if STAGES == 4
+    // Direct-to-LDS loads: one global_load_lds_dwordx4 moves 64 lanes x 16 B
+    // into 1 KiB of LDS at a wave-uniform base (M0), lane i at byte 16 i.
+    // The swizzles are applied by choosing which global chunk each lane
+    // fetches: LDS chunk c of a tile holds row c / CPR, logical chunk
+    // (c % CPR) XOR the row's swizzle (an involution).
+    //
+    // The loads are issued from inline assembly, so the compiler's
+    // wait-count bookkeeping does not see them: it cannot tell, across the
+    // loop's back edge, which ring buffer a load fills, and would otherwise
+    // drain every load before each LDS read.  The kernel's own waits below
+    // order the ring.  The compiler's waits for its own loads stay correct:
+    // extra loads in flight only make a vmcnt(n) wait longer.
+    constexpr int WL = BN * AD / 512 / NW;            // wave-loads per wave and operand
+    unsigned k_src[WL], v_src[WL];                    // byte offsets within a tile
+#pragma unroll
+    for (int j = 0; j < WL; ++j) {
+        const int c = (wave * WL + j) * 64 + lane;
+        const int row = c / CPR, pc = c % CPR;
+        k_src[j] = 2u * (row * AD + ((pc ^ ((row / RPL) % SWZ)) << 3));
+        v_src[j] = 2u * (row * AD + ((pc ^ VSWZ(row)) << 3));
+    }
+    // LDS byte addresses of the ring buffers and this wave's first 1 KiB
+    typedef __attribute__((address_space(3))) bf16_t *lds_p;
+    const unsigned wl0 = (unsigned)__builtin_amdgcn_readfirstlane(wave) * WL * 1024u;
+    const unsigned KA[3] = {(unsigned)(size_t)(lds_p)K0 + wl0, (unsigned)(size_t)(lds_p)K1 + wl0,
+                            (unsigned)(size_t)(lds_p)K2 + wl0};
+    const unsigned VA[3] = {(unsigned)(size_t)(lds_p)V0 + wl0, (unsigned)(size_t)(lds_p)V1 + wl0,
+                            (unsigned)(size_t)(lds_p)V2 + wl0};
+    auto dma = [&](const bf16_t *gbase, unsigned off, unsigned lds_addr) {
+        asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                     :: "v"(off), "s"(gbase), "s"(lds_addr) : "memory", "m0");
+    };
+    // tile kt into ring buffer b
+    auto gload_lds = [&](int kt, int b) {
+        const bf16_t *Kg = args.K + base + (size_t)kt * BN * AD;
+        const bf16_t *Vg = args.V + base + (size_t)kt * BN * AD;
+#pragma unroll
+        for (int j = 0; j < WL; ++j) dma(Kg, k_src[j], KA[b] + j * 1024u);
+#pragma unroll
+        for (int j = 0; j < WL; ++j) dma(Vg, v_src[j], VA[b] + j * 1024u);
+    };
+    // the first two key tiles are in flight while Q is read
+    gload_lds(0, 0);
+    if (n_kt > 1) gload_lds(1, 1);
+#endif
     bf16x8 qf[QB][AD / KSTEP];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb)
@@ -179,6 +282,16 @@ void rc_attention(AttnArgs args) {
         for (int ks = 0; ks < AD / KSTEP; ++ks)
             qf[qb][ks] = *(const bf16x8 *)(args.Q + base + (size_t)(q0w + qb * MF + lane % MF) * AD +
                                            ks * KSTEP + 8 * (lane / MF));
+#if STAGES == 4
+    // Consume Q here so that the compiler's wait for it (a full vmcnt drain,
+    // which also lands tiles 0 and 1) sits before the loop rather than in it.
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int ks = 0; ks < AD / KSTEP; ++ks) asm volatile("" :: "v"(qf[qb][ks]));
+    __builtin_amdgcn_s_waitcnt(0x0F70);      // vmcnt(0)
+    __syncthreads();
+#endif
 
     accT o[QB][DB];
     float m[QB], l[QB];
@@ -192,16 +305,9 @@ void rc_attention(AttnArgs args) {
             for (int r = 0; r < ACCN; ++r) o[qb][db][r] = 0.f;
     }
 
-#if CAUSAL
-    const int n_kt = (q0 + BM - 1) / BN + 1;
-#else
-    const int n_kt = AS / BN;
-#endif
 
     vecT rk[K_LOADS];
     u32x4 rv[V_BLKS][4];
-    const int x16 = (lane ^ 16) << 2, x32 = (lane ^ 32) << 2;
-    (void)x16;
     // per-lane offset of the K fragment of k-step ks in key block 0
     int koff[AD / KSTEP];
 #pragma unroll
@@ -219,7 +325,7 @@ void rc_attention(AttnArgs args) {
         for (int i = 0; i < V_BLKS; ++i) {
             int blk = tids + i * NTS;
             if ((BN * AD / 32) % NTS == 0 || blk < BN * AD / 32) {
-                int kr = (blk / (AD / 8)) * 4, dc = (blk % (AD / 8)) * 8;
+                int kr = (blk % (BN / 4)) * 4, dc = (blk / (BN / 4)) * 8;
 #pragma unroll
                 for (int j = 0; j < 4; ++j) rv[i][j] = *(const u32x4 *)(Vg + (size_t)(kr + j) * AD + dc);
             }
@@ -241,7 +347,8 @@ void rc_attention(AttnArgs args) {
         for (int i = 0; i < V_BLKS; ++i) {
             int blk = tids + i * NTS;
             if ((BN * AD / 32) % NTS == 0 || blk < BN * AD / 32) {
-                int kr = (blk / (AD / 8)) * 4, dc = (blk % (AD / 8)) * 8;
+                int kr = (blk % (BN / 4)) * 4, dc = (blk / (BN / 4)) * 8;
+                const int col = vcol(kr);
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
                     // column d = dc + j of keys kr .. kr+3: one byte permute per
@@ -251,7 +358,7 @@ void rc_attention(AttnArgs args) {
                     u32x2 w;
                     w[0] = __builtin_amdgcn_perm(rv[i][1][c], rv[i][0][c], sel);
                     w[1] = __builtin_amdgcn_perm(rv[i][3][c], rv[i][2][c], sel);
-                    *(u32x2 *)(Vt + (dc + j) * VTS + kr) = w;
+                    *(u32x2 *)(Vt + (dc + j) * VTS + col) = w;
                 }
             }
         }
@@ -269,8 +376,7 @@ void rc_attention(AttnArgs args) {
 
     // S^T = K Q^T of tile kt (LDS buffer s) for every query block; each K
     // fragment is read once
-    auto scores = [&](int s, accT (&sc)[QB][KB]) {
-        const bf16_t *const Ks = Kbase + s * KT_ELEMS;
+    auto scores_at = [&](const bf16_t *Ks, accT (&sc)[QB][KB]) {
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
@@ -286,10 +392,24 @@ void rc_attention(AttnArgs args) {
                 for (int qb = 0; qb < QB; ++qb) sc[qb][kb] = mfma(kf, qf[qb][ks], sc[qb][kb]);
             }
     };
+    auto scores = [&](int s, accT (&sc)[QB][KB]) { scores_at(Kbase + s * KT_ELEMS, sc); };
+
+#if STAGES == 4
+    // per-lane offsets (elements, relative to the V buffer) of the row and
+    // column this lane addresses in the transposing read of key block j,
+    // half h, d block db: row 32 j + 16 h + 4 (lane / 16) + (lane % 16) / 4,
+    // columns 16 db + 4 (lane % 4) .. + 3 (16x16 MFMA only)
+    int voff[DB];
+    {
+        const int vr = 4 * (lane >> 4) + ((lane & 15) >> 2);
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+            voff[db] = vr * AD + (((2 * db + ((lane & 3) >> 1)) ^ VSWZ(vr)) << 3) + (lane & 1) * 4;
+    }
+#endif
 
     // online softmax of tile kt's scores and O^T += V^T P^T (V^T from buffer s)
-    auto softmax_pv = [&](int kt, int s, accT (&sc)[QB][KB]) {
-        const bf16_t *const Vt = Vbase + s * VT_ELEMS;
+    auto softmax_pv_at = [&](int kt, const bf16_t *Vt, accT (&sc)[QB][KB]) {
         // online softmax, one query per lane; m is kept in log2 units and the
         // scale is folded into the exponent's fused multiply-add
 #if CAUSAL
@@ -313,7 +433,7 @@ void rc_attention(AttnArgs args) {
             for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
                 for (int r = 0; r < ACCN; ++r) mx = fmaxf(mx, sc[qb][kb][r]);
-            mx = group_max(mx, x16, x32) * SCALE_LOG2;
+            mx = group_max(mx) * SCALE_LOG2;
             if (__builtin_amdgcn_ballot_w64(mx > m[qb] + RESCALE_LOG2) != 0) {
                 const float mnew = fmaxf(m[qb], mx);
                 const float alpha = __builtin_amdgcn_exp2f(m[qb] - mnew);
@@ -334,17 +454,17 @@ void rc_attention(AttnArgs args) {
                     sc[qb][kb][r] = p;
                     ps += p;
                 }
-            l[qb] += group_sum(ps, x16, x32);
+            l[qb] += group_sum(ps);
         }
         // O^T += V^T P^T, KSTEP keys per MFMA; each V^T fragment is read once
 #pragma unroll
         for (int j = 0; j < BN / KSTEP; ++j) {
             bf16x8 pf[QB];
 #if MF == 16
-            const int c0 = 32 * j + 4 * (lane >> 4), c1 = c0 + 16;
+            const int c0 = 32 * j + 8 * (lane >> 4);
 #else
             const int kb = j >> 1, hf = (j & 1) * 8;
-            const int c0 = kb * 32 + (j & 1) * 16 + 4 * (lane >> 5), c1 = c0 + 8;
+            const int c0 = 16 * j + 8 * (lane >> 5);
 #endif
 #pragma unroll
             for (int qb = 0; qb < QB; ++qb) {
@@ -364,17 +484,25 @@ void rc_attention(AttnArgs args) {
             }
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
+#if STAGES == 4
+                typedef short v4i16 __attribute__((ext_vector_type(4)));
+                typedef __attribute__((address_space(3))) v4i16 *lds_v4p;
+                const bf16_t *const vp = Vt + voff[db] + 32 * j * AD;
+                const v4i16 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4p)(vp));
+                const v4i16 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4p)(vp + 16 * AD));
+                const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+                (void)c0;
+#else
                 const int drow = db * MF + lane % MF;
-                u32x4 vw;
-                u32x2 a = *(const u32x2 *)(Vt + drow * VTS + c0);
-                u32x2 b = *(const u32x2 *)(Vt + drow * VTS + c1);
-                vw[0] = a[0]; vw[1] = a[1]; vw[2] = b[0]; vw[3] = b[1];
-                const bf16x8 vf = __builtin_bit_cast(bf16x8, vw);
+                const bf16x8 vf = *(const bf16x8 *)(Vt + drow * VTS + c0);
+#endif
 #pragma unroll
                 for (int qb = 0; qb < QB; ++qb) o[qb][db] = mfma(vf, pf[qb], o[qb][db]);
             }
         }
     };
+
+    auto softmax_pv = [&](int kt, int s, accT (&sc)[QB][KB]) { softmax_pv_at(kt, Vbase + s * VT_ELEMS, sc); };
 
     auto compute = [&](int kt, int s) {
         if (skipped(kt)) return;
@@ -386,7 +514,40 @@ void rc_attention(AttnArgs args) {
     // split sp visits key tiles sp, sp + SPLITS, ...; every wave runs the same
     // number of iterations so the workgroup barriers line up
     const int n_it = (n_kt + SPLITS - 1) / SPLITS;
-#if STAGES == 3
+#if STAGES == 4
+    (void)n_it;
+    (void)compute;
+    // s_waitcnt with only the vector-memory count constrained (expcnt and
+    // lgkmcnt at their maxima): at most n loads of this wave still in flight
+#define WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | ((((n) >> 4) & 3) << 14) | (7 << 4) | (15 << 8))
+    // tile kt sits in buffer kt % 3; buffer (kt + 2) % 3 held tile kt - 1,
+    // finished before the last barrier, and receives tile kt + 2
+    auto body = [&](int kt, const bf16_t *kc, const bf16_t *vc, int fill) {
+        if (kt + 2 < n_kt) gload_lds(kt + 2, fill);
+        if (!skipped(kt)) {
+            accT sc[QB][KB];
+            scores_at(kc, sc);
+            softmax_pv_at(kt, vc, sc);
+        }
+        if (kt + 2 < n_kt) {
+            WAIT_VM(2 * WL);       // tile kt + 1 has landed; tile kt + 2 may be in flight
+        } else {
+            WAIT_VM(0);
+        }
+        // Barrier without a release fence: __syncthreads() would also wait for
+        // tile kt + 2's loads.  LDS written by this wave's completed loads is
+        // visible to the workgroup once the barrier is passed; the memory
+        // clobber keeps the compiler from moving LDS accesses across it.
+        __builtin_amdgcn_s_waitcnt(0xC07F);      // lgkmcnt(0): this wave's LDS reads are done
+        asm volatile("s_barrier" ::: "memory");
+    };
+    for (int kt = 0; kt < n_kt; kt += 3) {
+        body(kt, K0, V0, 2);
+        if (kt + 1 < n_kt) body(kt + 1, K1, V1, 0);
+        if (kt + 2 < n_kt) body(kt + 2, K2, V2, 1);
+    }
+#undef WAIT_VM
+#elif STAGES == 3
     // Software pipeline: iteration i issues the score MFMAs of tile i + 1
     // (K from the other buffer) ahead of the softmax of tile i, so the matrix
     // unit works while the vector unit exponentiates; then P V of tile i.
@@ -503,3 +664,4 @@ void rc_attention(AttnArgs args) {
             }
     }
 }
+

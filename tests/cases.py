@@ -66,6 +66,11 @@ SCHEDULES = {
         "block_m=64,block_n=64,waves=4,mfma=16,stages=3,vec=8,unroll=1,order=2,occ=2",
         "block_m=64,block_n=32,waves=2,mfma=32,stages=3,vec=8,unroll=1,order=1,occ=1,splits=2",
         "block_m=128,block_n=64,waves=4,mfma=16,stages=3,vec=4,unroll=1,order=0,occ=1",
+        "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=2,occ=2",
+        "block_m=32,block_n=64,waves=2,mfma=16,stages=4,vec=8,unroll=1,order=0,occ=1",
+        "block_m=128,block_n=64,waves=8,mfma=16,stages=4,vec=8,unroll=1,order=1,occ=2",
+        "block_m=64,block_n=64,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=2,occ=1",
+        "block_m=64,block_n=32,waves=2,mfma=16,stages=4,vec=8,unroll=1,order=1,occ=1",
     ],
     "attn_full": [
         "",
@@ -73,10 +78,12 @@ SCHEDULES = {
         "block_m=64,block_n=128,waves=4,mfma=16,stages=1,vec=4,unroll=2,order=0",
         "block_m=64,block_n=64,waves=4,mfma=16,stages=2,vec=8,unroll=1,order=0,splits=2",
         "block_m=64,block_n=64,waves=4,mfma=16,stages=3,vec=8,unroll=1,order=0,splits=2",
+        "block_m=64,block_n=64,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=0",
     ],
     "attn_d64": [
         "block_m=64,block_n=32,waves=2,mfma=32,stages=2,vec=8,unroll=1,order=0",
         "block_m=32,block_n=64,waves=2,mfma=16,stages=1,vec=4,unroll=1,order=1",
+        "block_m=32,block_n=32,waves=2,mfma=16,stages=4,vec=8,unroll=1,order=0",
     ],
     "mlp": [
         "",
