@@ -26,6 +26,12 @@
 //                tiles t and NQT-1-t, so that co-resident pairs carry equal
 //                causal work
 //   OCC          waves per SIMD the register allocation must leave room for
+//   CHUNK        0: a workgroup runs a query tile's whole key range; n > 0:
+//                the key range is cut into work items of at most n key tiles
+//                (Parallel).  Items of a cut tile leave their unnormalised
+//                state (O, m, l) in the workspace and rc_attention_combine
+//                merges them, which shortens the longest workgroup's chain
+//                of dependent key tiles
 //   AB AH AS AD  batch, heads, sequence length, head dim
 //   CAUSAL       top-left aligned causal mask (key j visible iff j <= i)
 //   SCALE_LOG2   log2(e) / sqrt(AD): scores are kept in log2 units
@@ -103,6 +109,7 @@ struct AttnArgs {
     const bf16_t *K;
     const bf16_t *V;
     bf16_t *O;
+    float *P;          // partial states of cut query tiles (CHUNK > 0)
 };
 
 // XOR swizzle of 16-byte chunks within a K-tile row.  The XOR value depends
@@ -156,38 +163,86 @@ __device__ __forceinline__ int key_of(int r, int lane) {
 // and v_permlane32_swap (VALU, no LDS round trip) hand every lane the pair
 // {v[l], v[l ^ 16]} (resp. l ^ 32) in the same order on both lanes, so the
 // reduced value is bit-identical across the lanes of a query.
-__device__ __forceinline__ void pair16(float v, float &a, float &b) {
-    const auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(unsigned, v),
-                                                    __builtin_bit_cast(unsigned, v), false, false);
-    a = __builtin_bit_cast(float, r[0]);
-    b = __builtin_bit_cast(float, r[1]);
-}
-
-__device__ __forceinline__ void pair32(float v, float &a, float &b) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, v),
-                                                    __builtin_bit_cast(unsigned, v), false, false);
-    a = __builtin_bit_cast(float, r[0]);
-    b = __builtin_bit_cast(float, r[1]);
-}
+// The swaps are issued from inline assembly: the compiler's intrinsic for
+// them returns the pair, but its optimiser folds the second result into the
+// first, which silently drops the partner lane from the reduction.  Both
+// registers start as copies of v; the swap and the max (or add) of the pair
+// share one asm block, so the compiler adds no NaN-quieting copies around
+// the max.  s_nop 1 before each swap and s_nop 0 after it give the wait
+// states between a VALU write and the swap's read, and between the swap's
+// write and the next VALU read.
+#define RC_PAIR_OP(swap, op)                                                              \
+    "s_nop 1\n\t" swap " %0, %1\n\ts_nop 0\n\t" op " %0, %0, %1"
 
 __device__ __forceinline__ float group_max(float v) {
-    float a, b;
+    unsigned x = __builtin_bit_cast(unsigned, v), y = x;
 #if MF == 16
-    pair16(v, a, b);
-    v = fmaxf(a, b);
+    asm volatile(RC_PAIR_OP("v_permlane16_swap_b32", "v_max_f32") : "+v"(x), "+v"(y));
+    y = x;
 #endif
-    pair32(v, a, b);
-    return fmaxf(a, b);
+    asm volatile(RC_PAIR_OP("v_permlane32_swap_b32", "v_max_f32") : "+v"(x), "+v"(y));
+    return __builtin_bit_cast(float, x);
 }
 
 __device__ __forceinline__ float group_sum(float v) {
-    float a, b;
+    unsigned x = __builtin_bit_cast(unsigned, v), y = x;
 #if MF == 16
-    pair16(v, a, b);
-    v = a + b;
+    asm volatile(RC_PAIR_OP("v_permlane16_swap_b32", "v_add_f32") : "+v"(x), "+v"(y));
+    y = x;
 #endif
-    pair32(v, a, b);
-    return a + b;
+    asm volatile(RC_PAIR_OP("v_permlane32_swap_b32", "v_add_f32") : "+v"(x), "+v"(y));
+    return __builtin_bit_cast(float, x);
+}
+
+// Key tiles seen by query tile t, and the number of work items it is cut into.
+constexpr int tiles_of(int t) { return CAUSAL ? (t * BM + BM - 1) / BN + 1 : AS / BN; }
+constexpr int chunks_of(int t) { return CHUNK > 0 ? (tiles_of(t) + CHUNK - 1) / CHUNK : 1; }
+constexpr int items_per_head() {
+    int n = 0;
+    for (int t = 0; t < NQT; ++t) n += chunks_of(t);
+    return n;
+}
+constexpr int max_chunks() {
+    int n = 1;
+    for (int t = 0; t < NQT; ++t) n = chunks_of(t) > n ? chunks_of(t) : n;
+    return n;
+}
+// Query tile at position k of the launch order: 0 in order, 1 longest
+// first, 2 paired (k and k + NQT / 2 take tiles NQT - 1 - k and k).
+constexpr int order_tile(int k) {
+    return ORDER == 1 ? NQT - 1 - k : ORDER == 2 ? (k < NQT / 2 ? NQT - 1 - k : k - NQT / 2) : k;
+}
+
+// Exponential weight of a state with maximum x relative to the joint maximum
+// mt >= x; a state that saw no key (x = mt = -inf) gets weight 1 on its zero
+// sums instead of a NaN.
+__device__ __forceinline__ float rel_weight(float x, float mt) {
+    return x == mt ? 1.0f : __builtin_amdgcn_exp2f(x - mt);
+}
+
+// Normalise the transposed output accumulators and store the bf16 rows.
+__device__ __forceinline__ void store_out(bf16_t *O, size_t base, int q0w, int lane,
+                                          const accT (&o)[QB][DB], const float (&l)[QB]) {
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+        const int q = q0w + qb * MF + lane % MF;
+        const float inv = 1.0f / l[qb];
+        bf16_t *orow = O + base + (size_t)q * AD;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int g = 0; g < ACCN / 4; ++g) {
+#if MF == 16
+                const int d = db * 16 + 4 * (lane >> 4);
+#else
+                const int d = db * 32 + g * 8 + 4 * (lane >> 5);
+#endif
+                u32x2 w;
+                w[0] = pack2(o[qb][db][g * 4 + 0] * inv, o[qb][db][g * 4 + 1] * inv);
+                w[1] = pack2(o[qb][db][g * 4 + 2] * inv, o[qb][db][g * 4 + 3] * inv);
+                *(u32x2 *)(orow + d) = w;
+            }
+    }
 }
 
 extern "C" __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
@@ -208,27 +263,34 @@ void rc_attention(AttnArgs args) {
     const int rg = wave % NW, sp = wave / NW, tids = tid % NTS;
     bf16_t *const Kbase = smem + sp * NBUF * (KT_ELEMS + VT_ELEMS);
     bf16_t *const Vbase = Kbase + NBUF * KT_ELEMS;
+    // work item: head bh, j-th item of its launch order (ORDER 0 keeps a
+    // head's items together, 1 and 2 interleave the heads)
     const int bid = blockIdx.x;
-#if ORDER == 1
-    const int qt = NQT - 1 - bid / (AB * AH);
-    const int bh = bid % (AB * AH);
-#elif ORDER == 2
-    const int half = (NQT / 2) * AB * AH;
-    const int qt = bid < half ? NQT - 1 - bid / (AB * AH) : (bid - half) / (AB * AH);
-    const int bh = bid % (AB * AH);
+#if ORDER == 0
+    const int bh = bid / items_per_head();
+    int j = bid % items_per_head();
 #else
-    const int qt = bid % NQT;
-    const int bh = bid / NQT;
+    const int bh = bid % (AB * AH);
+    int j = bid / (AB * AH);
+#endif
+    int qt = order_tile(j), ch = 0;
+#if CHUNK > 0
+    for (int k = 0; k < NQT; ++k) {
+        const int t = order_tile(k), n = chunks_of(t);
+        if (j < n) {
+            qt = t;
+            ch = j;
+            break;
+        }
+        j -= n;
+    }
 #endif
     const int q0 = qt * BM;
     const int q0w = q0 + rg * RPW;
     const size_t base = (size_t)bh * AS * AD;
-
-#if CAUSAL
-    const int n_kt = (q0 + BM - 1) / BN + 1;
-#else
-    const int n_kt = AS / BN;
-#endif
+    // key tiles kt0 .. kt0 + n_kt - 1; the loops below count kt from 0
+    const int kt0 = ch * CHUNK;
+    const int n_kt = CHUNK > 0 ? min(CHUNK, tiles_of(qt) - kt0) : tiles_of(qt);
 #if STAGES == 4
     // Direct-to-LDS loads: one global_load_lds_dwordx4 moves 64 lanes x 16 B
     // into 1 KiB of LDS at a wave-uniform base (M0), lane i at byte 16 i.
@@ -264,8 +326,8 @@ void rc_attention(AttnArgs args) {
     };
     // tile kt into ring buffer b
     auto gload_lds = [&](int kt, int b) {
-        const bf16_t *Kg = args.K + base + (size_t)kt * BN * AD;
-        const bf16_t *Vg = args.V + base + (size_t)kt * BN * AD;
+        const bf16_t *Kg = args.K + base + (size_t)(kt0 + kt) * BN * AD;
+        const bf16_t *Vg = args.V + base + (size_t)(kt0 + kt) * BN * AD;
 #pragma unroll
         for (int j = 0; j < WL; ++j) dma(Kg, k_src[j], KA[b] + j * 1024u);
 #pragma unroll
@@ -314,8 +376,8 @@ void rc_attention(AttnArgs args) {
     for (int ks = 0; ks < AD / KSTEP; ++ks) koff[ks] = kswz(lane % MF, ks * (KSTEP / 8) + lane / MF);
 
     auto gload = [&](int kt) {
-        const bf16_t *Kg = args.K + base + (size_t)kt * BN * AD;
-        const bf16_t *Vg = args.V + base + (size_t)kt * BN * AD;
+        const bf16_t *Kg = args.K + base + (size_t)(kt0 + kt) * BN * AD;
+        const bf16_t *Vg = args.V + base + (size_t)(kt0 + kt) * BN * AD;
 #pragma unroll
         for (int i = 0; i < K_LOADS; ++i) {
             int idx = tids + i * NTS;
@@ -367,7 +429,7 @@ void rc_attention(AttnArgs args) {
     // true when every key of tile kt is masked for this wave's queries
     auto skipped = [&](int kt) {
 #if CAUSAL
-        return kt * BN > q0w + RPW - 1;
+        return (kt0 + kt) * BN > q0w + RPW - 1;
 #else
         (void)kt;
         return false;
@@ -414,7 +476,7 @@ void rc_attention(AttnArgs args) {
         // scale is folded into the exponent's fused multiply-add
 #if CAUSAL
         // only a tile that crosses this wave's diagonal needs the mask
-        const bool diag = kt * BN + BN - 1 > q0w;
+        const bool diag = (kt0 + kt) * BN + BN - 1 > q0w;
 #endif
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
@@ -426,7 +488,7 @@ void rc_attention(AttnArgs args) {
                 for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
                     for (int r = 0; r < ACCN; ++r)
-                        if (kt * BN + kb * MF + key_of(r, lane) > q) sc[qb][kb][r] = -__builtin_inff();
+                        if ((kt0 + kt) * BN + kb * MF + key_of(r, lane) > q) sc[qb][kb][r] = -__builtin_inff();
             }
 #endif
 #pragma unroll
@@ -631,7 +693,7 @@ void rc_attention(AttnArgs args) {
         for (int qb = 0; qb < QB; ++qb) {
             const float mp = w[qb * 2 * MF + lane % MF], lp = w[qb * 2 * MF + MF + lane % MF];
             const float mt = fmaxf(m[qb], mp);
-            const float a0 = __builtin_amdgcn_exp2f(m[qb] - mt), a1 = __builtin_amdgcn_exp2f(mp - mt);
+            const float a0 = rel_weight(m[qb], mt), a1 = rel_weight(mp, mt);
             l[qb] = l[qb] * a0 + lp * a1;
             m[qb] = mt;
 #pragma unroll
@@ -643,25 +705,68 @@ void rc_attention(AttnArgs args) {
     }
 #endif
 
+#if CHUNK > 0
+    if (chunks_of(qt) > 1) {
+        // one of several items of this query tile: leave the state for the
+        // combine kernel, same layout as the split merge area
+        float *w = args.P + ((size_t)(bh * NQT + qt) * max_chunks() + ch) * (NW * WSLOT) + rg * WSLOT;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+            if (lane < MF) {
+                w[qb * 2 * MF + lane] = m[qb];
+                w[qb * 2 * MF + MF + lane] = l[qb];
+            }
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+                for (int r = 0; r < ACCN; ++r) w[QB * 2 * MF + ((qb * DB + db) * ACCN + r) * 64 + lane] = o[qb][db][r];
+        return;
+    }
+#endif
+    store_out(args.O, base, q0w, lane, o, l);
+}
+
+#if CHUNK > 0
+// Merge the partial states of the query tiles that were cut into several
+// work items (rescale each to the joint maximum, add, normalise).  One
+// workgroup per query tile, one wave per row group, lanes laid out as in
+// rc_attention.
+extern "C" __global__ __launch_bounds__(64 * NW) void rc_attention_combine(AttnArgs args) {
+    const int lane = threadIdx.x & 63, rg = threadIdx.x >> 6;
+    const int bh = blockIdx.x / NQT, qt = blockIdx.x % NQT;
+    const int nc = chunks_of(qt);
+    if (nc == 1) return;
+    const float *w = args.P + (size_t)(bh * NQT + qt) * max_chunks() * (NW * WSLOT) + rg * WSLOT;
+    accT o[QB][DB];
+    float m[QB], l[QB];
+    // chunk 0 holds key tile 0, which every query sees: its maximum is finite
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
-        const int q = q0w + qb * MF + lane % MF;
-        const float inv = 1.0f / l[qb];
-        bf16_t *orow = args.O + base + (size_t)q * AD;
+        m[qb] = w[qb * 2 * MF + lane % MF];
+        l[qb] = w[qb * 2 * MF + MF + lane % MF];
 #pragma unroll
         for (int db = 0; db < DB; ++db)
 #pragma unroll
-            for (int g = 0; g < ACCN / 4; ++g) {
-#if MF == 16
-                const int d = db * 16 + 4 * (lane >> 4);
-#else
-                const int d = db * 32 + g * 8 + 4 * (lane >> 5);
-#endif
-                u32x2 w;
-                w[0] = pack2(o[qb][db][g * 4 + 0] * inv, o[qb][db][g * 4 + 1] * inv);
-                w[1] = pack2(o[qb][db][g * 4 + 2] * inv, o[qb][db][g * 4 + 3] * inv);
-                *(u32x2 *)(orow + d) = w;
-            }
+            for (int r = 0; r < ACCN; ++r) o[qb][db][r] = w[QB * 2 * MF + ((qb * DB + db) * ACCN + r) * 64 + lane];
     }
+    for (int c = 1; c < nc; ++c) {
+        const float *v = w + (size_t)c * (NW * WSLOT);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+            const float mp = v[qb * 2 * MF + lane % MF], lp = v[qb * 2 * MF + MF + lane % MF];
+            const float mt = fmaxf(m[qb], mp);
+            const float a0 = rel_weight(m[qb], mt), a1 = rel_weight(mp, mt);
+            l[qb] = l[qb] * a0 + lp * a1;
+            m[qb] = mt;
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+                for (int r = 0; r < ACCN; ++r)
+                    o[qb][db][r] = o[qb][db][r] * a0 + v[QB * 2 * MF + ((qb * DB + db) * ACCN + r) * 64 + lane] * a1;
+        }
+    }
+    store_out(args.O, (size_t)bh * AS * AD, qt * BM + rg * RPW, lane, o, l);
 }
-
+#endif

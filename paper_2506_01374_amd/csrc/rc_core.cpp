@@ -94,6 +94,7 @@ static std::vector<KnobDef> attention_knobs() {
         {"order", "Parallel", {0, 1, 2}, 0},
         {"occ", "Parallel", {1, 2}, 1},
         {"splits", "Parallel", {1, 2, 4}, 1},
+        {"chunk", "Parallel", {0, 4, 8, 16}, 0},   // key tiles per work item (0: whole row)
     };
 }
 
@@ -300,6 +301,9 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
                 if (wgs * lds > LDS_LIMIT)
                     return fmt("%lld workgroups of %lld B LDS do not fit a CU", (long long)wgs, (long long)lds);
             }
+            int ch = kv(d, s, "chunk");
+            if (ch > 0 && ch >= S / bn)
+                return fmt("chunk of %d key tiles covers all %lld key tiles (same as chunk 0)", ch, (long long)(S / bn));
             if (kv(d, s, "order") == 2 && (S / bm) % 2)
                 return "paired tile order needs an even number of query tiles";
             return "";

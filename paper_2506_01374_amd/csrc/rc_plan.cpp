@@ -58,6 +58,7 @@ struct MoeCombineArgs {
 struct AttnArgs {
     const void *Q, *K, *V;
     void *O;
+    void *P;   // partial states of query tiles cut into several work items
 };
 
 struct Source {
@@ -428,26 +429,49 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
         }
         case RC_OP_ATTENTION: {
             long B = D[0], Hh = D[1], S = D[2], Dh = D[3];
-            int bm = kv(d, s, "block_m"), w = kv(d, s, "waves");
+            int bm = kv(d, s, "block_m"), bn = kv(d, s, "block_n"), w = kv(d, s, "waves");
+            int mf = kv(d, s, "mfma"), chunk = kv(d, s, "chunk");
+            bool causal = (d->flags & RC_FLAG_CAUSAL) != 0;
+            // work items: query tile t sees tiles(t) key tiles, cut into
+            // chunks of at most `chunk` tiles
+            long nqt = S / bm, items = 0, maxch = 1;
+            for (long t = 0; t < nqt; ++t) {
+                long tiles = causal ? (t * bm + bm - 1) / bn + 1 : S / bn;
+                long nc = chunk > 0 ? (tiles + chunk - 1) / chunk : 1;
+                items += nc;
+                maxch = std::max(maxch, nc);
+            }
+            // partial state per (head, query tile, chunk): for every wave, m
+            // and l of its rows, then its output accumulators
+            long qb = bm / w / mf, accn = mf == 16 ? 4 : 16;
+            long wslot = qb * 2 * mf + qb * (Dh / mf) * accn * 64;
+            size_t offP = chunk > 0 ? ws.add((size_t)B * Hh * nqt * maxch * w * wslot * 4) : 0;
             Kern k;
             double scale_log2 = 1.4426950408889634 / std::sqrt((double)Dh);
             char sbuf[64];
             snprintf(sbuf, sizeof sbuf, "#define SCALE_LOG2 %.17gf\n", scale_log2);
             k.src = Source{SRC_attention, "rc_attention",
-                           def("BM", bm) + def("BN", kv(d, s, "block_n")) + def("NW", w) +
-                               def("MF", kv(d, s, "mfma")) + def("STAGES", kv(d, s, "stages")) +
+                           def("BM", bm) + def("BN", bn) + def("NW", w) +
+                               def("MF", mf) + def("STAGES", kv(d, s, "stages")) +
                                def("VEC", kv(d, s, "vec")) + def("UNROLL", kv(d, s, "unroll")) +
                                def("ORDER", kv(d, s, "order")) + def("OCC", kv(d, s, "occ")) +
-                               def("SPLITS", kv(d, s, "splits")) +
+                               def("SPLITS", kv(d, s, "splits")) + def("CHUNK", chunk) +
                                def("AB", B) + def("AH", Hh) +
                                def("AS", S) + def("AD", Dh) +
-                               def("CAUSAL", (d->flags & RC_FLAG_CAUSAL) ? 1 : 0) + sbuf};
-            k.grid = dim3((unsigned)(B * Hh * (S / bm)), 1, 1);
+                               def("CAUSAL", causal ? 1 : 0) + sbuf};
+            k.grid = dim3((unsigned)(B * Hh * items), 1, 1);
             k.block = dim3(64 * w * kv(d, s, "splits"), 1, 1);
-            k.bind = [](const rc_args *a, char *, std::vector<char> &b) {
-                put(b, AttnArgs{a->in[0], a->in[1], a->in[2], a->out[0]});
+            k.bind = [=](const rc_args *a, char *ws_base, std::vector<char> &b) {
+                put(b, AttnArgs{a->in[0], a->in[1], a->in[2], a->out[0], chunk > 0 ? ws_base + offP : nullptr});
             };
             p.kerns.push_back(k);
+            if (chunk > 0) {
+                Kern kc = k;
+                kc.src.entry = "rc_attention_combine";
+                kc.grid = dim3((unsigned)(B * Hh * nqt), 1, 1);
+                kc.block = dim3(64 * w, 1, 1);
+                p.kerns.push_back(kc);
+            }
             p.dominant = 0;
             break;
         }

@@ -10,6 +10,15 @@ kernel's reading of the same counter).
 
   python -m paper_2506_01374_amd.profiling stats DIR [--kernel NAME]
   python -m paper_2506_01374_amd.profiling counter DIR COUNTER KERNEL_SUBSTRING
+  python -m paper_2506_01374_amd.profiling traffic --workload NAME --schedule KEY \
+      --kernel SUBSTRING --source FILE --fetch DIR --write DIR --cal-fetch DIR \
+      --cal-write DIR --copy-bytes N [--copy-kernel SUBSTRING] [--command CMD ...] \
+      --out profiles/traffic.json
+
+``traffic`` converts the two counter runs of a kernel and the two runs of
+a plain copy of N bytes into HBM bytes per launch and records them, keyed
+by workload, with the schedule and the sha1 of the kernel source they were
+taken for (the benchmark reports them only while both still match).
 """
 from __future__ import annotations
 
@@ -56,8 +65,57 @@ def counter_per_dispatch(dirpath: str, counter: str, kernel_sub: str) -> Dict[st
     return {"kernel": name, "dispatches": len(v), "mean": sum(v) / len(v), "min": min(v), "max": max(v)}
 
 
+def traffic_record(schedule: str, kernel_sub: str, source: str, fetch_dir: str, write_dir: str,
+                   cal_fetch_dir: str, cal_write_dir: str, copy_bytes: int,
+                   commands: List[str], copy_kernel: str = "copyBuffer") -> Dict[str, object]:
+    import hashlib
+    fk = counter_per_dispatch(fetch_dir, "FETCH_SIZE", kernel_sub)
+    wk = counter_per_dispatch(write_dir, "WRITE_SIZE", kernel_sub)
+    # the calibration runs also fill the source buffer; only the copy counts
+    cf = counter_per_dispatch(cal_fetch_dir, "FETCH_SIZE", copy_kernel)
+    cw = counter_per_dispatch(cal_write_dir, "WRITE_SIZE", copy_kernel)
+    for what, r in (("kernel FETCH_SIZE", fk), ("kernel WRITE_SIZE", wk), ("copy FETCH_SIZE", cf),
+                    ("copy WRITE_SIZE", cw)):
+        if not r["dispatches"]:
+            raise SystemExit(f"no dispatches found for {what}")
+    fscale = copy_bytes / (cf["mean"] * 1024.0)
+    wscale = copy_bytes / (cw["mean"] * 1024.0)
+    fb = fk["mean"] * 1024.0 * fscale
+    wb = wk["mean"] * 1024.0 * wscale
+    return {"key": schedule, "kernel": fk["kernel"],
+            "kernel_source_sha1": hashlib.sha1(open(source, "rb").read()).hexdigest()[:16],
+            "fetch_kib_per_dispatch": fk["mean"], "write_kib_per_dispatch": wk["mean"],
+            "dispatches": [fk["dispatches"], wk["dispatches"]],
+            "copy_reference_bytes": copy_bytes, "copy_kernel": cf["kernel"],
+            "copy_fetch_kib": cf["mean"], "copy_write_kib": cw["mean"],
+            "fetch_scale": fscale, "write_scale": wscale,
+            "fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
+            "bytes_per_launch": fb + wb, "commands": commands}
+
+
 def main(argv=None):
     argv = argv or sys.argv[1:]
+    if argv[:1] == ["traffic"]:
+        import argparse
+        import json
+        ap = argparse.ArgumentParser(prog="profiling traffic")
+        for flag in ("--workload", "--schedule", "--kernel", "--source", "--fetch", "--write",
+                     "--cal-fetch", "--cal-write", "--out"):
+            ap.add_argument(flag, required=True)
+        ap.add_argument("--copy-bytes", type=int, required=True)
+        ap.add_argument("--copy-kernel", default="copyBuffer", help="name substring of the copy kernel")
+        ap.add_argument("--command", action="append", default=[])
+        a = ap.parse_args(argv[1:])
+        rec = traffic_record(a.schedule, a.kernel, a.source, a.fetch, a.write, a.cal_fetch,
+                             a.cal_write, a.copy_bytes, a.command, a.copy_kernel)
+        table = json.load(open(a.out)) if os.path.exists(a.out) else {}
+        table[a.workload] = rec
+        with open(a.out, "w") as f:
+            json.dump(table, f, indent=2)
+            f.write("\n")
+        print(json.dumps({k: rec[k] for k in ("kernel", "fetch_kib_per_dispatch", "write_kib_per_dispatch",
+                                              "fetch_scale", "bytes_per_launch")}))
+        return
     if argv[:1] == ["stats"]:
         for r in kernel_stats(argv[1]):
             print(f"{r['name'][:60]:60s} calls={r['calls']:6d} avg={r['avg_ns'] / 1e3:9.3f} us "
