@@ -18,7 +18,9 @@
 //                softmax (software pipeline); 4: direct global-to-LDS loads
 //                into a ring of three K/V buffers, two tiles in flight
 //                while one is computed, V kept key-major and read with the
-//                transposing LDS load (ComputeLocation)
+//                transposing LDS load; 5: as 4 with a ring of four and the
+//                scores of the next tile computed ahead of this tile's
+//                softmax (ComputeLocation)
 //   VEC          bf16 per global load of K (Vectorize)
 //   UNROLL       unroll factor of the key-tile loop (Unroll)
 //   ORDER        0: query tiles in order; 1: longest (last) query tiles
@@ -51,7 +53,8 @@
 #define QB (RPW / MF)
 #define NTS (64 * NW)
 #define NT (NTS * SPLITS)
-#define NBUF (STAGES == 4 ? 3 : STAGES > 1 ? 2 : 1)
+#define NBUF (STAGES > 1 ? 2 : 1)      // register-staged paths
+#define RING (STAGES == 5 ? 4 : 3)     // direct-to-LDS paths
 #define KB (BN / MF)
 #define DB (AD / MF)
 #define NQT (AS / BM)
@@ -247,11 +250,13 @@ __device__ __forceinline__ void store_out(bf16_t *O, size_t base, int q0w, int l
 
 extern "C" __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
 void rc_attention(AttnArgs args) {
-#if STAGES == 4
-    // three distinct LDS objects per operand, so the compiler can tell the
-    // buffer being filled by direct-to-LDS loads from the one being read
+#if STAGES >= 4
+    // one LDS object per ring buffer and operand
     __shared__ __attribute__((aligned(16))) bf16_t K0[KT_ELEMS], K1[KT_ELEMS], K2[KT_ELEMS];
     __shared__ __attribute__((aligned(16))) bf16_t V0[KT_ELEMS], V1[KT_ELEMS], V2[KT_ELEMS];
+#if RING == 4
+    __shared__ __attribute__((aligned(16))) bf16_t K3[KT_ELEMS], V3[KT_ELEMS];
+#endif
     bf16_t *const smem = K0;                 // unused (no register-staged tiles)
 #else
     // one LDS block: per split, NBUF K tiles then NBUF V^T tiles; reused for
@@ -291,7 +296,7 @@ void rc_attention(AttnArgs args) {
     // key tiles kt0 .. kt0 + n_kt - 1; the loops below count kt from 0
     const int kt0 = ch * CHUNK;
     const int n_kt = CHUNK > 0 ? min(CHUNK, tiles_of(qt) - kt0) : tiles_of(qt);
-#if STAGES == 4
+#if STAGES >= 4
     // Direct-to-LDS loads: one global_load_lds_dwordx4 moves 64 lanes x 16 B
     // into 1 KiB of LDS at a wave-uniform base (M0), lane i at byte 16 i.
     // The swizzles are applied by choosing which global chunk each lane
@@ -316,10 +321,17 @@ void rc_attention(AttnArgs args) {
     // LDS byte addresses of the ring buffers and this wave's first 1 KiB
     typedef __attribute__((address_space(3))) bf16_t *lds_p;
     const unsigned wl0 = (unsigned)__builtin_amdgcn_readfirstlane(wave) * WL * 1024u;
+#if RING == 4
+    const unsigned KA[4] = {(unsigned)(size_t)(lds_p)K0 + wl0, (unsigned)(size_t)(lds_p)K1 + wl0,
+                            (unsigned)(size_t)(lds_p)K2 + wl0, (unsigned)(size_t)(lds_p)K3 + wl0};
+    const unsigned VA[4] = {(unsigned)(size_t)(lds_p)V0 + wl0, (unsigned)(size_t)(lds_p)V1 + wl0,
+                            (unsigned)(size_t)(lds_p)V2 + wl0, (unsigned)(size_t)(lds_p)V3 + wl0};
+#else
     const unsigned KA[3] = {(unsigned)(size_t)(lds_p)K0 + wl0, (unsigned)(size_t)(lds_p)K1 + wl0,
                             (unsigned)(size_t)(lds_p)K2 + wl0};
     const unsigned VA[3] = {(unsigned)(size_t)(lds_p)V0 + wl0, (unsigned)(size_t)(lds_p)V1 + wl0,
                             (unsigned)(size_t)(lds_p)V2 + wl0};
+#endif
     auto dma = [&](const bf16_t *gbase, unsigned off, unsigned lds_addr) {
         asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
                      :: "v"(off), "s"(gbase), "s"(lds_addr) : "memory", "m0");
@@ -333,9 +345,10 @@ void rc_attention(AttnArgs args) {
 #pragma unroll
         for (int j = 0; j < WL; ++j) dma(Vg, v_src[j], VA[b] + j * 1024u);
     };
-    // the first two key tiles are in flight while Q is read
-    gload_lds(0, 0);
-    if (n_kt > 1) gload_lds(1, 1);
+    // the first RING - 1 key tiles are in flight while Q is read
+#pragma unroll
+    for (int t = 0; t < RING - 1; ++t)
+        if (t < n_kt) gload_lds(t, t);
 #endif
     bf16x8 qf[QB][AD / KSTEP];
 #pragma unroll
@@ -344,7 +357,7 @@ void rc_attention(AttnArgs args) {
         for (int ks = 0; ks < AD / KSTEP; ++ks)
             qf[qb][ks] = *(const bf16x8 *)(args.Q + base + (size_t)(q0w + qb * MF + lane % MF) * AD +
                                            ks * KSTEP + 8 * (lane / MF));
-#if STAGES == 4
+#if STAGES >= 4
     // Consume Q here so that the compiler's wait for it (a full vmcnt drain,
     // which also lands tiles 0 and 1) sits before the loop rather than in it.
 #pragma unroll
@@ -456,7 +469,7 @@ void rc_attention(AttnArgs args) {
     };
     auto scores = [&](int s, accT (&sc)[QB][KB]) { scores_at(Kbase + s * KT_ELEMS, sc); };
 
-#if STAGES == 4
+#if STAGES >= 4
     // per-lane offsets (elements, relative to the V buffer) of the row and
     // column this lane addresses in the transposing read of key block j,
     // half h, d block db: row 32 j + 16 h + 4 (lane / 16) + (lane % 16) / 4,
@@ -546,7 +559,7 @@ void rc_attention(AttnArgs args) {
             }
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
-#if STAGES == 4
+#if STAGES >= 4
                 typedef short v4i16 __attribute__((ext_vector_type(4)));
                 typedef __attribute__((address_space(3))) v4i16 *lds_v4p;
                 const bf16_t *const vp = Vt + voff[db] + 32 * j * AD;
@@ -607,6 +620,38 @@ void rc_attention(AttnArgs args) {
         body(kt, K0, V0, 2);
         if (kt + 1 < n_kt) body(kt + 1, K1, V1, 0);
         if (kt + 2 < n_kt) body(kt + 2, K2, V2, 1);
+    }
+#undef WAIT_VM
+#elif STAGES == 5
+    (void)n_it;
+    (void)compute;
+#define WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | ((((n) >> 4) & 3) << 14) | (7 << 4) | (15 << 8))
+    // Software pipeline over a ring of four: iteration kt issues the score
+    // MFMAs of tile kt + 1 ahead of tile kt's softmax, so the matrix unit
+    // works while the exponentials and reductions run, then P V of tile kt.
+    // Tile kt sits in buffer kt % 4; buffer (kt + 3) % 4 held tile kt - 1
+    // (its K was read in iteration kt - 2, its V in kt - 1, both before the
+    // last barrier) and receives tile kt + 3.
+    accT sc_a[QB][KB], sc_b[QB][KB];
+    if (!skipped(0)) scores_at(K0, sc_a);
+    auto body = [&](int kt, accT (&cur)[QB][KB], accT (&nxt)[QB][KB], const bf16_t *kn,
+                    const bf16_t *vc, int fill) {
+        if (kt + 3 < n_kt) gload_lds(kt + 3, fill);
+        if (kt + 1 < n_kt && !skipped(kt + 1)) scores_at(kn, nxt);
+        if (!skipped(kt)) softmax_pv_at(kt, vc, cur);
+        if (kt + 3 < n_kt) {
+            WAIT_VM(2 * WL);       // tiles up to kt + 2 have landed; kt + 3 may be in flight
+        } else {
+            WAIT_VM(0);
+        }
+        __builtin_amdgcn_s_waitcnt(0xC07F);      // lgkmcnt(0): this wave's LDS reads are done
+        asm volatile("s_barrier" ::: "memory");
+    };
+    for (int kt = 0; kt < n_kt; kt += 4) {
+        body(kt, sc_a, sc_b, K1, V0, 3);
+        if (kt + 1 < n_kt) body(kt + 1, sc_b, sc_a, K2, V1, 0);
+        if (kt + 2 < n_kt) body(kt + 2, sc_a, sc_b, K3, V2, 1);
+        if (kt + 3 < n_kt) body(kt + 3, sc_b, sc_a, K0, V3, 2);
     }
 #undef WAIT_VM
 #elif STAGES == 3

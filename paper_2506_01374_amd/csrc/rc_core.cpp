@@ -88,7 +88,7 @@ static std::vector<KnobDef> attention_knobs() {
         {"block_n", "TileSize", {32, 64, 128}, 32},
         {"waves", "Parallel", {1, 2, 4, 8}, 1},
         {"mfma", "TileSize", {16, 32}, 16},
-        {"stages", "ComputeLocation", {1, 2, 3, 4}, 1},
+        {"stages", "ComputeLocation", {1, 2, 3, 4, 5}, 1},
         {"vec", "Vectorize", {2, 4, 8}, 2},
         {"unroll", "Unroll", {1, 2}, 1},
         {"order", "Parallel", {0, 1, 2}, 0},
@@ -271,7 +271,7 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
                 return fmt("head dim %lld must be 32, 64, 128 or 256", (long long)Dh);
             int sp = kv(d, s, "splits");
             if (w * sp > 16) return fmt("waves x splits = %d exceeds 16 waves per workgroup", w * sp);
-            if (st == 4) {
+            if (st >= 4) {
                 // direct-to-LDS ring: whole 1 KiB wave-loads, key-major V read
                 // by the 16x16 transposing load, one key split
                 if (mf != 16) return "direct-to-LDS attention uses the 16x16 MFMA shape";
@@ -285,7 +285,7 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
             // K tile + padded V^T tile per stage and split (three plain K/V
             // tiles for the direct-to-LDS ring)
             int64_t vts = bn + (mf == 16 ? 16 : 8);   // padded V^T row
-            int64_t lds = st == 4 ? 3 * 2 * (int64_t)bn * Dh * 2
+            int64_t lds = st >= 4 ? (st == 5 ? 4 : 3) * 2 * (int64_t)bn * Dh * 2
                                   : (int64_t)sp * (st > 1 ? 2 : 1) * ((int64_t)bn * Dh + Dh * vts) * 2;
             if (lds > LDS_LIMIT) return fmt("LDS %lld B exceeds limit", (long long)lds);
             int64_t mf_acc = (mf == 16) ? 4 : 16;

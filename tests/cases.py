@@ -75,6 +75,10 @@ SCHEDULES = {
         "block_m=32,block_n=32,waves=2,mfma=16,stages=2,vec=8,unroll=1,order=1,chunk=4",
         "block_m=64,block_n=32,waves=2,mfma=32,stages=2,vec=8,unroll=1,order=0,splits=2,chunk=4",
         "block_m=256,block_n=32,waves=8,mfma=16,stages=2,vec=8,unroll=1,order=0,chunk=4",
+        "block_m=64,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=1,order=2,occ=2",
+        "block_m=32,block_n=64,waves=2,mfma=16,stages=5,vec=8,unroll=1,order=0",
+        "block_m=64,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=1,order=2,occ=2,chunk=4",
+        "block_m=128,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=1,order=1",
     ],
     "attn_full": [
         "",
@@ -84,11 +88,13 @@ SCHEDULES = {
         "block_m=64,block_n=64,waves=4,mfma=16,stages=3,vec=8,unroll=1,order=0,splits=2",
         "block_m=64,block_n=64,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=0",
         "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=0,chunk=4",
+        "block_m=64,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=1,order=0",
     ],
     "attn_d64": [
         "block_m=64,block_n=32,waves=2,mfma=32,stages=2,vec=8,unroll=1,order=0",
         "block_m=32,block_n=64,waves=2,mfma=16,stages=1,vec=4,unroll=1,order=1",
         "block_m=32,block_n=32,waves=2,mfma=16,stages=4,vec=8,unroll=1,order=0",
+        "block_m=32,block_n=32,waves=2,mfma=16,stages=5,vec=8,unroll=1,order=0",
     ],
     "mlp": [
         "",
