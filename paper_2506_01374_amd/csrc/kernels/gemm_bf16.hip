@@ -14,7 +14,9 @@
 //                (ComputeLocation); 4: direct-to-LDS loads
 //                (global_load_lds_dwordx4) into a ring of three LDS buffers,
 //                two K tiles in flight, no register staging (weights stored
-//                [N][K], 16-byte vectors, non-im2col rows)
+//                [N][K], 16-byte vectors, non-im2col rows); 5: as 2 with two
+//                register sets, each tile's global loads issued two tiles
+//                before its LDS store
 //   VEC          bf16 elements per global load: 2, 4 or 8 (Vectorize)
 //   UNROLL       unroll factor of the K-tile loop (Unroll)
 //   LAYOUT       weights stored 0: [K][N], 1: [N][K] (Layout)
@@ -54,6 +56,8 @@
 #define NTN (GN / TN)
 
 typedef unsigned short bf16_t;
+
+template <int V> struct IntC { static constexpr int value = V; };
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -229,10 +233,12 @@ void rc_gemm_bf16(GemmBf16Args args) {
 #pragma unroll
                 for (int r = 0; r < ACCN; ++r) acc[b][i][j][r] = 0.f;
 
-    vecT ra[A_LOADS];
-    vecT rb[NB][B_LOADS];
+    // register staging sets: tile t uses set t % NSET
+#define NSET (STAGES == 5 ? 2 : 1)
+    vecT ra[NSET][A_LOADS];
+    vecT rb[NSET][NB][B_LOADS];
 
-    auto gload = [&](int k0) {
+    auto gload = [&](int k0, int set) {
 #pragma unroll
         for (int i = 0; i < A_LOADS; ++i) {
             int v = tid + i * NT;
@@ -243,9 +249,9 @@ void rc_gemm_bf16(GemmBf16Args args) {
             int ih = a_p[i] + tap / CV_S - CV_PAD, iw = a_q[i] + tap % CV_S - CV_PAD;
             bool ok = aval[i] && ih >= 0 && ih < CV_H && iw >= 0 && iw < CV_W;
             const bf16_t *src = args.A + (((size_t)a_n[i] * CV_H + (ok ? ih : 0)) * CV_W + (ok ? iw : 0)) * CV_C + ch;
-            ra[i] = ok ? *(const vecT *)src : (vecT)0;
+            ra[set][i] = ok ? *(const vecT *)src : (vecT)0;
 #else
-            ra[i] = aval[i] ? *(const vecT *)(arow[i] + k0 + c) : (vecT)0;
+            ra[set][i] = aval[i] ? *(const vecT *)(arow[i] + k0 + c) : (vecT)0;
 #endif
         }
 #pragma unroll
@@ -258,19 +264,19 @@ void rc_gemm_bf16(GemmBf16Args args) {
             int r = v / (TN / VEC), c = (v % (TN / VEC)) * VEC;
             size_t off = (size_t)(k0 + r) * GN + n0 + c;
 #endif
-            rb[0][i] = *(const vecT *)(B0 + off);
+            rb[set][0][i] = *(const vecT *)(B0 + off);
 #if NB == 2
-            rb[1][i] = *(const vecT *)(B1 + off);
+            rb[set][1][i] = *(const vecT *)(B1 + off);
 #endif
         }
     };
 
-    auto swrite = [&](int s) {
+    auto swrite = [&](int s, int set) {
 #pragma unroll
         for (int i = 0; i < A_LOADS; ++i) {
             int v = tid + i * NT;
             int r = v / (TK / VEC), c = (v % (TK / VEC)) * VEC;
-            lds_store_vec(As[s], swz(r, c >> 3) + (c & 7), ra[i]);
+            lds_store_vec(As[s], swz(r, c >> 3) + (c & 7), ra[set][i]);
         }
 #pragma unroll
         for (int b = 0; b < NB; ++b)
@@ -279,12 +285,12 @@ void rc_gemm_bf16(GemmBf16Args args) {
                 int v = tid + i * NT;
 #if LAYOUT == 1
                 int r = v / (TK / VEC), c = (v % (TK / VEC)) * VEC;
-                lds_store_vec(Bs[s][b], swz(r, c >> 3) + (c & 7), rb[b][i]);
+                lds_store_vec(Bs[s][b], swz(r, c >> 3) + (c & 7), rb[set][b][i]);
 #else
                 int kr = v / (TN / VEC), c = (v % (TN / VEC)) * VEC;
 #pragma unroll
                 for (int j = 0; j < VEC; ++j)
-                    Bs[s][b][swz(c + j, kr >> 3) + (kr & 7)] = vec_elem(rb[b][i], j);
+                    Bs[s][b][swz(c + j, kr >> 3) + (kr & 7)] = vec_elem(rb[set][b][i], j);
 #endif
             }
     };
@@ -429,30 +435,52 @@ void rc_gemm_bf16(GemmBf16Args args) {
 #elif STAGES == 1
 #pragma unroll UNROLL
     for (int kt = 0; kt < KTILES; ++kt) {
-        gload(kt * TK);
-        swrite(0);
+        gload(kt * TK, 0);
+        swrite(0, 0);
         __syncthreads();
         compute(0, nothing);
         __syncthreads();
     }
+#elif STAGES == 5
+    // Tile t lives in register set t % 2 and LDS buffer t % 2.  Its loads are
+    // issued at the end of iteration t - 3 (right after the set's previous
+    // tile was stored) and it is stored at the end of iteration t - 1, so two
+    // tiles of MFMAs cover the load latency.  The loop is unrolled by two so
+    // that every set and buffer index is a constant.
+    gload(0, 0);
+    swrite(0, 0);
+    if (KTILES > 1) gload(TK, 1);
+    if (KTILES > 2) gload(2 * TK, 0);
+    __syncthreads();
+    auto body = [&](int kt, auto par) {
+        constexpr int P = decltype(par)::value;
+        compute(P, nothing);
+        if (kt + 1 < KTILES) swrite(1 - P, 1 - P);
+        __syncthreads();
+        if (kt + 3 < KTILES) gload((kt + 3) * TK, 1 - P);
+    };
+    for (int kt = 0; kt < KTILES; kt += 2) {
+        body(kt, IntC<0>{});
+        if (kt + 1 < KTILES) body(kt + 1, IntC<1>{});
+    }
 #else
-    gload(0);
-    swrite(0);
+    gload(0, 0);
+    swrite(0, 0);
     __syncthreads();
 #pragma unroll UNROLL
     for (int kt = 0; kt < KTILES; ++kt) {
         // buffer (kt + 1) & 1 was last read in iteration kt - 1, which ended
         // with a barrier, so it may be overwritten during this tile's MFMAs
-        if (kt + 1 < KTILES) gload((kt + 1) * TK);
+        if (kt + 1 < KTILES) gload((kt + 1) * TK, 0);
         const int nxt = (kt + 1) & 1;
         const bool more = kt + 1 < KTILES;
 #if STAGES == 3
         compute(kt & 1, [&] {
-            if (more) swrite(nxt);
+            if (more) swrite(nxt, 0);
         });
 #else
         compute(kt & 1, nothing);
-        if (more) swrite(nxt);
+        if (more) swrite(nxt, 0);
 #endif
         __syncthreads();
     }

@@ -48,7 +48,7 @@ static void add_gemm_block(std::vector<KnobDef> &v, const char *const names[12],
     v.push_back({names[3], "Parallel", {1, 2, 4}, 1});
     v.push_back({names[4], "Parallel", {1, 2, 4}, 1});
     v.push_back({names[5], "TileSize", {16, 32}, 16});          // MFMA instruction shape
-    v.push_back({names[6], "ComputeLocation", {1, 2, 3, 4}, 1});   // LDS staging of the next K tile
+    v.push_back({names[6], "ComputeLocation", {1, 2, 3, 4, 5}, 1});   // LDS staging of the next K tile
     v.push_back({names[7], "Vectorize", {2, 4, 8}, 2});         // bf16 per global load
     v.push_back({names[8], "Unroll", {1, 2}, 1});
     v.push_back({names[9], "Layout", {0, 1}, 0});               // weight stored KxN / NxK
@@ -211,7 +211,9 @@ static std::string check_bf16_block(const rc_op_desc *d, const rc_schedule *s,
         int64_t waves = (int64_t)wm * wn, wgs = (occ * 4 + waves - 1) / waves;
         if (wgs * lds > LDS_LIMIT) return fmt("%s: %lld workgroups of %lld B LDS do not fit a CU", tag, (long long)wgs, (long long)lds);
     }
-    int64_t stage_regs = (st == 2 || st == 3) ? ((int64_t)tm * tk + (int64_t)NB * tn * tk) / (2 * nt) : 0;
+    // register staging: one set of the next tile (stages 2, 3), two (5)
+    int64_t stage_regs = (st == 2 || st == 3 || st == 5) ? ((int64_t)tm * tk + (int64_t)NB * tn * tk) / (2 * nt) : 0;
+    if (st == 5) stage_regs *= 2;
     if (acc + stage_regs > 384)
         return fmt("%s: %lld accumulator + %lld staging registers per lane exceed 384", tag,
                    (long long)acc, (long long)stage_regs);

@@ -98,6 +98,8 @@ SCHEDULES = {
     ],
     "mlp": [
         "",
+        _block("up.", 128, 128, 64, 2, 2, 16, 5, 8, 1, 1, 1) + "," +
+        _block("down.", 128, 64, 64, 2, 2, 32, 5, 8, 1, 1, 0) + ",fuse=1",
         _block("up.", 128, 128, 64, 2, 2, 32, 2, 8, 1, 1, 1) + "," +
         _block("down.", 128, 128, 64, 2, 2, 32, 2, 8, 1, 1, 1) + ",fuse=1",
         _block("up.", 64, 64, 32, 2, 2, 16, 1, 4, 2, 0, 0) + "," +
@@ -115,6 +117,8 @@ SCHEDULES = {
     ],
     "moe": [
         "",
+        _block("up.", 128, 128, 64, 2, 2, 16, 5, 8, 1, 1, 1) + "," +
+        _block("down.", 64, 128, 64, 2, 2, 16, 5, 8, 1, 1, 1) + ",fuse=1",
         _block("up.", 128, 128, 64, 2, 2, 32, 2, 8, 1, 1, 1) + "," +
         _block("down.", 128, 128, 64, 2, 2, 32, 2, 8, 1, 1, 1) + ",fuse=1",
         _block("up.", 64, 64, 32, 2, 2, 16, 1, 4, 1, 0, 0) + "," +
@@ -130,6 +134,7 @@ SCHEDULES = {
     ],
     "conv": [
         "",
+        _block("", 64, 64, 64, 2, 2, 32, 5, 8, 1, 1, 1) + ",fuse=1",
         _block("", 128, 64, 64, 2, 1, 16, 2, 8, 1, 1, 0) + ",fuse=1",
         _block("", 64, 32, 32, 2, 1, 16, 1, 4, 2, 0, 1) + ",fuse=0",
         _block("", 128, 64, 64, 2, 2, 32, 2, 8, 1, 1, 1) + ",fuse=1",
