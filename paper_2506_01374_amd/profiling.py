@@ -9,7 +9,8 @@ of a kernel = its counter reading x (known bytes of a plain copy / the copy
 kernel's reading of the same counter).
 
   python -m paper_2506_01374_amd.profiling stats DIR [--kernel NAME]
-  python -m paper_2506_01374_amd.profiling counter DIR COUNTER KERNEL_SUBSTRING
+  python -m paper_2506_01374_amd.profiling dispatches DIR
+  python -m paper_2506_01374_amd.profiling counter DIR COUNTER KERNEL_SUBSTRING [GRID_THREADS]
   python -m paper_2506_01374_amd.profiling traffic --workload NAME --schedule KEY \
       --kernel SUBSTRING --source FILE --fetch DIR --write DIR --cal-fetch DIR \
       --cal-write DIR --copy-bytes N [--copy-kernel SUBSTRING] [--command CMD ...] \
@@ -46,8 +47,28 @@ def kernel_stats(dirpath: str) -> List[Dict[str, float]]:
     return rows
 
 
-def counter_per_dispatch(dirpath: str, counter: str, kernel_sub: str) -> Dict[str, float]:
-    """Mean value of `counter` per dispatch of kernels whose name contains kernel_sub."""
+def dispatch_stats(dirpath: str) -> List[Dict[str, float]]:
+    """Per (kernel name, grid size in threads) duration statistics from the
+    per-dispatch ``*_kernel_trace.csv`` (two launches of one kernel with
+    different schedules share a name but not a grid)."""
+    groups: Dict[tuple, List[float]] = {}
+    for path in _find(dirpath, "kernel_trace.csv"):
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                g = int(r.get("Grid_Size_X", 0)) * int(r.get("Grid_Size_Y", 1)) * int(r.get("Grid_Size_Z", 1))
+                d = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+                groups.setdefault((r.get("Kernel_Name", ""), g), []).append(d)
+    out = []
+    for (name, g), ds in groups.items():
+        out.append({"name": name, "grid_threads": g, "calls": len(ds), "avg_ns": sum(ds) / len(ds),
+                    "min_ns": min(ds), "max_ns": max(ds)})
+    return sorted(out, key=lambda r: -r["avg_ns"] * r["calls"])
+
+
+def counter_per_dispatch(dirpath: str, counter: str, kernel_sub: str,
+                         grid_threads: int = 0) -> Dict[str, float]:
+    """Mean value of `counter` per dispatch of kernels whose name contains
+    kernel_sub (and, if given, whose grid has grid_threads threads)."""
     vals: Dict[int, float] = {}
     name = None
     for path in _find(dirpath, "counter_collection.csv"):
@@ -55,6 +76,8 @@ def counter_per_dispatch(dirpath: str, counter: str, kernel_sub: str) -> Dict[st
             for r in csv.DictReader(f):
                 kn = r.get("Kernel_Name", "")
                 if kernel_sub not in kn or r.get("Counter_Name") != counter:
+                    continue
+                if grid_threads and int(r.get("Grid_Size", 0)) != grid_threads:
                     continue
                 name = kn
                 d = int(r.get("Dispatch_Id", len(vals)))
@@ -67,10 +90,11 @@ def counter_per_dispatch(dirpath: str, counter: str, kernel_sub: str) -> Dict[st
 
 def traffic_record(schedule: str, kernel_sub: str, source: str, fetch_dir: str, write_dir: str,
                    cal_fetch_dir: str, cal_write_dir: str, copy_bytes: int,
-                   commands: List[str], copy_kernel: str = "copyBuffer") -> Dict[str, object]:
+                   commands: List[str], copy_kernel: str = "copyBuffer",
+                   grid_threads: int = 0) -> Dict[str, object]:
     import hashlib
-    fk = counter_per_dispatch(fetch_dir, "FETCH_SIZE", kernel_sub)
-    wk = counter_per_dispatch(write_dir, "WRITE_SIZE", kernel_sub)
+    fk = counter_per_dispatch(fetch_dir, "FETCH_SIZE", kernel_sub, grid_threads)
+    wk = counter_per_dispatch(write_dir, "WRITE_SIZE", kernel_sub, grid_threads)
     # the calibration runs also fill the source buffer; only the copy counts
     cf = counter_per_dispatch(cal_fetch_dir, "FETCH_SIZE", copy_kernel)
     cw = counter_per_dispatch(cal_write_dir, "WRITE_SIZE", copy_kernel)
@@ -82,7 +106,7 @@ def traffic_record(schedule: str, kernel_sub: str, source: str, fetch_dir: str, 
     wscale = copy_bytes / (cw["mean"] * 1024.0)
     fb = fk["mean"] * 1024.0 * fscale
     wb = wk["mean"] * 1024.0 * wscale
-    return {"key": schedule, "kernel": fk["kernel"],
+    return {"key": schedule, "kernel": fk["kernel"], "grid_threads": grid_threads or None,
             "kernel_source_sha1": hashlib.sha1(open(source, "rb").read()).hexdigest()[:16],
             "fetch_kib_per_dispatch": fk["mean"], "write_kib_per_dispatch": wk["mean"],
             "dispatches": [fk["dispatches"], wk["dispatches"]],
@@ -104,10 +128,12 @@ def main(argv=None):
             ap.add_argument(flag, required=True)
         ap.add_argument("--copy-bytes", type=int, required=True)
         ap.add_argument("--copy-kernel", default="copyBuffer", help="name substring of the copy kernel")
+        ap.add_argument("--grid-threads", type=int, default=0,
+                        help="only dispatches of this many threads (kernels sharing a name)")
         ap.add_argument("--command", action="append", default=[])
         a = ap.parse_args(argv[1:])
         rec = traffic_record(a.schedule, a.kernel, a.source, a.fetch, a.write, a.cal_fetch,
-                             a.cal_write, a.copy_bytes, a.command, a.copy_kernel)
+                             a.cal_write, a.copy_bytes, a.command, a.copy_kernel, a.grid_threads)
         table = json.load(open(a.out)) if os.path.exists(a.out) else {}
         table[a.workload] = rec
         with open(a.out, "w") as f:
@@ -120,8 +146,12 @@ def main(argv=None):
         for r in kernel_stats(argv[1]):
             print(f"{r['name'][:60]:60s} calls={r['calls']:6d} avg={r['avg_ns'] / 1e3:9.3f} us "
                   f"min={r['min_ns'] / 1e3:9.3f} max={r['max_ns'] / 1e3:9.3f} ({r['pct']:.1f}%)")
+    elif argv[:1] == ["dispatches"]:
+        for r in dispatch_stats(argv[1]):
+            print(f"{r['name'][:50]:50s} grid={r['grid_threads']:9d} calls={r['calls']:6d} "
+                  f"avg={r['avg_ns'] / 1e3:9.3f} us min={r['min_ns'] / 1e3:9.3f} max={r['max_ns'] / 1e3:9.3f}")
     elif argv[:1] == ["counter"]:
-        print(counter_per_dispatch(argv[1], argv[2], argv[3]))
+        print(counter_per_dispatch(argv[1], argv[2], argv[3], int(argv[4]) if len(argv) > 4 else 0))
     else:
         print(__doc__)
 
