@@ -452,6 +452,32 @@ void rc_attention(AttnArgs args) {
     // S^T = K Q^T of tile kt (LDS buffer s) for every query block; each K
     // fragment is read once
     auto scores_at = [&](const bf16_t *Ks, accT (&sc)[QB][KB]) {
+#if STAGES >= 4
+        // even and odd k-steps accumulate separately and are added at the
+        // end: dependent MFMA chains half as long
+        accT sc2[QB][KB];
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int r = 0; r < ACCN; ++r) sc[qb][kb][r] = sc2[qb][kb][r] = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+            for (int ks = 0; ks < AD / KSTEP; ++ks) {
+                bf16x8 kf = *(const bf16x8 *)(Ks + kb * MF * AD + koff[ks]);
+#pragma unroll
+                for (int qb = 0; qb < QB; ++qb) {
+                    if (ks & 1) sc2[qb][kb] = mfma(kf, qf[qb][ks], sc2[qb][kb]);
+                    else sc[qb][kb] = mfma(kf, qf[qb][ks], sc[qb][kb]);
+                }
+            }
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) sc[qb][kb] += sc2[qb][kb];
+#else
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
@@ -466,6 +492,7 @@ void rc_attention(AttnArgs args) {
 #pragma unroll
                 for (int qb = 0; qb < QB; ++qb) sc[qb][kb] = mfma(kf, qf[qb][ks], sc[qb][kb]);
             }
+#endif
     };
     auto scores = [&](int s, accT (&sc)[QB][KB]) { scores_at(Kbase + s * KT_ELEMS, sc); };
 
@@ -485,6 +512,26 @@ void rc_attention(AttnArgs args) {
 
     // online softmax of tile kt's scores and O^T += V^T P^T (V^T from buffer s)
     auto softmax_pv_at = [&](int kt, const bf16_t *Vt, accT (&sc)[QB][KB]) {
+#if STAGES >= 4
+        // the tile's V^T fragments (at most 16 x 16 B per lane) are read
+        // before the softmax, which does not need them, so their LDS latency
+        // overlaps the exponentials and reductions
+        typedef short v4i16 __attribute__((ext_vector_type(4)));
+        typedef __attribute__((address_space(3))) v4i16 *lds_v4p;
+        constexpr bool VPRE = (BN / KSTEP) * DB <= 16;
+        bf16x8 vpre[VPRE ? BN / KSTEP : 1][VPRE ? DB : 1];
+        if (VPRE) {
+#pragma unroll
+            for (int j = 0; j < (VPRE ? BN / KSTEP : 1); ++j)
+#pragma unroll
+                for (int db = 0; db < (VPRE ? DB : 1); ++db) {
+                    const bf16_t *const vp = Vt + voff[db] + 32 * j * AD;
+                    const v4i16 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4p)(vp));
+                    const v4i16 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4p)(vp + 16 * AD));
+                    vpre[j][db] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+                }
+        }
+#endif
         // online softmax, one query per lane; m is kept in log2 units and the
         // scale is folded into the exponent's fused multiply-add
 #if CAUSAL
@@ -560,12 +607,15 @@ void rc_attention(AttnArgs args) {
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
 #if STAGES >= 4
-                typedef short v4i16 __attribute__((ext_vector_type(4)));
-                typedef __attribute__((address_space(3))) v4i16 *lds_v4p;
-                const bf16_t *const vp = Vt + voff[db] + 32 * j * AD;
-                const v4i16 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4p)(vp));
-                const v4i16 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4p)(vp + 16 * AD));
-                const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+                bf16x8 vf;
+                if (VPRE) {
+                    vf = vpre[VPRE ? j : 0][VPRE ? db : 0];
+                } else {
+                    const bf16_t *const vp = Vt + voff[db] + 32 * j * AD;
+                    const v4i16 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4p)(vp));
+                    const v4i16 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4p)(vp + 16 * AD));
+                    vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+                }
                 (void)c0;
 #else
                 const int drow = db * MF + lane % MF;
