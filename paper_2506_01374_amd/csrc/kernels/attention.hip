@@ -54,7 +54,8 @@
 #define NTS (64 * NW)
 #define NT (NTS * SPLITS)
 #define NBUF (STAGES > 1 ? 2 : 1)      // register-staged paths
-#define RING (STAGES == 5 ? 4 : 3)     // direct-to-LDS paths
+// direct-to-LDS paths: ring slots per operand (two per split with two splits)
+#define RING (STAGES == 5 || SPLITS == 2 ? 4 : 3)
 #define KB (BN / MF)
 #define DB (AD / MF)
 #define NQT (AS / BM)
@@ -251,20 +252,24 @@ __device__ __forceinline__ void store_out(bf16_t *O, size_t base, int q0w, int l
 extern "C" __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(OCC, 8)))
 void rc_attention(AttnArgs args) {
 #if STAGES >= 4
-    // one LDS object per ring buffer and operand
-    __shared__ __attribute__((aligned(16))) bf16_t K0[KT_ELEMS], K1[KT_ELEMS], K2[KT_ELEMS];
-    __shared__ __attribute__((aligned(16))) bf16_t V0[KT_ELEMS], V1[KT_ELEMS], V2[KT_ELEMS];
+    // ring slots: K tiles in slots 0 .. RING - 1, V tiles after them (one
+    // block, reused for the merge of two splits' states at the end)
+    __shared__ __attribute__((aligned(16))) bf16_t ring[2 * RING][KT_ELEMS];
+    bf16_t *const K0 = ring[0], *const K1 = ring[1], *const K2 = ring[2];
+    bf16_t *const V0 = ring[RING], *const V1 = ring[RING + 1], *const V2 = ring[RING + 2];
 #if RING == 4
-    __shared__ __attribute__((aligned(16))) bf16_t K3[KT_ELEMS], V3[KT_ELEMS];
+    bf16_t *const K3 = ring[3], *const V3 = ring[RING + 3];
 #endif
-    bf16_t *const smem = K0;                 // unused (no register-staged tiles)
+    bf16_t *const smem = ring[0];
 #else
     // one LDS block: per split, NBUF K tiles then NBUF V^T tiles; reused for
     // the merge of the splits' states at the end
     __shared__ __attribute__((aligned(16))) bf16_t smem[LDS_ELEMS];
 #endif
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // wave index made wave-uniform: the row group and split it selects feed
+    // scalar operands (direct-to-LDS addresses) and scalar branches
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int rg = wave % NW, sp = wave / NW, tids = tid % NTS;
     bf16_t *const Kbase = smem + sp * NBUF * (KT_ELEMS + VT_ELEMS);
     bf16_t *const Vbase = Kbase + NBUF * KT_ELEMS;
@@ -309,18 +314,19 @@ void rc_attention(AttnArgs args) {
     // drain every load before each LDS read.  The kernel's own waits below
     // order the ring.  The compiler's waits for its own loads stay correct:
     // extra loads in flight only make a vmcnt(n) wait longer.
+    // Each split's NW waves load that split's tiles.
     constexpr int WL = BN * AD / 512 / NW;            // wave-loads per wave and operand
     unsigned k_src[WL], v_src[WL];                    // byte offsets within a tile
 #pragma unroll
     for (int j = 0; j < WL; ++j) {
-        const int c = (wave * WL + j) * 64 + lane;
+        const int c = (rg * WL + j) * 64 + lane;
         const int row = c / CPR, pc = c % CPR;
         k_src[j] = 2u * (row * AD + ((pc ^ ((row / RPL) % SWZ)) << 3));
         v_src[j] = 2u * (row * AD + ((pc ^ VSWZ(row)) << 3));
     }
     // LDS byte addresses of the ring buffers and this wave's first 1 KiB
     typedef __attribute__((address_space(3))) bf16_t *lds_p;
-    const unsigned wl0 = (unsigned)__builtin_amdgcn_readfirstlane(wave) * WL * 1024u;
+    const unsigned wl0 = (unsigned)__builtin_amdgcn_readfirstlane(rg) * WL * 1024u;
 #if RING == 4
     const unsigned KA[4] = {(unsigned)(size_t)(lds_p)K0 + wl0, (unsigned)(size_t)(lds_p)K1 + wl0,
                             (unsigned)(size_t)(lds_p)K2 + wl0, (unsigned)(size_t)(lds_p)K3 + wl0};
@@ -345,10 +351,15 @@ void rc_attention(AttnArgs args) {
 #pragma unroll
         for (int j = 0; j < WL; ++j) dma(Vg, v_src[j], VA[b] + j * 1024u);
     };
+#if SPLITS == 1
     // the first RING - 1 key tiles are in flight while Q is read
 #pragma unroll
     for (int t = 0; t < RING - 1; ++t)
         if (t < n_kt) gload_lds(t, t);
+#else
+    // split sp's first tile (tile sp) is in flight while Q is read
+    if (sp < n_kt) gload_lds(sp, sp);
+#endif
 #endif
     bf16x8 qf[QB][AD / KSTEP];
 #pragma unroll
@@ -518,7 +529,7 @@ void rc_attention(AttnArgs args) {
         // overlaps the exponentials and reductions
         typedef short v4i16 __attribute__((ext_vector_type(4)));
         typedef __attribute__((address_space(3))) v4i16 *lds_v4p;
-        constexpr bool VPRE = (BN / KSTEP) * DB <= 16;
+        constexpr bool VPRE = SPLITS == 1 && (BN / KSTEP) * DB <= 16;
         bf16x8 vpre[VPRE ? BN / KSTEP : 1][VPRE ? DB : 1];
         if (VPRE) {
 #pragma unroll
@@ -639,7 +650,31 @@ void rc_attention(AttnArgs args) {
     // split sp visits key tiles sp, sp + SPLITS, ...; every wave runs the same
     // number of iterations so the workgroup barriers line up
     const int n_it = (n_kt + SPLITS - 1) / SPLITS;
-#if STAGES == 4
+#if STAGES == 4 && SPLITS == 2
+    (void)compute;
+#define WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | ((((n) >> 4) & 3) << 14) | (7 << 4) | (15 << 8))
+    // Two splits share a ring of four slots: iteration i computes tile 2i
+    // (split 0) and tile 2i + 1 (split 1) from slots 2 (i % 2) + split,
+    // while each split loads its next tile into the other pair of slots.
+    // The pair was last read in iteration i - 1, before the last barrier.
+    auto body = [&](int it, int pair) {
+        const int kt = 2 * it + sp, nk = kt + 2;
+        if (nk < n_kt) gload_lds(nk, 2 - pair + sp);
+        if (kt < n_kt && !skipped(kt)) {
+            accT sc[QB][KB];
+            scores_at(ring[pair + sp], sc);
+            softmax_pv_at(kt, ring[RING + pair + sp], sc);
+        }
+        WAIT_VM(0);                // this wave's share of the next tiles has landed
+        __builtin_amdgcn_s_waitcnt(0xC07F);      // lgkmcnt(0): this wave's LDS reads are done
+        asm volatile("s_barrier" ::: "memory");
+    };
+    for (int it = 0; it < n_it; it += 2) {
+        body(it, 0);
+        if (it + 1 < n_it) body(it + 1, 2);
+    }
+#undef WAIT_VM
+#elif STAGES == 4
     (void)n_it;
     (void)compute;
     // s_waitcnt with only the vector-memory count constrained (expcnt and

@@ -79,6 +79,9 @@ SCHEDULES = {
         "block_m=32,block_n=64,waves=2,mfma=16,stages=5,vec=8,unroll=1,order=0",
         "block_m=64,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=1,order=2,occ=2,chunk=4",
         "block_m=128,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=1,order=1",
+        "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=2,occ=4,splits=2",
+        "block_m=32,block_n=32,waves=2,mfma=16,stages=4,vec=8,unroll=1,order=0,occ=2,splits=2",
+        "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=1,occ=4,splits=2,chunk=4",
     ],
     "attn_full": [
         "",
@@ -89,12 +92,14 @@ SCHEDULES = {
         "block_m=64,block_n=64,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=0",
         "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=0,chunk=4",
         "block_m=64,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=1,order=0",
+        "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=0,occ=4,splits=2",
     ],
     "attn_d64": [
         "block_m=64,block_n=32,waves=2,mfma=32,stages=2,vec=8,unroll=1,order=0",
         "block_m=32,block_n=64,waves=2,mfma=16,stages=1,vec=4,unroll=1,order=1",
         "block_m=32,block_n=32,waves=2,mfma=16,stages=4,vec=8,unroll=1,order=0",
         "block_m=32,block_n=32,waves=2,mfma=16,stages=5,vec=8,unroll=1,order=0",
+        "block_m=32,block_n=32,waves=2,mfma=16,stages=4,vec=8,unroll=1,order=0,splits=2",
     ],
     "mlp": [
         "",
