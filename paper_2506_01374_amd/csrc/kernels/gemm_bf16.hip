@@ -196,7 +196,12 @@ void rc_gemm_bf16(GemmBf16Args args) {
     const bf16_t *arow[A_LOADS];
     bool aval[A_LOADS];
 #if AMODE == 2
-    int a_n[A_LOADS], a_p[A_LOADS], a_q[A_LOADS];
+    // Implicit im2col: per load, the element offset of its output pixel's
+    // input window corner (filter tap (0, 0), which may lie in the padding)
+    // plus its column, and a mask of the filter taps that fall inside the
+    // image; a K tile then only adds the tap's offset (wave-uniform).
+    long long a_off[A_LOADS];
+    unsigned a_mask[A_LOADS];
 #endif
 #pragma unroll
     for (int i = 0; i < A_LOADS; ++i) {
@@ -215,10 +220,16 @@ void rc_gemm_bf16(GemmBf16Args args) {
 #elif AMODE == 3
         arow[i] = args.A + (size_t)(aval[i] ? row_base + r : 0) * GK;
 #else
-        int m = row_base + r;
-        a_n[i] = m / (CV_P * CV_Q);
-        a_p[i] = (m / CV_Q) % CV_P;
-        a_q[i] = m % CV_Q;
+        const int m = row_base + r, c = (v % (TK / VEC)) * VEC;
+        const int n = m / (CV_P * CV_Q), p = (m / CV_Q) % CV_P, q = m % CV_Q;
+        a_off[i] = ((long long)(n * CV_H + p - CV_PAD) * CV_W + (q - CV_PAD)) * CV_C + c;
+        unsigned mask = 0;
+#pragma unroll
+        for (int tap = 0; tap < GK / CV_C; ++tap) {
+            const int ih = p + tap / CV_S - CV_PAD, iw = q + tap % CV_S - CV_PAD;
+            if (ih >= 0 && ih < CV_H && iw >= 0 && iw < CV_W) mask |= 1u << tap;
+        }
+        a_mask[i] = mask;
         arow[i] = args.A;
 #endif
     }
@@ -244,12 +255,12 @@ void rc_gemm_bf16(GemmBf16Args args) {
             int v = tid + i * NT;
             int c = (v % (TK / VEC)) * VEC;
 #if AMODE == 2
-            // K index k0 + c lies in filter tap (r, s) = divmod(k0 / C, S).
-            int tap = k0 / CV_C, ch = k0 % CV_C + c;
-            int ih = a_p[i] + tap / CV_S - CV_PAD, iw = a_q[i] + tap % CV_S - CV_PAD;
-            bool ok = aval[i] && ih >= 0 && ih < CV_H && iw >= 0 && iw < CV_W;
-            const bf16_t *src = args.A + (((size_t)a_n[i] * CV_H + (ok ? ih : 0)) * CV_W + (ok ? iw : 0)) * CV_C + ch;
-            ra[set][i] = ok ? *(const vecT *)src : (vecT)0;
+            // K tile k0 lies in filter tap (r, s) = divmod(k0 / C, S), channels
+            // k0 % C ..; the offsets below are the same for the whole wave.
+            (void)c;
+            const int tap = k0 / CV_C;
+            const long long tap_off = ((long long)(tap / CV_S) * CV_W + tap % CV_S) * CV_C + (k0 - tap * CV_C);
+            ra[set][i] = ((a_mask[i] >> tap) & 1u) ? *(const vecT *)(args.A + (a_off[i] + tap_off)) : (vecT)0;
 #else
             ra[set][i] = aval[i] ? *(const vecT *)(arow[i] + k0 + c) : (vecT)0;
 #endif

@@ -333,6 +333,7 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
             if (P <= 0 || Q <= 0) return "empty output";
             int tk = kv(d, s, "tile_k");
             if (C % tk) return fmt("tile_k %d does not divide C = %lld (a K tile must stay in one filter tap)", tk, (long long)C);
+            if (R * S > 32) return fmt("%lld filter taps exceed the 32-bit tap mask", (long long)(R * S));
             return check_bf16_block(d, s, PLAIN, N * P * Q, K, R * S * C, 1, "conv", true);
         }
     }
