@@ -142,14 +142,57 @@ class TableEvaluator:
         return self.table.get(str(sched), {"schedule": str(sched), "valid": False, "error": "not in table"})
 
 
+class FeedbackProposer:
+    """Expansion proposals from measured history (Sec. 3.1's proposal step,
+    with the language model replaced by a plain rule): take the `top`
+    best schedules measured so far, find each knob's most common value among
+    them, and propose setting one knob (chosen at random among those where
+    the node disagrees with that consensus) to its consensus value.  Before
+    `warm` valid samples exist, or when the node already agrees everywhere,
+    it proposes nothing and the search expands with a random legal
+    transformation."""
+
+    def __init__(self, op: rc.Op, seed: int, top: int = 8, warm: int = 8):
+        import random
+        self.op, self.top, self.warm = op, top, warm
+        self.rng = random.Random(seed)
+        self.names = op.knob_names()
+        self.classes = [op.knob_class(i) for i in range(len(self.names))]
+        self.seen: List[tuple] = []          # (reward, {knob: value})
+
+    def record(self, sched: rc.Schedule, reward: Optional[float]):
+        if reward is not None:
+            self.seen.append((reward, sched.as_dict()))
+
+    def __call__(self, at: rc.Schedule, parent, grandparent) -> str:
+        if len(self.seen) < self.warm:
+            return ""
+        best = sorted(self.seen, key=lambda t: -t[0])[: self.top]
+        cur = at.as_dict()
+        moves = []
+        for i, name in enumerate(self.names):
+            counts: Dict[int, int] = {}
+            for _, d in best:
+                counts[d[name]] = counts.get(d[name], 0) + 1
+            value = max(counts, key=lambda v: (counts[v], -abs(v - cur[name])))
+            if value != cur[name]:
+                moves.append(f"{self.classes[i]}({name}={value})")
+        return self.rng.choice(moves) if moves else ""
+
+
 def run_search(op, evaluator, policy: str, budget: int, seed: int, horizon=12, branching=2,
-               c=math.sqrt(2.0)):
+               c=math.sqrt(2.0), proposer: Optional[str] = None):
+    prop = FeedbackProposer(op, seed) if proposer == "feedback" else None
+
     def ev(s):
         r = evaluator.measure(s)
-        return r["reward"] if r.get("valid") else None
+        reward = r["reward"] if r.get("valid") else None
+        if prop is not None:
+            prop.record(s, reward)
+        return reward
 
     srch = rc.Search(op, ev, policy=POLICIES[policy], budget=budget, horizon=horizon,
-                     branching=branching, c=c, seed=seed)
+                     branching=branching, c=c, seed=seed, propose=prop)
     srch.run()
     hist = srch.history()
     try:
@@ -160,7 +203,8 @@ def run_search(op, evaluator, policy: str, budget: int, seed: int, horizon=12, b
     curve = [h["best_so_far"] for h in hist if h["valid"]]
     # samples to reach the run's best (within 1%)
     to_best = next((i + 1 for i, v in enumerate(curve) if v >= 0.99 * reward), None) if curve else None
-    return {"policy": policy, "seed": seed, "budget": budget, "valid": sum(h["valid"] for h in hist),
+    return {"policy": policy, "proposer": proposer, "fallbacks": srch.fallbacks() if prop else None,
+            "seed": seed, "budget": budget, "valid": sum(h["valid"] for h in hist),
             "invalid": sum(not h["valid"] for h in hist), "best": best_text, "best_reward": reward,
             "best_index": idx, "samples_to_best": to_best, "curve": curve}
 
@@ -185,6 +229,8 @@ def main(argv=None):
     ap.add_argument("--horizon", type=int, default=12)
     ap.add_argument("--branching", type=int, default=2)
     ap.add_argument("--c", type=float, default=math.sqrt(2.0))
+    ap.add_argument("--proposer", default=None, choices=["feedback"],
+                    help="expansion proposals from measured history (default: random legal)")
     ap.add_argument("--repeat", type=int, default=10)
     ap.add_argument("--out", default="tune_out")
     ap.add_argument("--enumerate", action="store_true", help="list the whole legal space")
@@ -218,7 +264,8 @@ def main(argv=None):
                       f"{time.time() - t0:.0f}s", flush=True)
         return
 
-    log = open(os.path.join(args.out, f"{args.workload}.{args.policy}.jsonl"), "a")
+    tag = args.policy + (f"+{args.proposer}" if args.proposer else "")
+    log = open(os.path.join(args.out, f"{args.workload}.{tag}.jsonl"), "a")
     if args.replay:
         evaluator = TableEvaluator(args.replay)
     else:
@@ -239,7 +286,8 @@ def main(argv=None):
 
     for seed in _parse_seeds(args.seeds):
         t0 = time.time()
-        res = run_search(op, evaluator, args.policy, args.budget, seed, args.horizon, args.branching, args.c)
+        res = run_search(op, evaluator, args.policy, args.budget, seed, args.horizon, args.branching, args.c,
+                         args.proposer)
         res.update(workload=args.workload, kind="search", wall_s=time.time() - t0)
         log.write(json.dumps(res) + "\n")
         log.flush()

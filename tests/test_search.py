@@ -184,3 +184,54 @@ def test_report_helpers():
     assert report.samples_to_reach([1, 3, 3, 5, 5], 4) == 4
     assert report.samples_to_reach([1, 2], 4) is None
     assert report.mean_curve([[1, 2, 3], [3, 4]]) == [2, 3]
+
+
+def test_feedback_proposer_moves_toward_the_best_measured_schedules():
+    # Before `warm` samples it proposes nothing (the search falls back to a
+    # random legal transformation); afterwards it proposes one knob set to
+    # the value most common among the best measured schedules, as text that
+    # the proposal parser accepts.
+    from paper_2506_01374_amd.tune import FeedbackProposer, legal_space
+    op = rc.Op(rc.RC_OP_GEMM_F32, (128, 128, 128))
+    space = legal_space(op)
+    prop = FeedbackProposer(op, seed=0, top=4, warm=4)
+    at = op.default()
+    assert prop(at, None, None) == ""
+    good = [s for s in space if s["tile_m"] == 64 and s["vec"] == 4][:4]
+    bad = [s for s in space if s["tile_m"] == 16][:4]
+    for s in good:
+        prop.record(s, 1.0)
+    for s in bad:
+        prop.record(s, 0.1)
+    prop.record(space[0], None)                   # invalid samples are ignored
+    seen = set()
+    for _ in range(50):
+        text = prop(at, None, None)
+        assert text
+        op.parse(text)                            # a valid proposal for this operator
+        seen.add(text)
+    assert any("tile_m=64" in t for t in seen) and any("vec=4" in t for t in seen)
+    # with a single best schedule, that schedule is the consensus: a node
+    # equal to it gets no proposal
+    solo = FeedbackProposer(op, seed=0, top=1, warm=1)
+    solo.record(good[0], 1.0)
+    assert solo(good[0], None, None) == ""
+
+
+def test_uct_with_feedback_proposer_runs_and_uses_proposals():
+    from paper_2506_01374_amd.tune import FeedbackProposer
+    op = rc.Op(rc.RC_OP_GEMM_F32, (128, 128, 128))
+    prop = FeedbackProposer(op, seed=1)
+
+    def ev(s):
+        r = synthetic_reward(s)
+        prop.record(s, r)
+        return r
+
+    s = rc.Search(op, ev, policy=rc.RC_POLICY_UCT, budget=200, seed=1, propose=prop).run()
+    hist = s.history()
+    assert sum(h["valid"] for h in hist) == 200
+    # some expansions came from proposals (not every one fell back)
+    assert s.fallbacks() < 200
+    _, r, _ = s.best()
+    assert r > 0
