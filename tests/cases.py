@@ -154,6 +154,28 @@ def small_op(key):
     return rc.Op(kind, dims, flags)
 
 
+# Full-size workloads in schedules that take the other code paths (pipelined
+# and split direct-to-LDS attention, chunked work items, two-set register
+# prefetch and direct-to-LDS GEMM staging), sampled outputs.
+FULL_ALT = [
+    ("attention_causal_b1_h32_s1024_d128",
+     "block_m=64,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=2,order=2,occ=2"),
+    ("attention_causal_b1_h32_s1024_d128",
+     "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=1,occ=4,splits=2"),
+    ("attention_causal_b1_h32_s1024_d128",
+     "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=2,occ=2,chunk=16"),
+    ("gated_mlp_t2048_h4096_i14336",
+     _block("up.", 128, 128, 64, 2, 2, 16, 5, 8, 1, 1, 1) + "," +
+     _block("down.", 128, 256, 64, 2, 4, 16, 4, 8, 1, 1, 1) + ",fuse=1"),
+    ("moe_t4096_h2048_e64_i1408_top6",
+     _block("up.", 128, 128, 64, 2, 2, 16, 5, 8, 1, 1, 1) + "," +
+     _block("down.", 128, 128, 64, 2, 2, 16, 3, 8, 1, 1, 0) + ",fuse=1"),
+    ("conv3x3_n2_64x64_c320_k320",
+     _block("", 64, 64, 64, 4, 2, 16, 2, 8, 1, 1, 1) + ",fuse=1"),
+]
+
+
+
 def all_compile_jobs():
     """(op, [schedules]) pairs for ahead-of-time compilation."""
     jobs = []
@@ -163,4 +185,7 @@ def all_compile_jobs():
     for name, s in TUNED.items():
         op = W.workload_op(name)
         jobs.append((op, [op.from_string(s), op.default()]))
+    for name, s in FULL_ALT:
+        op = W.workload_op(name)
+        jobs.append((op, [op.from_string(s)]))
     return jobs

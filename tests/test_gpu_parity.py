@@ -192,6 +192,19 @@ def test_full_size_sampled(name, which):
     assert np.all(np.isfinite(y))
 
 
+@pytest.mark.parametrize("name,sched_text", cases.FULL_ALT,
+                         ids=[f"{n.split('_')[0]}-{i}" for i, (n, _) in enumerate(cases.FULL_ALT)])
+def test_full_size_alternative_paths(name, sched_text):
+    op = W.workload_op(name)
+    sched = op.from_string(sched_text)
+    assert sched.validate() == "", sched.validate()
+    host = W.host_inputs(op, seed=0)
+    y, _ = run(op, sched, host)
+    n = {rc.RC_OP_ATTENTION: 96, rc.RC_OP_GATED_MLP: 12, rc.RC_OP_MOE: 12, rc.RC_OP_CONV2D: 64}[op.kind]
+    assert_parity(op, y, host, rows=_sample_rows(op, n, seed=7), label=f"{name} {sched_text}")
+    assert np.all(np.isfinite(y))
+
+
 @pytest.mark.parametrize("key", ["attn_causal", "mlp", "moe"])
 def test_graph_replay_matches_eager(key):
     # The benchmark replays captured launches.  Capture one execution on a
