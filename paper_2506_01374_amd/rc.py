@@ -233,6 +233,13 @@ class Op:
     def peak_flops(self) -> float:
         return lib().rc_peak_flops(self.ref)
 
+    def bound(self) -> str:
+        """The roofline that binds: "hbm" when the algorithmic intensity
+        (FLOPs per compulsory HBM byte) is below the ridge point peak FLOP/s
+        / peak bytes/s of the operator's MFMA type, else "mfma"."""
+        ridge = self.peak_flops() / lib().rc_peak_bytes_per_s()
+        return "hbm" if self.flops() / self.bytes() < ridge else "mfma"
+
     def knob_names(self) -> List[str]:
         return [lib().rc_knob_name(self.ref, i).decode() for i in range(lib().rc_knob_count(self.ref))]
 

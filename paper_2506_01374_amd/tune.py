@@ -39,12 +39,12 @@ from . import workloads as W
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 POLICIES = {"random": rc.RC_POLICY_RANDOM, "uct": rc.RC_POLICY_UCT, "exhaustive": rc.RC_POLICY_EXHAUSTIVE}
-HBM_BOUND = {rc.RC_OP_ATTENTION}
 
 
 def reward_of(op: rc.Op, ms: float) -> float:
+    """Fraction of the binding roofline reached (HBM or MFMA, by intensity)."""
     sec = ms * 1e-3
-    if op.kind in HBM_BOUND:
+    if op.bound() == "hbm":
         return op.bytes() / sec / rc.lib().rc_peak_bytes_per_s()
     return op.flops() / sec / op.peak_flops()
 

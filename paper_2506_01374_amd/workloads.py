@@ -5,9 +5,11 @@ Shapes: fp32 GEMM 128^3 (the contraction of the App. A example module,
 scaled down); Llama-3-8B-style causal attention 1 x 32 heads x 1024 x 128;
 Llama-4-Scout-style gated MLP 2048 x 4096 x 14336; DeepSeek-style MoE with
 4096 tokens, hidden 2048, 64 experts of intermediate 1408, top-6; FLUX-style
-3x3 convolution 2 x 64 x 64 x 320 -> 320 (Sec. 4.1 names the layers; it
-prints no shapes, so these are chosen stand-ins).  All inputs are synthetic
-and seeded (see ``inputs``).
+3x3 convolution 2 x 64 x 64 x 320 -> 320; FLUX-style bidirectional (no
+mask) self-attention 1 x 24 heads x 4096 x 128, the image tokens of a
+1024 x 1024 image (Sec. 4.1 names the layers; it prints no shapes, so these
+are chosen stand-ins).  All inputs are synthetic and seeded (see
+``inputs``).
 """
 from __future__ import annotations
 
@@ -24,6 +26,7 @@ WORKLOADS: Dict[str, Tuple[int, Tuple[int, ...], int]] = {
     "gated_mlp_t2048_h4096_i14336": (rc.RC_OP_GATED_MLP, (2048, 4096, 14336), 0),
     "moe_t4096_h2048_e64_i1408_top6": (rc.RC_OP_MOE, (4096, 2048, 64, 1408, 6), 0),
     "conv3x3_n2_64x64_c320_k320": (rc.RC_OP_CONV2D, (2, 64, 64, 320, 320, 3, 3, 1), 0),
+    "attention_noncausal_b1_h24_s4096_d128": (rc.RC_OP_ATTENTION, (1, 24, 4096, 128), 0),
 }
 
 

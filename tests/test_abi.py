@@ -64,6 +64,9 @@ def test_flops_and_bytes_model():
     assert e.flops() == 6 * 4096 * 6 * 2048 * 1408 == 425_201_762_304
     c = W.workload_op("conv3x3_n2_64x64_c320_k320")
     assert c.flops() == 2 * 8192 * 320 * 2880 == 15_099_494_400
+    f = W.workload_op("attention_noncausal_b1_h24_s4096_d128")
+    assert f.flops() == 4 * 24 * 4096 * 4096 * 128 == 206_158_430_208
+    assert f.bytes() == 4 * 2 * 24 * 4096 * 128
     assert g.peak_flops() == 157.3e12 and a.peak_flops() == 2516.6e12
     assert rc.lib().rc_peak_bytes_per_s() == 8.0e12
 

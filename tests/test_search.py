@@ -235,3 +235,27 @@ def test_uct_with_feedback_proposer_runs_and_uses_proposals():
     assert s.fallbacks() < 200
     _, r, _ = s.best()
     assert r > 0
+
+
+@pytest.mark.parametrize("B", [2, 4])
+def test_branching_factor_bounds_children_per_node(B):
+    # B is the most children a node gets (Sec. 3.2; the branching ablation
+    # compares B = 2 and B = 4): the root is expanded until it has B
+    # children, after which iterations only select among them.
+    op = rc.Op(rc.RC_OP_GEMM_F32, (128, 128, 128))
+    moves = ["TileSize(tile_m=32)", "TileSize(tile_n=32)", "Unroll(unroll=2)", "Layout(layout=1)"]
+    evals = []
+
+    def ev(s):
+        evals.append(str(s))
+        return 0.5
+
+    s = rc.Search(op, ev, policy=rc.RC_POLICY_UCT, budget=100, horizon=1, branching=B, seed=0,
+                  propose=lambda at, par, gpar: ";".join(moves))
+    for _ in range(8):
+        s.step()
+    visits = [s.node_stats([op.parse(m)])[0] for m in moves]
+    assert all(v > 0 for v in visits[:B]) and all(v == 0 for v in visits[B:])
+    assert sum(visits) == 8 and s.node_stats([])[0] == 8
+    assert len(evals) == B and len(set(evals)) == B     # each leaf measured once
+    assert s.fallbacks() == 0
