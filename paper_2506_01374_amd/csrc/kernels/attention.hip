@@ -86,6 +86,7 @@
 #define WSLOT (QB * 2 * MF + QB * DB * ACCN * 64)
 
 typedef unsigned short bf16_t;
+template <int V> struct IntC { static constexpr int value = V; };
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -711,19 +712,222 @@ void rc_attention(AttnArgs args) {
     (void)n_it;
     (void)compute;
 #define WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | ((((n) >> 4) & 3) << 14) | (7 << 4) | (15 << 8))
-    // Software pipeline over a ring of four: iteration kt issues the score
-    // MFMAs of tile kt + 1 ahead of tile kt's softmax, so the matrix unit
-    // works while the exponentials and reductions run, then P V of tile kt.
-    // Tile kt sits in buffer kt % 4; buffer (kt + 3) % 4 held tile kt - 1
+    // Software pipeline over a ring of four K/V tiles.  Iteration kt runs two
+    // phases, each pairing matrix work with vector work that does not depend
+    // on it, so the MFMAs execute while the VALU exponentiates:
+    //   phase 1: S^T of tile kt + 1 (MFMA)  |  exponentials, row sums and
+    //            bf16 packing of tile kt's probabilities (VALU)
+    //   phase 2: O^T += V^T P^T of tile kt (MFMA)  |  row maximum of tile
+    //            kt + 1's scores (VALU)
+    // The order inside each phase is fixed with scheduling-group barriers.
+    // The lazy rescale of tile kt (rare) sits between iterations, the causal
+    // mask (only a wave's last tile crosses its diagonal) between the phases.
+    // Row sums are kept per lane and reduced across lane groups once, after
+    // the loop: every lane of a query applies the same rescale factors.
+    //
+    // Tile kt sits in ring slot kt % 4.  Iteration kt reads K of tile kt + 1
+    // and V of tile kt and fills slot (kt + 3) % 4, which held tile kt - 1
     // (its K was read in iteration kt - 2, its V in kt - 1, both before the
-    // last barrier) and receives tile kt + 3.
+    // last barrier).
+#if CAUSAL
+    // last key tile (relative) holding a key visible to this wave's rows
+    const int nact = max(0, min(n_kt, (q0w + RPW - 1) / BN - kt0 + 1));
+#else
+    const int nact = n_kt;
+#endif
+    constexpr int NKS = AD / KSTEP;            // k-steps of the score product
+    constexpr int NPJ = BN / KSTEP;            // k-steps of the P V product
+    constexpr int MF1 = KB * NKS * QB;         // phase-1 MFMAs
+    constexpr int MF2 = NPJ * DB * QB;         // phase-2 MFMAs
+    constexpr int VALU1 = QB * KB * ACCN * 3 + NPJ * QB * 4;   // phase-1 VALU (approx.)
+    constexpr int V1_PER = (VALU1 + MF1 - 1) / MF1;
+    constexpr int DS1 = KB * NKS + 2 * NPJ * DB;            // phase-1 LDS reads
+    constexpr int DS1_PER = (DS1 - KB * NKS + MF1 - 1) / MF1;
+    typedef short v4i16 __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) v4i16 *lds_v4p;
+    auto needs_mask = [&](int kt) {
+#if CAUSAL
+        return (kt0 + kt) * BN + BN - 1 > q0w;
+#else
+        (void)kt;
+        return false;
+#endif
+    };
+    auto mask = [&](int kt, accT (&sc)[QB][KB]) {
+#if CAUSAL
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+            const int q = q0w + qb * MF + lane % MF;
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int r = 0; r < ACCN; ++r)
+                    if ((kt0 + kt) * BN + kb * MF + key_of(r, lane) > q) sc[qb][kb][r] = -__builtin_inff();
+        }
+#else
+        (void)kt;
+        (void)sc;
+#endif
+    };
+    // row maximum of a tile in log2 units, identical on every lane of a query
+    auto tile_max = [&](const accT (&sc)[QB][KB], float (&mx)[QB]) {
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+            float v = -__builtin_inff();
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int r = 0; r < ACCN; ++r) v = fmaxf(v, sc[qb][kb][r]);
+            mx[qb] = group_max(v) * SCALE_LOG2;
+        }
+    };
+    auto rescale = [&](const float (&mx)[QB]) {
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+            if (__builtin_amdgcn_ballot_w64(mx[qb] > m[qb] + RESCALE_LOG2) != 0) {
+                const float mnew = fmaxf(m[qb], mx[qb]);
+                const float alpha = __builtin_amdgcn_exp2f(m[qb] - mnew);
+                l[qb] *= alpha;
+#pragma unroll
+                for (int db = 0; db < DB; ++db)
+#pragma unroll
+                    for (int r = 0; r < ACCN; ++r) o[qb][db][r] *= alpha;
+                m[qb] = mnew;
+            }
+    };
+    // probabilities of a tile, packed into the P^T fragments of the P V product
+    auto probs = [&](accT (&sc)[QB][KB], bf16x8 (&pf)[NPJ][QB]) {
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+            float ps = l[qb];
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int r = 0; r < ACCN; ++r) {
+                    const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[qb][kb][r], SCALE_LOG2, -m[qb]));
+                    sc[qb][kb][r] = p;
+                    ps += p;
+                }
+            l[qb] = ps;
+        }
+#pragma unroll
+        for (int j = 0; j < NPJ; ++j)
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) {
+                u32x4 pw;
+                pw[0] = pack2(sc[qb][2 * j][0], sc[qb][2 * j][1]);
+                pw[1] = pack2(sc[qb][2 * j][2], sc[qb][2 * j][3]);
+                pw[2] = pack2(sc[qb][2 * j + 1][0], sc[qb][2 * j + 1][1]);
+                pw[3] = pack2(sc[qb][2 * j + 1][2], sc[qb][2 * j + 1][3]);
+                pf[j][qb] = __builtin_bit_cast(bf16x8, pw);
+            }
+    };
+    auto read_k = [&](const bf16_t *Ks, bf16x8 (&kf)[KB][NKS]) {
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+            for (int ks = 0; ks < NKS; ++ks) kf[kb][ks] = *(const bf16x8 *)(Ks + kb * MF * AD + koff[ks]);
+    };
+    auto read_v = [&](const bf16_t *Vt, bf16x8 (&vf)[NPJ][DB]) {
+#pragma unroll
+        for (int j = 0; j < NPJ; ++j)
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                const bf16_t *const vp = Vt + voff[db] + 32 * j * AD;
+                const v4i16 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4p)(vp));
+                const v4i16 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4p)(vp + 16 * AD));
+                vf[j][db] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+            }
+    };
+    auto score_mfmas = [&](const bf16x8 (&kf)[KB][NKS], accT (&sc)[QB][KB]) {
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int r = 0; r < ACCN; ++r) sc[qb][kb][r] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int qb = 0; qb < QB; ++qb) sc[qb][kb] = mfma(kf[kb][ks], qf[qb][ks], sc[qb][kb]);
+    };
+    auto pv_mfmas = [&](const bf16x8 (&vf)[NPJ][DB], const bf16x8 (&pf)[NPJ][QB]) {
+#pragma unroll
+        for (int j = 0; j < NPJ; ++j)
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+                for (int qb = 0; qb < QB; ++qb) o[qb][db] = mfma(vf[j][db], pf[j][qb], o[qb][db]);
+    };
+
     accT sc_a[QB][KB], sc_b[QB][KB];
-    if (!skipped(0)) scores_at(K0, sc_a);
+    float mx[QB];
+    if (nact > 0) {
+        bf16x8 kf[KB][NKS];
+        read_k(K0, kf);
+        score_mfmas(kf, sc_a);
+        if (needs_mask(0)) mask(0, sc_a);
+        tile_max(sc_a, mx);
+    }
+    // Phase 1 as straight-line code (the scheduling groups act within one
+    // basic block); MASKED applies the causal mask to tile kt + 1's scores.
+    auto phase1 = [&](auto masked, int kt, accT (&cur)[QB][KB], accT (&nxt)[QB][KB], const bf16_t *kn,
+                      const bf16_t *vc, bf16x8 (&vf)[NPJ][DB], bf16x8 (&pf)[NPJ][QB]) {
+        bf16x8 kf[KB][NKS];
+        // distinct markers keep the compiler from hoisting the variants'
+        // common code above the branch that selects the variant
+        if (decltype(masked)::value) asm volatile("; pipelined tile, masked successor");
+        else asm volatile("; pipelined tile");
+        read_k(kn, kf);
+        read_v(vc, vf);
+        probs(cur, pf);
+        score_mfmas(kf, nxt);
+        __builtin_amdgcn_sched_group_barrier(0x100, KB * NKS, 0);    // K fragment reads
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+#pragma unroll
+        for (int i = 0; i < MF1; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, V1_PER, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, DS1_PER, 0);
+        }
+        if (decltype(masked)::value) {
+            mask(kt + 1, nxt);
+            // keep the mask inside this variant (not merged into the common
+            // block as selects that every tile would execute)
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+                for (int kb = 0; kb < KB; ++kb) asm volatile("" : "+v"(nxt[qb][kb]));
+        }
+    };
     auto body = [&](int kt, accT (&cur)[QB][KB], accT (&nxt)[QB][KB], const bf16_t *kn,
                     const bf16_t *vc, int fill) {
         if (kt + 3 < n_kt) gload_lds(kt + 3, fill);
-        if (kt + 1 < n_kt && !skipped(kt + 1)) scores_at(kn, nxt);
-        if (!skipped(kt)) softmax_pv_at(kt, vc, cur);
+        if (kt < nact) {
+            rescale(mx);
+            bf16x8 vf[NPJ][DB], pf[NPJ][QB];
+            if (kt + 1 < nact) {
+                if (needs_mask(kt + 1)) phase1(IntC<1>{}, kt, cur, nxt, kn, vc, vf, pf);
+                else phase1(IntC<0>{}, kt, cur, nxt, kn, vc, vf, pf);
+            } else {
+                // the wave's last tile: no successor to overlap with
+                asm volatile("; last tile");
+                read_v(vc, vf);
+                probs(cur, pf);
+            }
+            // phase 2 (one block for every variant, so each output
+            // accumulator has a single MFMA site); after the last tile the
+            // maximum is of stale scores and unused
+            pv_mfmas(vf, pf);
+            tile_max(nxt, mx);
+#pragma unroll
+            for (int i = 0; i < MF2; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+                __builtin_amdgcn_sched_group_barrier(0x002, 2, 1);
+            }
+        }
         if (kt + 3 < n_kt) {
             WAIT_VM(2 * WL);       // tiles up to kt + 2 have landed; kt + 3 may be in flight
         } else {
@@ -738,6 +942,8 @@ void rc_attention(AttnArgs args) {
         if (kt + 2 < n_kt) body(kt + 2, sc_a, sc_b, K3, V2, 1);
         if (kt + 3 < n_kt) body(kt + 3, sc_b, sc_a, K0, V3, 2);
     }
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) l[qb] = group_sum(l[qb]);
 #undef WAIT_VM
 #elif STAGES == 3
     // Software pipeline: iteration i issues the score MFMAs of tile i + 1
