@@ -16,7 +16,12 @@
 //                two K tiles in flight, no register staging (weights stored
 //                [N][K], 16-byte vectors, non-im2col rows); 5: as 2 with two
 //                register sets, each tile's global loads issued two tiles
-//                before its LDS store
+//                before its LDS store; 6: ping-pong - eight waves in two
+//                groups of four, one wave of each group per SIMD; while one
+//                group issues a whole K tile of MFMAs from registers, the
+//                other reads its next K tile's fragments from LDS and issues
+//                the direct-to-LDS loads of a later tile; the groups swap
+//                roles at each barrier (three LDS buffers)
 //   VEC          bf16 elements per global load: 2, 4 or 8 (Vectorize)
 //   UNROLL       unroll factor of the K-tile loop (Unroll)
 //   LAYOUT       weights stored 0: [K][N], 1: [N][K] (Layout)
@@ -139,6 +144,13 @@ void rc_gemm_bf16(GemmBf16Args args) {
     __shared__ __attribute__((aligned(16))) bf16_t Bs0[NB][TN * TK], Bs1[NB][TN * TK], Bs2[NB][TN * TK];
 #define NBUF 2
     bf16_t (*As)[TM * TK] = nullptr;           // unused with the DMA ring
+    bf16_t (*Bs)[NB][TN * TK] = nullptr;
+#elif STAGES == 6
+    // three distinct LDS objects per operand (tile t in buffer t % 3)
+    __shared__ __attribute__((aligned(16))) bf16_t As0[TM * TK], As1[TM * TK], As2[TM * TK];
+    __shared__ __attribute__((aligned(16))) bf16_t Bs0[NB][TN * TK], Bs1[NB][TN * TK], Bs2[NB][TN * TK];
+#define NBUF 2
+    bf16_t (*As)[TM * TK] = nullptr;           // unused with the ping-pong buffers
     bf16_t (*Bs)[NB][TN * TK] = nullptr;
 #else
 #define NBUF (STAGES > 1 ? 2 : 1)
@@ -443,6 +455,187 @@ void rc_gemm_bf16(GemmBf16Args args) {
         if (kt + 2 < KTILES) body(kt + 2, As2, Bs2, As1, Bs1);
     }
 #undef WAIT_VM
+#elif STAGES == 6
+    // Ping-pong.  Waves 0-3 (group 0) and 4-7 (group 1) hold one wave per
+    // SIMD each.  Time is cut into slots separated by workgroup barriers:
+    //   slot 2t:     group 0 computes K tile t from registers;
+    //                group 1 reads tile t's fragments (LDS buffer t % 3)
+    //   slot 2t + 1: group 0 reads tile t + 1's fragments and loads tile
+    //                t + 3 into buffer t % 3 (direct to LDS);
+    //                group 1 computes tile t
+    // so on every SIMD one wave issues MFMAs while the other moves data.
+    // Buffer t % 3 was last read by group 1 in slot 2t, before the barrier
+    // that opens slot 2t + 1; tile t + 3's loads have the slots up to group
+    // 0's read in slot 2t + 5 to land (waited for at the end of slot 2t + 4,
+    // with the next tile's loads still in flight).  Group 0 issues all
+    // direct-to-LDS loads.
+    typedef __attribute__((address_space(3))) void *lds_vp;
+    typedef __attribute__((address_space(1))) void *gbl_vp;
+    constexpr int A_WL = TM * TK / 8 / 64 / 4;       // wave-loads per loading wave, A tile
+    constexpr int B_WL = TN * TK / 8 / 64 / 4;       // per weight operand
+    const int grp = __builtin_amdgcn_readfirstlane(wave >> 2);
+    const int lw = __builtin_amdgcn_readfirstlane(wave & 3);
+    // Source of the 16-byte chunk a lane moves in wave-load W of a tile: row
+    // W * (64 / CPR) + lane / CPR, chunk lc0 ^ 4 x with lc0 = (lane % CPR) ^
+    // (lane / CPR / RPL) and x = W % (CPR / 4) (the row swizzle of load W
+    // differs from load 0 by a wave-uniform XOR).  So a lane needs one byte
+    // offset per distinct x for dense rows; the rest of each address is
+    // wave-uniform and lives in scalar registers.
+    constexpr int NX = CPR / 4;
+    const int r_l = lane / CPR;
+    const int lc0 = (lane % CPR) ^ (r_l / RPL);
+    unsigned voff[NX];
+#pragma unroll
+    for (int x = 0; x < NX; ++x) voff[x] = (unsigned)(r_l * GK * 2 + ((lc0 ^ (4 * x)) << 4));
+#if AMODE != 0
+    // gathered or ragged rows: one offset (from args.A) per load
+    unsigned a_off[A_WL];
+#pragma unroll
+    for (int j = 0; j < A_WL; ++j) {
+        const int row = (lw * A_WL + j) * (64 / CPR) + r_l;
+        const int lc = lc0 ^ (4 * ((lw * A_WL + j) % NX));
+#if AMODE == 1
+        // rows past the group read a valid row; their products are never stored
+        const int tok = args.perm[row_base + (row < rows_valid ? row : 0)] / TOPK;
+        a_off[j] = (unsigned)(tok * GK * 2 + (lc << 4));
+#else
+        a_off[j] = (unsigned)((row_base + (row < rows_valid ? row : 0)) * GK * 2 + (lc << 4));
+#endif
+    }
+#endif
+    auto gload_lds = [&](int k0, bf16_t *la, bf16_t (*lb)[TN * TK]) {
+        // the empty asm keeps each address a scalar base + this lane offset
+        // (no per-load 64-bit address registers hoisted out of the loop)
+        unsigned vo[NX];
+#pragma unroll
+        for (int x = 0; x < NX; ++x) {
+            vo[x] = voff[x];
+            asm volatile("" : "+v"(vo[x]));
+        }
+#if AMODE != 0
+        unsigned ao[A_WL];
+#pragma unroll
+        for (int j = 0; j < A_WL; ++j) {
+            ao[j] = a_off[j];
+            asm volatile("" : "+v"(ao[j]));
+        }
+#endif
+#pragma unroll
+        for (int j = 0; j < A_WL; ++j) {
+            const int W = lw * A_WL + j;
+#if AMODE == 0
+            const char *base = (const char *)(args.A + ((size_t)row_base + W * (64 / CPR)) * GK + k0);
+            __builtin_amdgcn_global_load_lds((gbl_vp)(base + vo[A_WL % NX == 0 ? j % NX : W % NX]), (lds_vp)(la + W * 512), 16, 0, 0);
+#else
+            const char *base = (const char *)(args.A + k0);
+            __builtin_amdgcn_global_load_lds((gbl_vp)(base + ao[j]), (lds_vp)(la + W * 512), 16, 0, 0);
+#endif
+        }
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int j = 0; j < B_WL; ++j) {
+                const int W = lw * B_WL + j;
+                const bf16_t *bb = b == 0 ? B0 :
+#if NB == 2
+                                   B1;
+#else
+                                   B0;
+#endif
+                const char *base = (const char *)(bb + ((size_t)n0 + W * (64 / CPR)) * GK + k0);
+                __builtin_amdgcn_global_load_lds((gbl_vp)(base + vo[B_WL % NX == 0 ? j % NX : W % NX]), (lds_vp)(lb[b] + W * 512), 16, 0, 0);
+            }
+    };
+#define WAIT_VM0() __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (15 << 8))
+#define WAIT_LGKM0() __builtin_amdgcn_s_waitcnt(0xC07F)
+    // barrier without a release fence (which would also wait for in-flight
+    // direct-to-LDS loads); the clobber keeps LDS accesses on their side
+#define SLOT_BARRIER() asm volatile("s_barrier" ::: "memory")
+    Frags fr[TK / KSTEP];
+    // One LDS base address per operand and k-step, computed where it is used
+    // (the empty asm keeps the compiler from hoisting one address register
+    // per fragment out of the loop); fragments are base + immediate offset.
+    typedef __attribute__((address_space(3))) const bf16x8 *lfp;
+    auto read_tile = [&](const bf16_t *la, const bf16_t (*lb)[TN * TK]) {
+#pragma unroll
+        for (int ks = 0; ks < TK / KSTEP; ++ks) {
+            lfp pa = (lfp)(la + wm * WTM * TK + foff[ks]);
+            asm volatile("" : "+v"(pa));
+#pragma unroll
+            for (int i = 0; i < FM; ++i) fr[ks].a[i] = pa[i * MF * TK / 8];
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                lfp pb = (lfp)(lb[b] + wn * WTN * TK + foff[ks]);
+                asm volatile("" : "+v"(pb));
+#pragma unroll
+                for (int j = 0; j < FN; ++j) fr[ks].b[b][j] = pb[j * MF * TK / 8];
+            }
+        }
+        WAIT_LGKM0();
+    };
+    auto compute_tile = [&]() {
+        __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+        for (int ks = 0; ks < TK / KSTEP; ++ks) mfmas(fr[ks]);
+        __builtin_amdgcn_s_setprio(0);
+    };
+    // Both groups run the same loop, "compute tile t; barrier; memory work
+    // for tile t + 1; barrier", group 1 entering it one slot later (after
+    // reading tile 0 while group 0 computes it) and group 0 leaving with one
+    // extra barrier, so the MFMAs have a single site and the accumulators
+    // stay in place.
+    constexpr int LPT = A_WL + NB * B_WL;           // loads per loading wave per tile
+#define WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | ((((n) >> 4) & 3) << 14) | (7 << 4) | (15 << 8))
+    if (grp == 0) {
+        gload_lds(0, As0, Bs0);
+        if (KTILES > 1) gload_lds(TK, As1, Bs1);
+        if (KTILES > 2) gload_lds(2 * TK, As2, Bs2);
+        if (KTILES > 2) {
+            WAIT_VM(LPT);          // tiles 0 and 1 have landed
+        } else {
+            WAIT_VM0();
+        }
+    }
+    SLOT_BARRIER();
+    if (grp == 0) read_tile(As0, Bs0);
+    SLOT_BARRIER();
+    if (grp == 1) {
+        read_tile(As0, Bs0);       // slot 0, while group 0 computes tile 0
+        SLOT_BARRIER();
+    }
+    // tile t sits in buffer cur, t + 1 in nxt; tile t + 3 goes to cur
+    auto step = [&](int t, bf16_t *cur_a, bf16_t (*cur_b)[TN * TK], bf16_t *nxt_a,
+                    bf16_t (*nxt_b)[TN * TK]) {
+        compute_tile();
+        if (grp == 0) {
+            // tile t + 1 has landed (tile t + 2 may still be in flight)
+            if (t + 2 < KTILES) {
+                WAIT_VM(LPT);
+            } else {
+                WAIT_VM0();
+            }
+        }
+        SLOT_BARRIER();
+        if (t + 1 < KTILES) {
+            if (grp == 0) {
+                if (t + 3 < KTILES) gload_lds((t + 3) * TK, cur_a, cur_b);
+                read_tile(nxt_a, nxt_b);
+            } else {
+                read_tile(nxt_a, nxt_b);
+            }
+        }
+        SLOT_BARRIER();
+    };
+    for (int t = 0; t < KTILES; t += 3) {
+        step(t, As0, Bs0, As1, Bs1);
+        if (t + 1 < KTILES) step(t + 1, As1, Bs1, As2, Bs2);
+        if (t + 2 < KTILES) step(t + 2, As2, Bs2, As0, Bs0);
+    }
+    if (grp == 0) SLOT_BARRIER();
+#undef WAIT_VM
+#undef WAIT_VM0
+#undef WAIT_LGKM0
+#undef SLOT_BARRIER
 #elif STAGES == 1
 #pragma unroll UNROLL
     for (int kt = 0; kt < KTILES; ++kt) {

@@ -48,7 +48,7 @@ static void add_gemm_block(std::vector<KnobDef> &v, const char *const names[12],
     v.push_back({names[3], "Parallel", {1, 2, 4}, 1});
     v.push_back({names[4], "Parallel", {1, 2, 4}, 1});
     v.push_back({names[5], "TileSize", {16, 32}, 16});          // MFMA instruction shape
-    v.push_back({names[6], "ComputeLocation", {1, 2, 3, 4, 5}, 1});   // LDS staging of the next K tile
+    v.push_back({names[6], "ComputeLocation", {1, 2, 3, 4, 5, 6}, 1});   // LDS staging of the next K tile
     v.push_back({names[7], "Vectorize", {2, 4, 8}, 2});         // bf16 per global load
     v.push_back({names[8], "Unroll", {1, 2}, 1});
     v.push_back({names[9], "Layout", {0, 1}, 0});               // weight stored KxN / NxK
@@ -198,7 +198,28 @@ static std::string check_bf16_block(const rc_op_desc *d, const rc_schedule *s,
         if (((int64_t)tn * tk / 512) % (wm * wn) || tn * tk < 512 * wm * wn)
             return fmt("%s: B tile is not a whole number of 1 KiB wave-loads per wave", tag);
     }
-    int64_t lds = (int64_t)(st == 4 ? 3 : st > 1 ? 2 : 1) * ((int64_t)tm * tk + (int64_t)NB * tn * tk) * 2;
+    if (st == 6) {
+        // ping-pong: two groups of four waves, one wave of each per SIMD;
+        // group 0 moves whole tiles direct to LDS, every wave holds a whole
+        // K tile of fragments in registers
+        if (wm * wn != 8) return fmt("%s: ping-pong staging needs 8 waves (has %d)", tag, wm * wn);
+        if (lay != 1) return fmt("%s: ping-pong staging needs weights stored N x K", tag);
+        if (vec != 8) return fmt("%s: ping-pong staging moves 16-byte vectors (vec 8)", tag);
+        if (im2col) return fmt("%s: ping-pong staging cannot zero-fill padded im2col rows", tag);
+        if (((int64_t)tm * tk / 512) % 4 || tm * tk < 512 * 4)
+            return fmt("%s: A tile is not a whole number of 1 KiB wave-loads per loading wave", tag);
+        if (((int64_t)tn * tk / 512) % 4 || tn * tk < 512 * 4)
+            return fmt("%s: B tile is not a whole number of 1 KiB wave-loads per loading wave", tag);
+        if (((int64_t)tm * tk + (int64_t)NB * tn * tk) / 512 / 4 > 62)
+            return fmt("%s: loads per loading wave per K tile exceed the 6-bit vector-memory counter", tag);
+        if (kv(d, s, names[11]) != 2) return fmt("%s: ping-pong staging runs two waves per SIMD (occ 2)", tag);
+        int64_t frag = (int64_t)(tm / wm / mf + NB * (tn / wn / mf)) * (tk / (mf == 16 ? 32 : 16)) * 4;
+        int64_t accr = (int64_t)NB * tm * tn / nt;
+        if (accr + frag > 224)
+            return fmt("%s: %lld accumulator + %lld fragment registers per lane exceed 224", tag,
+                       (long long)accr, (long long)frag);
+    }
+    int64_t lds = (int64_t)(st == 4 || st == 6 ? 3 : st > 1 ? 2 : 1) * ((int64_t)tm * tk + (int64_t)NB * tn * tk) * 2;
     if (lds > LDS_LIMIT)
         return fmt("%s: LDS %lld B exceeds %lld B", tag, (long long)lds, (long long)LDS_LIMIT);
     int64_t acc = (int64_t)NB * tm * tn / nt;

@@ -18,6 +18,8 @@ SMALL = {
     "attn_full": (rc.RC_OP_ATTENTION, (1, 2, 256, 128), 0),
     "attn_d64": (rc.RC_OP_ATTENTION, (2, 1, 128, 64), rc.RC_FLAG_CAUSAL),
     "mlp": (rc.RC_OP_GATED_MLP, (256, 256, 512), 0),
+    # odd numbers of K tiles (3 for gate/up, 5 for down) for the ping-pong loop
+    "mlp_odd": (rc.RC_OP_GATED_MLP, (256, 192, 320), 0),
     "moe": (rc.RC_OP_MOE, (256, 256, 8, 128, 2), 0),
     "conv": (rc.RC_OP_CONV2D, (2, 16, 12, 64, 64, 3, 3, 1), 0),
 }
@@ -119,6 +121,17 @@ SCHEDULES = {
         _block("down.", 128, 128, 64, 2, 2, 16, 4, 8, 1, 1, 1) + ",fuse=1",
         _block("up.", 64, 128, 32, 2, 2, 32, 4, 8, 1, 1, 0) + "," +
         _block("down.", 256, 64, 32, 4, 1, 16, 4, 8, 1, 1, 0) + ",fuse=0",
+        # ping-pong staging
+        _block("up.", 256, 128, 32, 4, 2, 32, 6, 8, 1, 1, 1, 2) + "," +
+        _block("down.", 128, 256, 64, 2, 4, 32, 6, 8, 1, 1, 1, 2) + ",fuse=1",
+        _block("up.", 128, 128, 32, 4, 2, 16, 6, 8, 1, 1, 0, 2) + "," +
+        _block("down.", 256, 128, 32, 4, 2, 16, 6, 8, 1, 1, 0, 2) + ",fuse=0",
+    ],
+    "mlp_odd": [
+        _block("up.", 256, 64, 64, 4, 2, 16, 6, 8, 1, 1, 1, 2) + "," +
+        _block("down.", 256, 64, 64, 4, 2, 16, 6, 8, 1, 1, 1, 2) + ",fuse=1",
+        _block("up.", 256, 64, 64, 4, 2, 32, 6, 8, 1, 1, 0, 2) + "," +
+        _block("down.", 128, 64, 64, 4, 2, 16, 6, 8, 1, 1, 0, 2) + ",fuse=1",
     ],
     "moe": [
         "",
@@ -136,6 +149,11 @@ SCHEDULES = {
         _block("down.", 128, 128, 64, 2, 2, 16, 4, 8, 1, 1, 1) + ",fuse=1",
         _block("up.", 32, 128, 64, 1, 2, 16, 4, 8, 1, 1, 0) + "," +
         _block("down.", 64, 64, 64, 2, 1, 32, 4, 8, 1, 1, 0) + ",fuse=0",
+        # ping-pong staging over gathered (gate/up) and grouped (down) rows
+        _block("up.", 128, 128, 64, 4, 2, 16, 6, 8, 1, 1, 1, 2) + "," +
+        _block("down.", 128, 256, 64, 2, 4, 16, 6, 8, 1, 1, 1, 2) + ",fuse=1",
+        _block("up.", 128, 128, 32, 2, 4, 16, 6, 8, 1, 1, 0, 2) + "," +
+        _block("down.", 128, 128, 32, 4, 2, 32, 6, 8, 1, 1, 0, 2) + ",fuse=0",
     ],
     "conv": [
         "",
