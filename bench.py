@@ -34,7 +34,7 @@ METRIC = "best-schedule TFLOP/s and % of MFMA peak per operator; samples to reac
 DEFAULT_WORKLOAD = "attention_causal_b1_h32_s1024_d128"
 HBM_PEAK_GBS = 8000.0
 
-DTYPE = {"gemm_f32_128": "f32"}   # the others compute in bf16 (fp32 accumulation)
+DTYPE = {"gemm_f32_128": "f32", "gemm_f32_m16_n2048_k7168": "f32"}   # the others: bf16 (fp32 accumulation)
 
 
 def _oracle_baseline(name, op, host, budget_s):
@@ -128,6 +128,9 @@ def main():
     ap.add_argument("--eager", action="store_true",
                     help="launch each step from the host instead of replaying a captured HIP graph")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle work")
+    ap.add_argument("--rotate", type=int, default=1, metavar="R",
+                    help="cycle the steps through R copies of the inputs (R x the working set "
+                         "above the 256 MB MALL measures HBM rather than cache bandwidth)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES, --steps times "
                          "(the reference reading for HBM traffic counters)")
@@ -162,7 +165,8 @@ def main():
     tuned = json.load(open(os.path.join(ROOT, "paper_2506_01374_amd", "tuned.json")))
     sched = op.from_string(args.schedule if args.schedule else tuned[name])
     host = W.host_inputs(op, seed=0)
-    dev = W.to_device(W.stored_inputs(op, sched, host))
+    R = max(1, args.rotate)
+    devs = [W.to_device(W.stored_inputs(op, sched, host)) for _ in range(R)]
     out = W.empty_output(op)
     plan = rc.Plan(op, sched)
     ws = plan.workspace()
@@ -179,24 +183,24 @@ def main():
     stream = torch.cuda.Stream()
     ev_region = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     with torch.cuda.stream(stream):
-        prep = plan.prepare(dev, out, ws, stream)
-        for _ in range(args.warmup):
-            prep.launch()
+        preps = [plan.prepare(d, out, ws, stream) for d in devs]
+        for i in range(args.warmup):
+            preps[i % R].launch()
         # eager pass: per-kernel events (also the whole measurement with --eager)
         n_eager = K if args.eager else min(K, 20)
         eager_ev = [[torch.cuda.Event(enable_timing=True) for _ in range(nk + 1)] for _ in range(n_eager)]
         for row in eager_ev:        # torch creates an event on its first record
             for e in row:
                 e.record(stream)
-        ev_arrays = [prep.events(row) for row in eager_ev]
+        ev_arrays = [preps[i % R].events(row) for i, row in enumerate(eager_ev)]
     torch.cuda.synchronize()
     graph = None
     if not args.eager:
         try:
             graph = torch.cuda.CUDAGraph()
             with torch.cuda.graph(graph, stream=stream):
-                for _ in range(K):
-                    prep.launch()
+                for i in range(K):
+                    preps[i % R].launch()
             torch.cuda.synchronize()
             graph.replay()              # warm replay
             torch.cuda.synchronize()
@@ -211,7 +215,7 @@ def main():
             graph.replay()
         else:
             for i in range(K):
-                prep.launch_timed(ev_arrays[i % len(ev_arrays)])
+                preps[i % R].launch_timed(ev_arrays[i % len(ev_arrays)])
         ev_region[1].record(stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
@@ -219,7 +223,7 @@ def main():
     if graph is not None:
         with torch.cuda.stream(stream):
             for i in range(len(ev_arrays)):
-                prep.launch_timed(ev_arrays[i])
+                preps[i % R].launch_timed(ev_arrays[i])
         torch.cuda.synchronize()
     ms_per_step = elapsed * 1e3 / K
     flops = op.flops()
@@ -266,6 +270,7 @@ def main():
         "config": {"workload": name, "dims": list(op.dims), "flags": op.flags,
                    "schedule": str(sched), "parallelism": "single GPU",
                    "launch": "hip_graph" if graph is not None else "eager",
+                   "input_copies": R,
                    "frac_of_mfma_peak": value * 1e12 / op.peak_flops()},
         "roofline": roof, "cpu_baseline": cpu,
     }

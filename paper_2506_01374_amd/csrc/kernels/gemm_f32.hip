@@ -6,7 +6,16 @@
 //   WM WN        waves per workgroup along M and N (Parallel)
 //   VEC          fp32 elements per global load (Vectorize)
 //   STAGES       1: load-store-compute; 2: LDS double buffer with register
-//                prefetch of the next K tile (ComputeLocation)
+//                prefetch of the next K tile (ComputeLocation); 3: streaming
+//                for decode-shaped operators (M <= 16 rows, one MFMA row
+//                block): no LDS staging, each wave streams its own slice of
+//                the K range straight from memory into MFMA operands with
+//                the loads of the next 2 x UNROLL - 1 batches of TK rows in
+//                flight (Unroll sets the prefetch depth), the waves' partial sums
+//                are added in LDS, and with SPLITS > 1 the workgroups of one
+//                column tile split K further and rc_gemm_f32_splitk_reduce
+//                adds their partials (in a fixed order)
+//   SPLITS       K splits across workgroups (Parallel; STAGES 3 only)
 //   UNROLL       unroll factor of the K-tile loop (Unroll)
 //   LAYOUT       0: B stored [K][N]; 1: B stored [N][K] (Layout)
 //   GM GN GK     problem size; every tile is perfect (checked on the host).
@@ -36,6 +45,7 @@ struct GemmF32Args {
     const float *A;
     const float *B;
     float *C;
+    float *P;          // per-split partial sums [SPLITS][GM][GN] (STAGES 3, SPLITS > 1)
 };
 
 __device__ __forceinline__ float vget(const vecT &v, int j) {
@@ -47,6 +57,128 @@ __device__ __forceinline__ float vget(const vecT &v, int j) {
 #endif
 }
 
+#if STAGES == 3
+// Streaming variant.  Workgroup (nt, s) owns columns nt * 64 .. + 63 and the
+// s-th of SPLITS equal K ranges; wave w of its NT / 64 waves takes the w-th
+// slice of that range, KW rows, in batches of TK rows.
+//
+// Lane layout of one 16-row block kb .. kb + 15 (k-step e = 0..3 contracts
+// the rows kb + 4 q + e, q = lane / 16 being the MFMA's k slot, so that A
+// and B agree on which row each slot holds):
+//   A: one 16-byte load per lane, A[lane % 16][kb + 4 q .. + 3]; element e
+//      is the lane's A operand of k-step e (rows >= GM read as zero)
+//   B: for each e one 16-byte load per lane, B[kb + 4 q + e][n0 + 4 c .. + 3]
+//      with c = lane % 16; element j is the lane's B operand of the MFMA for
+//      column group j (output columns n0 + 4 c + j)
+// Accumulator j, element r of lane l is C[4 (l / 16) + r][n0 + 4 (l % 16) + j]:
+// for each r a lane owns four consecutive columns.
+#define SWAVES (WM * WN)
+#define KSPLIT (GK / SPLITS)
+#define KW (KSPLIT / SWAVES)
+#define NBATCH (KW / TK)
+#define BLK (TK / 16)
+
+extern "C" __global__ __launch_bounds__(NT) void rc_gemm_f32(GemmF32Args args) {
+    __shared__ f32x4 red[SWAVES][4][64];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int ntn = GN / 64;
+    const int nt = blockIdx.x % ntn, sp = blockIdx.x / ntn;
+    const int n0 = nt * 64;
+    const int k_first = sp * KSPLIT + wave * KW;
+    const int q = lane >> 4, c = lane & 15;
+    const bool arow = c < GM;
+    const float *Arow = args.A + (size_t)(arow ? c : 0) * GK + 4 * q;
+    const float *Bcol = args.B + (size_t)(4 * q) * GN + n0 + 4 * c;
+
+    f32x4 acc[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // Ring of PF register sets: the loads of the next PF - 1 batches are in
+    // flight while a batch is multiplied (PF = 2 x UNROLL, at most NBATCH).
+    constexpr int PF = (2 * UNROLL < NBATCH) ? 2 * UNROLL : NBATCH;
+    f32x4 ra[PF][BLK], rb[PF][BLK][4];
+    auto load = [&](int k0, int set) {
+#pragma unroll
+        for (int b = 0; b < BLK; ++b) {
+            const int kb = k0 + 16 * b;
+            ra[set][b] = arow ? *(const f32x4 *)(Arow + kb) : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) rb[set][b][e] = *(const f32x4 *)(Bcol + (size_t)(kb + e) * GN);
+        }
+    };
+    auto compute = [&](int set) {
+#pragma unroll
+        for (int b = 0; b < BLK; ++b)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(ra[set][b][e], rb[set][b][e][j], acc[j], 0, 0, 0);
+    };
+#pragma unroll
+    for (int p = 0; p < PF; ++p) load(k_first + p * TK, p);
+    for (int i = 0; i < NBATCH; i += PF) {
+#pragma unroll
+        for (int p = 0; p < PF; ++p) {
+            if (i + p < NBATCH) {
+                compute(p);
+                if (i + p + PF < NBATCH) load(k_first + (i + p + PF) * TK, p);
+            }
+        }
+    }
+
+    // add the waves' partial sums in wave order
+    if (SWAVES > 1) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) red[wave][r][lane] = f32x4{acc[0][r], acc[1][r], acc[2][r], acc[3][r]};
+        __syncthreads();
+        if (wave != 0) return;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            f32x4 v = red[0][r][lane];
+#pragma unroll
+            for (int w = 1; w < SWAVES; ++w) v += red[w][r][lane];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[j][r] = v[j];
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int m = 4 * q + r;
+        if (m >= GM) continue;
+        const f32x4 v = f32x4{acc[0][r], acc[1][r], acc[2][r], acc[3][r]};
+#if SPLITS == 1
+        *(f32x4 *)(args.C + (size_t)m * GN + n0 + 4 * c) = v;
+#else
+        *(f32x4 *)(args.P + ((size_t)sp * GM + m) * GN + n0 + 4 * c) = v;
+#endif
+    }
+}
+
+#if SPLITS > 1
+// C = sum over splits of the partials in a fixed association: each of four
+// threads per 4-column group sums the splits g, g + 4, g + 8, ... in order
+// and the four group sums are added in group order through LDS.  A
+// workgroup covers 64 four-column groups.
+extern "C" __global__ __launch_bounds__(256) void rc_gemm_f32_splitk_reduce(GemmF32Args args) {
+    __shared__ f32x4 part[4][64];
+    const int t = threadIdx.x, g = t >> 6;
+    const size_t i = (size_t)blockIdx.x * 64 + (t & 63);
+    const bool ok = i < (size_t)GM * GN / 4;
+    f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (ok) {
+#pragma unroll
+        for (int s = g; s < SPLITS; s += 4) v += *(const f32x4 *)(args.P + (size_t)s * GM * GN + 4 * i);
+    }
+    part[g][t & 63] = v;
+    __syncthreads();
+    if (g == 0 && ok) *(f32x4 *)(args.C + 4 * i) = ((part[0][t] + part[1][t]) + part[2][t]) + part[3][t];
+}
+#endif
+
+#else
 extern "C" __global__ __launch_bounds__(NT) void rc_gemm_f32(GemmF32Args args) {
     __shared__ float As[STAGES][TM][TK + 1];
     __shared__ float Bs[STAGES][TK][TN + 1];
@@ -157,3 +289,4 @@ extern "C" __global__ __launch_bounds__(NT) void rc_gemm_f32(GemmF32Args args) {
                 args.C[(size_t)m * GN + n] = acc[i][j][r];
             }
 }
+#endif

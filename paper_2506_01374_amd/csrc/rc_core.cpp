@@ -33,9 +33,10 @@ static std::vector<KnobDef> gemm_f32_knobs() {
         {"waves_m", "Parallel", {1, 2}, 1},
         {"waves_n", "Parallel", {1, 2}, 1},
         {"vec", "Vectorize", {1, 4}, 1},
-        {"stages", "ComputeLocation", {1, 2}, 1},
+        {"stages", "ComputeLocation", {1, 2, 3}, 1},
         {"unroll", "Unroll", {1, 2, 4}, 1},
         {"layout", "Layout", {0, 1}, 0},
+        {"splits", "Parallel", {1, 2, 4, 8, 16, 32, 64}, 1},   // K splits across workgroups
     };
 }
 
@@ -261,6 +262,33 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
             int st = kv(d, s, "stages"), un = kv(d, s, "unroll"), lay = kv(d, s, "layout");
             int64_t M = D[0], N = D[1], K = D[2];
             int nt = 64 * wm * wn;
+            int sp = kv(d, s, "splits");
+            if (st == 3) {
+                // streaming: one 16-row MFMA block of outputs (decode-shaped
+                // operators), 64 columns per workgroup as 16 lanes x 4
+                // floats, B stored [K][N]; the waves and the SPLITS
+                // workgroups of a column tile each take whole batches of
+                // tile_k rows (16-row blocks) of the K range
+                if (M > 16) return fmt("streaming stage needs M <= 16 (one MFMA row block), M = %lld", (long long)M);
+                if (tm != 16) return "streaming stage takes tile_m 16";
+                if (tn != 64) return "streaming stage takes tile_n 64 (16 lanes x 4 floats)";
+                if (vec != 4) return "streaming stage moves 16-byte vectors (vec 4)";
+                if (lay != 0) return "streaming stage reads B stored K x N";
+                if (tk % 16) return fmt("streaming stage takes tile_k in 16-row blocks (tile_k %d)", tk);
+                if (N % tn) return fmt("tile_n %d does not divide N = %lld", tn, (long long)N);
+                int64_t per = (int64_t)sp * wm * wn * tk;
+                if (K % per)
+                    return fmt("K = %lld is not a whole number of %d-row batches for %d splits x %d waves",
+                               (long long)K, tk, sp, wm * wn);
+                // unroll sets the prefetch depth: 2 x unroll batches of
+                // tile_k rows (5 tile_k / 4 registers each) in flight
+                int64_t nb = K / per;
+                if (2 * un > nb && un > 1) return fmt("prefetch depth %d exceeds the %lld batches per wave", 2 * un, (long long)nb);
+                if ((int64_t)2 * un * tk * 5 / 4 > 160)
+                    return fmt("%d batches of %d rows in flight need more than 160 registers", 2 * un, tk);
+                return "";
+            }
+            if (sp != 1) return "K splits across workgroups need the streaming stage (stages 3)";
             if ((tm / wm) % 16 || tm % wm) return fmt("tile_m/waves_m = %d/%d is not a multiple of 16", tm, wm);
             if ((tn / wn) % 16 || tn % wn) return fmt("tile_n/waves_n = %d/%d is not a multiple of 16", tn, wn);
             if (M % tm) return fmt("tile_m %d does not divide M = %lld", tm, (long long)M);

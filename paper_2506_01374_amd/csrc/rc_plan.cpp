@@ -37,6 +37,7 @@ namespace {
 struct GemmF32Args {
     const void *A, *B;
     void *C;
+    void *P;   // per-split partial sums (streaming stage with K splits)
 };
 struct GemmBf16Args {
     const void *A, *B0, *B1;
@@ -265,20 +266,35 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
         case RC_OP_GEMM_F32: {
             int tm = kv(d, s, "tile_m"), tn = kv(d, s, "tile_n");
             int nt = 64 * kv(d, s, "waves_m") * kv(d, s, "waves_n");
+            int st = kv(d, s, "stages"), sp = kv(d, s, "splits");
             Kern k;
             k.src = Source{SRC_gemm_f32, "rc_gemm_f32", ""};
             k.src.defines = def("TM", tm) + def("TN", tn) + def("TK", kv(d, s, "tile_k")) +
                             def("WM", kv(d, s, "waves_m")) + def("WN", kv(d, s, "waves_n")) +
-                            def("VEC", kv(d, s, "vec")) + def("STAGES", kv(d, s, "stages")) +
+                            def("VEC", kv(d, s, "vec")) + def("STAGES", st) +
                             def("UNROLL", kv(d, s, "unroll")) + def("LAYOUT", kv(d, s, "layout")) +
-                            def("GM", D[0]) + def("GN", D[1]) + def("GK", D[2]);
-            k.grid = dim3((unsigned)(D[1] / tn), (unsigned)(D[0] / tm), 1);
+                            def("SPLITS", sp) + def("GM", D[0]) + def("GN", D[1]) + def("GK", D[2]);
+            // streaming stage: one workgroup per (64-column tile, K split);
+            // with K splits the per-split partial sums live in the workspace
+            const bool split = st == 3 && sp > 1;
+            size_t offP = split ? ws.add((size_t)sp * D[0] * D[1] * 4) : 0;
+            if (st == 3)
+                k.grid = dim3((unsigned)(D[1] / 64 * sp), 1, 1);
+            else
+                k.grid = dim3((unsigned)(D[1] / tn), (unsigned)(D[0] / tm), 1);
             k.block = dim3(nt, 1, 1);
-            k.bind = [](const rc_args *a, char *, std::vector<char> &b) {
-                put(b, GemmF32Args{a->in[0], a->in[1], a->out[0]});
+            k.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
+                put(b, GemmF32Args{a->in[0], a->in[1], a->out[0], split ? w + offP : nullptr});
             };
             p.kerns.push_back(k);
             p.dominant = 0;
+            if (split) {
+                Kern kr = k;
+                kr.src.entry = "rc_gemm_f32_splitk_reduce";
+                kr.grid = dim3((unsigned)((D[0] * D[1] / 4 + 63) / 64), 1, 1);
+                kr.block = dim3(256, 1, 1);
+                p.kerns.push_back(kr);
+            }
             break;
         }
         case RC_OP_GATED_MLP: {

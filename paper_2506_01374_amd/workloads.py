@@ -8,8 +8,10 @@ Llama-4-Scout-style gated MLP 2048 x 4096 x 14336; DeepSeek-style MoE with
 3x3 convolution 2 x 64 x 64 x 320 -> 320; FLUX-style bidirectional (no
 mask) self-attention 1 x 24 heads x 4096 x 128, the image tokens of a
 1024 x 1024 image (Sec. 4.1 names the layers; it prints no shapes, so these
-are chosen stand-ins).  All inputs are synthetic and seeded (see
-``inputs``).
+are chosen stand-ins); and the App. A example module at its printed size,
+C[1, 16, 2048] = A[1, 16, 7168] B[7168, 2048] in fp32 (one expert
+projection of an MoE layer for 16 decode tokens).  All inputs are synthetic
+and seeded (see ``inputs``).
 """
 from __future__ import annotations
 
@@ -27,6 +29,7 @@ WORKLOADS: Dict[str, Tuple[int, Tuple[int, ...], int]] = {
     "moe_t4096_h2048_e64_i1408_top6": (rc.RC_OP_MOE, (4096, 2048, 64, 1408, 6), 0),
     "conv3x3_n2_64x64_c320_k320": (rc.RC_OP_CONV2D, (2, 64, 64, 320, 320, 3, 3, 1), 0),
     "attention_noncausal_b1_h24_s4096_d128": (rc.RC_OP_ATTENTION, (1, 24, 4096, 128), 0),
+    "gemm_f32_m16_n2048_k7168": (rc.RC_OP_GEMM_F32, (16, 2048, 7168), 0),
 }
 
 

@@ -14,6 +14,10 @@ TUNED = json.load(open(os.path.join(ROOT, "paper_2506_01374_amd", "tuned.json"))
 
 SMALL = {
     "gemm": (rc.RC_OP_GEMM_F32, (128, 128, 128), 0),
+    # decode-shaped fp32 contractions (streaming stage, K splits): a full
+    # 16-row MFMA block, and 5 rows (padded inside the block)
+    "gemm_skinny": (rc.RC_OP_GEMM_F32, (16, 256, 1024), 0),
+    "gemm_skinny5": (rc.RC_OP_GEMM_F32, (5, 128, 512), 0),
     "attn_causal": (rc.RC_OP_ATTENTION, (1, 2, 256, 128), rc.RC_FLAG_CAUSAL),
     "attn_full": (rc.RC_OP_ATTENTION, (1, 2, 256, 128), 0),
     "attn_d64": (rc.RC_OP_ATTENTION, (2, 1, 128, 64), rc.RC_FLAG_CAUSAL),
@@ -50,6 +54,20 @@ SCHEDULES = {
         "tile_m=64,tile_n=64,tile_k=32,waves_m=2,waves_n=2,vec=4,stages=2,unroll=2,layout=1",
         "tile_m=32,tile_n=64,tile_k=8,waves_m=2,waves_n=1,vec=1,stages=1,unroll=4,layout=1",
         "tile_m=64,tile_n=32,tile_k=4,waves_m=1,waves_n=2,vec=1,stages=2,unroll=1,layout=0",
+    ],
+    "gemm_skinny": [
+        "",
+        "tile_m=16,tile_n=64,tile_k=32,waves_m=2,waves_n=2,vec=4,stages=3,unroll=1,layout=0,splits=8",
+        "tile_m=16,tile_n=64,tile_k=16,waves_m=1,waves_n=1,vec=4,stages=3,unroll=2,layout=0,splits=1",
+        "tile_m=16,tile_n=64,tile_k=16,waves_m=1,waves_n=2,vec=4,stages=3,unroll=1,layout=0,splits=4",
+        "tile_m=16,tile_n=64,tile_k=32,waves_m=2,waves_n=1,vec=4,stages=3,unroll=2,layout=0,splits=2",
+        "tile_m=16,tile_n=64,tile_k=16,waves_m=2,waves_n=2,vec=4,stages=3,unroll=1,layout=0,splits=16",
+        "tile_m=16,tile_n=64,tile_k=16,waves_m=1,waves_n=1,vec=4,stages=3,unroll=1,layout=0,splits=64",
+    ],
+    "gemm_skinny5": [
+        "tile_m=16,tile_n=64,tile_k=16,waves_m=2,waves_n=2,vec=4,stages=3,unroll=1,layout=0,splits=8",
+        "tile_m=16,tile_n=64,tile_k=32,waves_m=1,waves_n=2,vec=4,stages=3,unroll=1,layout=0,splits=1",
+        "tile_m=16,tile_n=64,tile_k=16,waves_m=1,waves_n=1,vec=4,stages=3,unroll=2,layout=0,splits=2",
     ],
     "attn_causal": [
         "",
