@@ -10,6 +10,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <algorithm>
 #include <cstring>
 #include <string>
 
@@ -280,12 +281,16 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
                 if (K % per)
                     return fmt("K = %lld is not a whole number of %d-row batches for %d splits x %d waves",
                                (long long)K, tk, sp, wm * wn);
-                // unroll sets the prefetch depth: 2 x unroll batches of
-                // tile_k rows (5 tile_k / 4 registers each) in flight
+                // unroll sets the prefetch depth: min(2 x unroll, batches
+                // per wave) batches of tile_k rows (5 tile_k / 4 registers
+                // each) in flight
                 int64_t nb = K / per;
-                if (2 * un > nb && un > 1) return fmt("prefetch depth %d exceeds the %lld batches per wave", 2 * un, (long long)nb);
-                if ((int64_t)2 * un * tk * 5 / 4 > 160)
-                    return fmt("%d batches of %d rows in flight need more than 160 registers", 2 * un, tk);
+                if (un > 1 && un >= nb)
+                    return fmt("unroll %d: all %lld batches per wave are already in flight at a smaller unroll", un,
+                               (long long)nb);
+                int64_t pf = std::min<int64_t>(2 * un, nb);
+                if (pf * tk * 5 / 4 > 160)
+                    return fmt("%lld batches of %d rows in flight need more than 160 registers", (long long)pf, tk);
                 return "";
             }
             if (sp != 1) return "K splits across workgroups need the streaming stage (stages 3)";

@@ -131,12 +131,45 @@ class GpuEvaluator:
 
 
 class TableEvaluator:
-    def __init__(self, path: str):
+    """Measured samples replayed from a table: a previous run's JSONL, or a
+    TSV of one sub-space (comment lines, a '# fixed: knob=v,...' line, a
+    header of the varying knobs and 'us', then one row per schedule with its
+    median microseconds or the reason it was rejected)."""
+
+    def __init__(self, path: str, op: Optional[rc.Op] = None):
         self.table: Dict[str, dict] = {}
+        if path.endswith(".tsv"):
+            if op is None:
+                raise ValueError("a TSV table needs the operator")
+            fixed, header = "", None
+            for line in open(path):
+                line = line.rstrip("\n")
+                if line.startswith("# fixed:"):
+                    fixed = line.split(":", 1)[1].strip()
+                elif line.startswith("#") or not line:
+                    continue
+                elif header is None:
+                    header = line.split("\t")
+                else:
+                    vals = line.split("\t")
+                    text = ",".join([fixed] + [f"{k}={v}" for k, v in zip(header[:-1], vals[:-1])])
+                    key = str(op.from_string(text))
+                    if vals[-1] in ("spill", "error"):
+                        self.table[key] = {"schedule": key, "valid": False, "error": vals[-1]}
+                    else:
+                        ms = float(vals[-1]) * 1e-3
+                        self.table[key] = {"schedule": key, "valid": True, "ms": ms,
+                                           "reward": reward_of(op, ms)}
+            return
         for line in open(path):
             r = json.loads(line)
             if "schedule" in r and "valid" in r:
                 self.table[r["schedule"]] = r
+
+    def contains(self, sched: rc.Schedule) -> bool:
+        """Whether the schedule lies in the measured space (outside it the
+        table plays the part of a compiler that rejects it)."""
+        return str(sched) in self.table
 
     def measure(self, sched: rc.Schedule) -> dict:
         return self.table.get(str(sched), {"schedule": str(sched), "valid": False, "error": "not in table"})
@@ -180,32 +213,123 @@ class FeedbackProposer:
         return self.rng.choice(moves) if moves else ""
 
 
+class SurrogateEvaluator:
+    """Rollout rewards from a learned surrogate (Sec. 3.2: the terminal
+    program of a rollout is scored by a cheap learned model f-hat rather
+    than on hardware).  Wraps a real evaluator.  The first `warm` distinct
+    schedules are measured; after that an ensemble of randomised regression
+    trees, refitted every `refit` measurements on the measured knob vectors,
+    predicts each new rollout terminal.  A terminal is measured only when
+    its prediction is within `margin` of the best measured reward (or, with
+    probability `explore`, at random); otherwise the prediction is the
+    rollout reward and no sample is spent.  Only measurements are samples:
+    `curve` is the best measured reward after each of them.  A schedule the
+    inner evaluator places outside its space (a replayed table's `contains`)
+    is invalid at no cost, as it is without the surrogate."""
+
+    def __init__(self, op: rc.Op, inner, seed: int, warm: int = 16, refit: int = 8,
+                 margin: float = 0.9, explore: float = 0.05):
+        import random
+        self.op, self.inner, self.seed = op, inner, seed
+        self.warm, self.refit, self.margin, self.explore = warm, refit, margin, explore
+        self.rng = random.Random(seed)
+        self.X: List[List[int]] = []
+        self.y: List[float] = []
+        self.model = None
+        self.fitted_at = 0
+        self.measured = 0
+        self.predicted = 0
+        self.calls = 0
+        self.best = 0.0
+        self.best_text: Optional[str] = None
+        self.curve: List[float] = []
+
+    @staticmethod
+    def features(sched: rc.Schedule) -> List[int]:
+        return list(sched.as_dict().values())
+
+    def _fit(self):
+        from sklearn.ensemble import ExtraTreesRegressor
+        import numpy as np
+        m = ExtraTreesRegressor(n_estimators=48, min_samples_leaf=2, random_state=self.seed)
+        m.fit(np.array(self.X, dtype=np.float64), np.array(self.y, dtype=np.float64))
+        self.model, self.fitted_at = m, len(self.y)
+
+    def _measure(self, sched: rc.Schedule) -> Optional[float]:
+        r = self.inner.measure(sched)
+        reward = r["reward"] if r.get("valid") else None
+        self.X.append(self.features(sched))
+        self.y.append(reward if reward is not None else 0.0)   # invalid: learn it as worthless
+        if reward is not None:
+            self.measured += 1
+            if reward > self.best:
+                self.best, self.best_text = reward, str(sched)
+            self.curve.append(self.best)
+        return reward
+
+    def __call__(self, sched: rc.Schedule) -> Optional[float]:
+        self.calls += 1
+        contains = getattr(self.inner, "contains", None)
+        if contains is not None and not contains(sched):
+            return None
+        if len(self.y) < self.warm:
+            return self._measure(sched)
+        if self.model is None or len(self.y) - self.fitted_at >= self.refit:
+            self._fit()
+        import numpy as np
+        pred = float(self.model.predict(np.array([self.features(sched)], dtype=np.float64))[0])
+        if pred >= self.margin * self.best or self.rng.random() < self.explore:
+            return self._measure(sched)
+        self.predicted += 1
+        return max(pred, 0.0)
+
+
 def run_search(op, evaluator, policy: str, budget: int, seed: int, horizon=12, branching=2,
-               c=math.sqrt(2.0), proposer: Optional[str] = None):
+               c=math.sqrt(2.0), proposer: Optional[str] = None, surrogate: bool = False):
     prop = FeedbackProposer(op, seed) if proposer == "feedback" else None
+    sur = SurrogateEvaluator(op, evaluator, seed) if surrogate else None
 
     def ev(s):
-        r = evaluator.measure(s)
-        reward = r["reward"] if r.get("valid") else None
+        if sur is not None:
+            reward = sur(s)
+        else:
+            r = evaluator.measure(s)
+            reward = r["reward"] if r.get("valid") else None
         if prop is not None:
             prop.record(s, reward)
         return reward
 
-    srch = rc.Search(op, ev, policy=POLICIES[policy], budget=budget, horizon=horizon,
+    # with a surrogate only measurements count, so the driver's own budget
+    # (which counts every rollout reward) is a loose cap
+    srch = rc.Search(op, ev, policy=POLICIES[policy], budget=budget * (40 if sur else 1), horizon=horizon,
                      branching=branching, c=c, seed=seed, propose=prop)
-    srch.run()
+    if sur is None:
+        srch.run()
+    else:
+        # stop when the measurements are spent, or when the tree has stopped
+        # reaching schedules it has not scored (every rollout a repeat)
+        last, idle = sur.calls, 0
+        while sur.measured < budget and idle < 20 * budget and not srch.step():
+            idle = 0 if sur.calls != last else idle + 1
+            last = sur.calls
     hist = srch.history()
-    try:
-        best, reward, idx = srch.best()
-        best_text = str(best)
-    except rc.RCError:
-        best_text, reward, idx = None, 0.0, -1
-    curve = [h["best_so_far"] for h in hist if h["valid"]]
+    if sur is None:
+        try:
+            best, reward, idx = srch.best()
+            best_text = str(best)
+        except rc.RCError:
+            best_text, reward, idx = None, 0.0, -1
+        curve = [h["best_so_far"] for h in hist if h["valid"]]
+    else:
+        best_text, reward, idx = sur.best_text, sur.best, len(sur.curve) - 1
+        curve = sur.curve
     # samples to reach the run's best (within 1%)
     to_best = next((i + 1 for i, v in enumerate(curve) if v >= 0.99 * reward), None) if curve else None
-    return {"policy": policy, "proposer": proposer, "fallbacks": srch.fallbacks() if prop else None,
-            "seed": seed, "budget": budget, "valid": sum(h["valid"] for h in hist),
-            "invalid": sum(not h["valid"] for h in hist), "best": best_text, "best_reward": reward,
+    return {"policy": policy, "proposer": proposer, "surrogate": surrogate,
+            "fallbacks": srch.fallbacks() if prop else None,
+            "seed": seed, "budget": budget, "valid": len(curve) if sur else sum(h["valid"] for h in hist),
+            "invalid": sum(not h["valid"] for h in hist), "predicted": sur.predicted if sur else 0,
+            "best": best_text, "best_reward": reward,
             "best_index": idx, "samples_to_best": to_best, "curve": curve}
 
 
@@ -231,6 +355,8 @@ def main(argv=None):
     ap.add_argument("--c", type=float, default=math.sqrt(2.0))
     ap.add_argument("--proposer", default=None, choices=["feedback"],
                     help="expansion proposals from measured history (default: random legal)")
+    ap.add_argument("--surrogate", action="store_true",
+                    help="score rollouts with a learned surrogate; measure only promising ones")
     ap.add_argument("--repeat", type=int, default=10)
     ap.add_argument("--out", default="tune_out")
     ap.add_argument("--enumerate", action="store_true", help="list the whole legal space")
@@ -264,10 +390,10 @@ def main(argv=None):
                       f"{time.time() - t0:.0f}s", flush=True)
         return
 
-    tag = args.policy + (f"+{args.proposer}" if args.proposer else "")
+    tag = args.policy + (f"+{args.proposer}" if args.proposer else "") + ("+surrogate" if args.surrogate else "")
     log = open(os.path.join(args.out, f"{args.workload}.{tag}.jsonl"), "a")
     if args.replay:
-        evaluator = TableEvaluator(args.replay)
+        evaluator = TableEvaluator(args.replay, op)
     else:
         evaluator = GpuEvaluator(op, repeat=args.repeat, log=log)
 
@@ -287,7 +413,7 @@ def main(argv=None):
     for seed in _parse_seeds(args.seeds):
         t0 = time.time()
         res = run_search(op, evaluator, args.policy, args.budget, seed, args.horizon, args.branching, args.c,
-                         args.proposer)
+                         args.proposer, args.surrogate)
         res.update(workload=args.workload, kind="search", wall_s=time.time() - t0)
         log.write(json.dumps(res) + "\n")
         log.flush()

@@ -259,3 +259,84 @@ def test_branching_factor_bounds_children_per_node(B):
     assert sum(visits) == 8 and s.node_stats([])[0] == 8
     assert len(evals) == B and len(set(evals)) == B     # each leaf measured once
     assert s.fallbacks() == 0
+
+
+class _SyntheticTable:
+    """A measured-table stand-in: the synthetic reward of every schedule."""
+
+    def __init__(self):
+        self.calls = 0
+
+    def measure(self, s):
+        self.calls += 1
+        return {"schedule": str(s), "valid": True, "reward": synthetic_reward(s)}
+
+
+def test_surrogate_scores_rollouts_and_counts_only_measurements():
+    # Rollout terminals are predicted by the learned surrogate and measured
+    # only when promising (Sec. 3.2): the GPU budget counts measurements, not
+    # rollouts; the curve is the best measured reward per measurement.
+    from paper_2506_01374_amd.tune import run_search
+    op = rc.Op(rc.RC_OP_GEMM_F32, (128, 128, 128))
+    ex = rc.Search(op, synthetic_reward, policy=rc.RC_POLICY_EXHAUSTIVE, budget=100000).run()
+    _, r_ex, _ = ex.best()
+    table = _SyntheticTable()
+    res = run_search(op, table, "uct", budget=64, seed=3, surrogate=True)
+    # (the driver may run out of new schedules in this small space first)
+    assert res["valid"] == len(res["curve"]) == table.calls and 32 <= table.calls <= 64
+    assert res["predicted"] > table.calls
+    assert res["curve"] == sorted(res["curve"]) and res["best_reward"] == res["curve"][-1]
+    assert res["best_reward"] <= r_ex + 1e-12 and res["best_reward"] >= 0.8 * r_ex
+    # deterministic for a seed
+    again = run_search(op, _SyntheticTable(), "uct", budget=64, seed=3, surrogate=True)
+    assert again["curve"] == res["curve"] and again["best"] == res["best"]
+
+
+def test_measured_attention_table_parses_and_its_optimum_is_the_tuned_schedule():
+    # The committed table of measured schedules (one sub-space of causal
+    # attention) replays through the same evaluator interface as a live GPU
+    # run; every row is a legal schedule of the workload.
+    import json
+    from paper_2506_01374_amd import workloads as W
+    from paper_2506_01374_amd.tune import TableEvaluator
+    name = "attention_causal_b1_h32_s1024_d128"
+    op = W.workload_op(name)
+    path = os.path.join(HERE, "..", "results", f"{name}.space.tsv")
+    tab = TableEvaluator(path, op)
+    assert len(tab.table) == 3174
+    assert all(op.from_string(k).validate() == "" for k in tab.table)
+    valid = [r for r in tab.table.values() if r["valid"]]
+    assert len(valid) == 2916
+    best = max(valid, key=lambda r: r["reward"])
+    tuned = json.load(open(os.path.join(HERE, "..", "paper_2506_01374_amd", "tuned.json")))[name]
+    assert best["schedule"] == str(op.from_string(tuned))
+
+
+def test_surrogate_replay_spends_nothing_outside_the_measured_space():
+    # Replayed against a table, a schedule the table does not hold is
+    # invalid at no cost: it is neither measured nor predicted, exactly as
+    # it is for the search without a surrogate.
+    from paper_2506_01374_amd import workloads as W
+    from paper_2506_01374_amd.tune import SurrogateEvaluator, TableEvaluator
+    name = "attention_causal_b1_h32_s1024_d128"
+    op = W.workload_op(name)
+    tab = TableEvaluator(os.path.join(HERE, "..", "results", f"{name}.space.tsv"), op)
+    looked = []
+
+    class Spy:
+        contains = staticmethod(tab.contains)
+
+        def measure(self, s):
+            looked.append(str(s))
+            return tab.measure(s)
+
+    sur = SurrogateEvaluator(op, Spy(), seed=1)
+    srch = rc.Search(op, sur, policy=rc.RC_POLICY_UCT, budget=2000, seed=1)
+    while sur.measured < 24 and not srch.step():
+        pass
+    assert sur.measured >= 24 and sur.predicted > 0
+    assert all(k in tab.table for k in looked)
+    spills = sum(1 for k in looked if not tab.table[k]["valid"])
+    invalid = sum(1 for h in srch.history() if not h["valid"])
+    assert len(looked) == sur.measured + spills
+    assert sur.calls == sur.measured + sur.predicted + invalid and invalid > spills
