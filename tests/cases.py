@@ -197,6 +197,8 @@ FULL_ALT = [
     ("attention_causal_b1_h32_s1024_d128",
      "block_m=64,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=2,order=2,occ=2"),
     ("attention_causal_b1_h32_s1024_d128",
+     "block_m=64,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=1,order=2,occ=2"),
+    ("attention_causal_b1_h32_s1024_d128",
      "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=1,occ=4,splits=2"),
     ("attention_causal_b1_h32_s1024_d128",
      "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=2,occ=2,chunk=16"),

@@ -292,24 +292,29 @@ def test_surrogate_scores_rollouts_and_counts_only_measurements():
     assert again["curve"] == res["curve"] and again["best"] == res["best"]
 
 
-def test_measured_attention_table_parses_and_its_optimum_is_the_tuned_schedule():
-    # The committed table of measured schedules (one sub-space of causal
-    # attention) replays through the same evaluator interface as a live GPU
-    # run; every row is a legal schedule of the workload.
+def test_measured_attention_tables_parse_and_hold_the_tuned_schedule():
+    # The committed tables of measured schedules (one sub-space of causal
+    # attention, cold; its direct-to-LDS part, warm) replay through the same
+    # evaluator interface as a live GPU run; every row is a legal schedule of
+    # the workload.  The benchmark runs warm, and its tuned schedule is the
+    # warm table's fastest (within the 1 % the table's ties span).
     import json
     from paper_2506_01374_amd import workloads as W
     from paper_2506_01374_amd.tune import TableEvaluator
     name = "attention_causal_b1_h32_s1024_d128"
     op = W.workload_op(name)
-    path = os.path.join(HERE, "..", "results", f"{name}.space.tsv")
-    tab = TableEvaluator(path, op)
-    assert len(tab.table) == 3174
-    assert all(op.from_string(k).validate() == "" for k in tab.table)
-    valid = [r for r in tab.table.values() if r["valid"]]
+    tuned = str(op.from_string(json.load(open(os.path.join(HERE, "..", "paper_2506_01374_amd", "tuned.json")))[name]))
+    cold = TableEvaluator(os.path.join(HERE, "..", "results", f"{name}.space.tsv"), op)
+    assert len(cold.table) == 3174
+    assert all(op.from_string(k).validate() == "" for k in cold.table)
+    valid = [r for r in cold.table.values() if r["valid"]]
     assert len(valid) == 2916
-    best = max(valid, key=lambda r: r["reward"])
-    tuned = json.load(open(os.path.join(HERE, "..", "paper_2506_01374_amd", "tuned.json")))[name]
-    assert best["schedule"] == str(op.from_string(tuned))
+    assert cold.table[tuned]["valid"]
+    warm = TableEvaluator(os.path.join(HERE, "..", "results", f"{name}.direct_lds.warm.tsv"), op)
+    assert len(warm.table) == 166 and all(r["valid"] for r in warm.table.values())
+    assert set(warm.table) <= set(cold.table)
+    fastest = min(r["ms"] for r in warm.table.values())
+    assert warm.table[tuned]["ms"] <= 1.01 * fastest
 
 
 def test_surrogate_replay_spends_nothing_outside_the_measured_space():
