@@ -526,22 +526,28 @@ void rc_attention(AttnArgs args) {
     auto softmax_pv_at = [&](int kt, const bf16_t *Vt, accT (&sc)[QB][KB]) {
 #if STAGES >= 4
         // the tile's V^T fragments (at most 16 x 16 B per lane) are read
-        // before the softmax, which does not need them, so their LDS latency
-        // overlaps the exponentials and reductions
+        // ahead of their MFMAs: the first NPRE d-blocks before the softmax,
+        // which does not need them, so their LDS latency overlaps the
+        // exponentials and reductions, the rest together before the first
+        // P.V MFMA.  With two key splits the workgroup's waves must fit four
+        // per SIMD (128 registers), which leaves room for half of them
+        // across the softmax.
         typedef short v4i16 __attribute__((ext_vector_type(4)));
         typedef __attribute__((address_space(3))) v4i16 *lds_v4p;
-        constexpr bool VPRE = SPLITS == 1 && (BN / KSTEP) * DB <= 16;
+        constexpr bool VPRE = (BN / KSTEP) * DB <= 16;
+        constexpr int NPRE = SPLITS == 1 ? DB : DB / 2;
         bf16x8 vpre[VPRE ? BN / KSTEP : 1][VPRE ? DB : 1];
+        auto read_vt = [&](int j, int db) {
+            const bf16_t *const vp = Vt + voff[db] + 32 * j * AD;
+            const v4i16 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4p)(vp));
+            const v4i16 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4p)(vp + 16 * AD));
+            return __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+        };
         if (VPRE) {
 #pragma unroll
             for (int j = 0; j < (VPRE ? BN / KSTEP : 1); ++j)
 #pragma unroll
-                for (int db = 0; db < (VPRE ? DB : 1); ++db) {
-                    const bf16_t *const vp = Vt + voff[db] + 32 * j * AD;
-                    const v4i16 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4p)(vp));
-                    const v4i16 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4p)(vp + 16 * AD));
-                    vpre[j][db] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
-                }
+                for (int db = 0; db < (VPRE ? NPRE : 1); ++db) vpre[j][db] = read_vt(j, db);
         }
 #endif
         // online softmax, one query per lane; m is kept in log2 units and the
@@ -616,18 +622,16 @@ void rc_attention(AttnArgs args) {
 #endif
                 pf[qb] = __builtin_bit_cast(bf16x8, pw);
             }
+#if STAGES >= 4
+            if (VPRE) {
+#pragma unroll
+                for (int db = NPRE; db < (VPRE ? DB : 0); ++db) vpre[VPRE ? j : 0][db] = read_vt(j, db);
+            }
+#endif
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
 #if STAGES >= 4
-                bf16x8 vf;
-                if (VPRE) {
-                    vf = vpre[VPRE ? j : 0][VPRE ? db : 0];
-                } else {
-                    const bf16_t *const vp = Vt + voff[db] + 32 * j * AD;
-                    const v4i16 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4p)(vp));
-                    const v4i16 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4p)(vp + 16 * AD));
-                    vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
-                }
+                const bf16x8 vf = VPRE ? vpre[VPRE ? j : 0][VPRE ? db : 0] : read_vt(j, db);
                 (void)c0;
 #else
                 const int drow = db * MF + lane % MF;
