@@ -36,7 +36,10 @@
 //   EPI          0 store bf16; 1 + bias, SiLU, store bf16; 2 SiLU(acc0) *
 //                acc1, store bf16; 3 store fp32 accumulators (unfused)
 //   GM GN GK     GEMM sizes (GM = rows for AMODE 0/2, total routed rows for
-//                AMODE 1/3)
+//                AMODE 1/3).  Dense rows (AMODE 0/2) need not fill the last
+//                M tile: its missing rows load zeros (register staging) or
+//                repeat the tile's first row (direct-to-LDS loads) and are
+//                never stored.
 //
 // LDS holds both operands as rows of TK bf16 (K contiguous).  16-byte
 // chunks are XOR-swizzled with the row so that the 16 lanes that share a
@@ -56,6 +59,7 @@
 #define CPR (TK / 8)
 #define RPL ((16 / CPR) > 0 ? (16 / CPR) : 1)
 #define KTILES (GK / TK)
+#define RAGGED_M ((AMODE == 0 || AMODE == 2) && (GM % TM) != 0)
 #define A_LOADS ((TM * TK) / (VEC * NT))
 #define B_LOADS ((TN * TK) / (VEC * NT))
 #define NTN (GN / TN)
@@ -197,7 +201,7 @@ void rc_gemm_bf16(GemmBf16Args args) {
 #endif
 #else
     const int row_base = mt * TM;
-    const int rows_valid = TM;
+    const int rows_valid = RAGGED_M ? min(TM, GM - row_base) : TM;
     const bf16_t *B0 = args.B0;
 #if NB == 2
     const bf16_t *B1 = args.B1;
@@ -222,10 +226,10 @@ void rc_gemm_bf16(GemmBf16Args args) {
 #if AMODE == 1 || AMODE == 3
         aval[i] = r < rows_valid;
 #else
-        aval[i] = true;          // dense rows: every tile is full
+        aval[i] = !RAGGED_M || r < rows_valid;
 #endif
 #if AMODE == 0
-        arow[i] = args.A + (size_t)(row_base + r) * GK;
+        arow[i] = args.A + (size_t)(aval[i] ? row_base + r : 0) * GK;
 #elif AMODE == 1
         int tok = aval[i] ? args.perm[row_base + r] / TOPK : 0;
         arow[i] = args.A + (size_t)tok * GK;
@@ -241,7 +245,7 @@ void rc_gemm_bf16(GemmBf16Args args) {
             const int ih = p + tap / CV_S - CV_PAD, iw = q + tap % CV_S - CV_PAD;
             if (ih >= 0 && ih < CV_H && iw >= 0 && iw < CV_W) mask |= 1u << tap;
         }
-        a_mask[i] = mask;
+        a_mask[i] = aval[i] ? mask : 0u;      // rows past GM load nothing
         arow[i] = args.A;
 #endif
     }
@@ -385,7 +389,8 @@ void rc_gemm_bf16(GemmBf16Args args) {
         const int c = (wave * A_WL + j) * 64 + lane;
         const int row = c / CPR, lc = (c % CPR) ^ ((row / RPL) % CPR);
 #if AMODE == 0
-        a_src[j] = args.A + (size_t)(row_base + row) * GK + lc * 8;
+        // rows past GM read the tile's first row; their products are never stored
+        a_src[j] = args.A + (size_t)(row_base + (RAGGED_M && row >= rows_valid ? 0 : row)) * GK + lc * 8;
 #elif AMODE == 1
         // rows past the group read a valid row; their products are never stored
         const int tok = args.perm[row_base + (row < rows_valid ? row : 0)] / TOPK;
@@ -487,7 +492,7 @@ void rc_gemm_bf16(GemmBf16Args args) {
     unsigned voff[NX];
 #pragma unroll
     for (int x = 0; x < NX; ++x) voff[x] = (unsigned)(r_l * GK * 2 + ((lc0 ^ (4 * x)) << 4));
-#if AMODE != 0
+#if AMODE != 0 || RAGGED_M
     // gathered or ragged rows: one offset (from args.A) per load
     unsigned a_off[A_WL];
 #pragma unroll
@@ -512,7 +517,7 @@ void rc_gemm_bf16(GemmBf16Args args) {
             vo[x] = voff[x];
             asm volatile("" : "+v"(vo[x]));
         }
-#if AMODE != 0
+#if AMODE != 0 || RAGGED_M
         unsigned ao[A_WL];
 #pragma unroll
         for (int j = 0; j < A_WL; ++j) {
@@ -523,7 +528,7 @@ void rc_gemm_bf16(GemmBf16Args args) {
 #pragma unroll
         for (int j = 0; j < A_WL; ++j) {
             const int W = lw * A_WL + j;
-#if AMODE == 0
+#if AMODE == 0 && !RAGGED_M
             const char *base = (const char *)(args.A + ((size_t)row_base + W * (64 / CPR)) * GK + k0);
             __builtin_amdgcn_global_load_lds((gbl_vp)(base + vo[A_WL % NX == 0 ? j % NX : W % NX]), (lds_vp)(la + W * 512), 16, 0, 0);
 #else

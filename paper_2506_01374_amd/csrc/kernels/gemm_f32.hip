@@ -18,7 +18,11 @@
 //   SPLITS       K splits across workgroups (Parallel; STAGES 3 only)
 //   UNROLL       unroll factor of the K-tile loop (Unroll)
 //   LAYOUT       0: B stored [K][N]; 1: B stored [N][K] (Layout)
-//   GM GN GK     problem size; every tile is perfect (checked on the host).
+//   GM GN GK     problem size.  Stages 1 and 2 take any size: tiles that
+//                cross the edge of M, N or K load zeros there and store only
+//                inside C (VEC divides the row lengths, so a vector is wholly
+//                inside or outside); a problem that every tile divides
+//                compiles without the guards.  Stage 3 needs whole tiles.
 //
 // MFMA lane layout (16x16x4, one block): lane l supplies A[l % 16][l / 16]
 // and B[l / 16][l % 16]; accumulator element r of lane l is
@@ -29,7 +33,8 @@
 #define WTN (TN / WN)
 #define FM (WTM / 16)
 #define FN (WTN / 16)
-#define KTILES (GK / TK)
+#define KTILES ((GK + TK - 1) / TK)
+#define RAGGED ((GM % TM) != 0 || (GN % TN) != 0 || (GK % TK) != 0)
 #define A_LOADS ((TM * TK) / (VEC * NT))
 #define B_LOADS ((TK * TN) / (VEC * NT))
 
@@ -197,22 +202,28 @@ extern "C" __global__ __launch_bounds__(NT) void rc_gemm_f32(GemmF32Args args) {
 
     vecT ra[A_LOADS], rb[B_LOADS];
 
+    // a vector load of row `row`, columns col .. col + VEC - 1 of a
+    // rows x cols matrix; zeros outside it (tiles crossing an edge)
+    auto ld = [&](const float *base, int row, int col, int rows, int cols) -> vecT {
+        if (RAGGED && (row >= rows || col >= cols)) return vecT{};
+        return *(const vecT *)(base + (size_t)row * cols + col);
+    };
     auto gload = [&](int k0) {
 #pragma unroll
         for (int i = 0; i < A_LOADS; ++i) {
             int v = tid + i * NT;
             int r = v / (TK / VEC), c = (v % (TK / VEC)) * VEC;
-            ra[i] = *(const vecT *)(args.A + (size_t)(m0 + r) * GK + k0 + c);
+            ra[i] = ld(args.A, m0 + r, k0 + c, GM, GK);
         }
 #pragma unroll
         for (int i = 0; i < B_LOADS; ++i) {
             int v = tid + i * NT;
 #if LAYOUT == 0
             int r = v / (TN / VEC), c = (v % (TN / VEC)) * VEC;
-            rb[i] = *(const vecT *)(args.B + (size_t)(k0 + r) * GN + n0 + c);
+            rb[i] = ld(args.B, k0 + r, n0 + c, GK, GN);
 #else
             int r = v / (TK / VEC), c = (v % (TK / VEC)) * VEC;
-            rb[i] = *(const vecT *)(args.B + (size_t)(n0 + r) * GK + k0 + c);
+            rb[i] = ld(args.B, n0 + r, k0 + c, GN, GK);
 #endif
         }
     };
@@ -286,7 +297,7 @@ extern "C" __global__ __launch_bounds__(NT) void rc_gemm_f32(GemmF32Args args) {
             for (int r = 0; r < 4; ++r) {
                 int m = m0 + wm * WTM + i * 16 + 4 * (lane >> 4) + r;
                 int n = n0 + wn * WTN + j * 16 + (lane & 15);
-                args.C[(size_t)m * GN + n] = acc[i][j][r];
+                if (!RAGGED || (m < GM && n < GN)) args.C[(size_t)m * GN + n] = acc[i][j][r];
             }
 }
 #endif

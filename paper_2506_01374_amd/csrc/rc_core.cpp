@@ -162,8 +162,9 @@ static std::string fmt(const char *f, ...) {
 
 static const int64_t LDS_LIMIT = 163840;   // bytes one workgroup may allocate on gfx950
 
-// Rules for one bf16 GEMM stage of shape M x N x K (M < 0: ragged rows,
-// predicated), NB weight operands sharing the A tile.
+// Rules for one bf16 GEMM stage of shape M x N x K (M < 0: ragged expert
+// groups), NB weight operands sharing the A tile.  Any M is legal: the last
+// M tile's missing rows are predicated off.
 static std::string check_bf16_block(const rc_op_desc *d, const rc_schedule *s,
                                     const char *const names[12], int64_t M, int64_t N, int64_t K,
                                     int NB, const char *tag, bool im2col = false) {
@@ -180,7 +181,10 @@ static std::string check_bf16_block(const rc_op_desc *d, const rc_schedule *s,
         return fmt("%s: tile_n/waves_n = %d/%d is not a multiple of the %dx%d MFMA", tag, tn, wn,
                    mf, mf);
     if (tk % 32) return fmt("%s: tile_k %d is not a multiple of 32", tag, tk);
-    if (M > 0 && M % tm) return fmt("%s: tile_m %d does not divide M = %lld", tag, tm, (long long)M);
+    // rows need not fill the last M tile (predicated, for dense and ragged
+    // rows alike); a tile twice the rows it covers adds only empty work
+    if (M > 0 && tm > M && tm / 2 >= M)
+        return fmt("%s: tile_m %d: tile_m %d already covers M = %lld", tag, tm, tm / 2, (long long)M);
     if (N % tn) return fmt("%s: tile_n %d does not divide N = %lld", tag, tn, (long long)N);
     if (K % tk) return fmt("%s: tile_k %d does not divide K = %lld", tag, tk, (long long)K);
     if ((int64_t)tm * tk % ((int64_t)vec * nt))
@@ -296,16 +300,23 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
             if (sp != 1) return "K splits across workgroups need the streaming stage (stages 3)";
             if ((tm / wm) % 16 || tm % wm) return fmt("tile_m/waves_m = %d/%d is not a multiple of 16", tm, wm);
             if ((tn / wn) % 16 || tn % wn) return fmt("tile_n/waves_n = %d/%d is not a multiple of 16", tn, wn);
-            if (M % tm) return fmt("tile_m %d does not divide M = %lld", tm, (long long)M);
-            if (N % tn) return fmt("tile_n %d does not divide N = %lld", tn, (long long)N);
-            if (K % tk) return fmt("tile_k %d does not divide K = %lld", tk, (long long)K);
+            // tiles may cross the edges of M, N and K (zero-filled loads,
+            // predicated stores), but a tile twice the extent it covers adds
+            // only empty work (the halved tile covers it too); a vector load
+            // must not cross a row end
+            if (tm > M && tm / 2 >= M) return fmt("tile_m %d: tile_m %d already covers M = %lld", tm, tm / 2, (long long)M);
+            if (tn > N && tn / 2 >= N) return fmt("tile_n %d: tile_n %d already covers N = %lld", tn, tn / 2, (long long)N);
+            if (tk > K && tk / 2 >= K) return fmt("tile_k %d: tile_k %d already covers K = %lld", tk, tk / 2, (long long)K);
+            if (K % vec) return fmt("vec %d does not divide the rows of A (K = %lld)", vec, (long long)K);
+            if (lay == 0 && N % vec) return fmt("vec %d does not divide the rows of B (N = %lld)", vec, (long long)N);
             if ((tm * tk) % (vec * nt))
                 return fmt("A tile %dx%d does not split into %d threads x %d-wide loads", tm, tk, nt, vec);
             if ((tk * tn) % (vec * nt))
                 return fmt("B tile %dx%d does not split into %d threads x %d-wide loads", tk, tn, nt, vec);
             if (tk % vec) return fmt("vec %d does not divide tile_k %d", vec, tk);
             if (lay == 0 && tn % vec) return fmt("vec %d does not divide tile_n %d", vec, tn);
-            if ((K / tk) % un) return fmt("unroll %d does not divide the %lld K tiles", un, (long long)(K / tk));
+            const int64_t ktiles = (K + tk - 1) / tk;
+            if (ktiles % un) return fmt("unroll %d does not divide the %lld K tiles", un, (long long)ktiles);
             int64_t lds = (int64_t)st * (tm * (tk + 1) + tk * (tn + 1)) * 4;
             if (lds > LDS_LIMIT) return fmt("LDS %lld B exceeds limit", (long long)lds);
             return "";

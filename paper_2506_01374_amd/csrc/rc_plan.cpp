@@ -281,7 +281,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             if (st == 3)
                 k.grid = dim3((unsigned)(D[1] / 64 * sp), 1, 1);
             else
-                k.grid = dim3((unsigned)(D[1] / tn), (unsigned)(D[0] / tm), 1);
+                k.grid = dim3((unsigned)((D[1] + tn - 1) / tn), (unsigned)((D[0] + tm - 1) / tm), 1);
             k.block = dim3(nt, 1, 1);
             k.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
                 put(b, GemmF32Args{a->in[0], a->in[1], a->out[0], split ? w + offP : nullptr});
@@ -309,7 +309,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             }
             Kern k1;
             k1.src = Source{SRC_gemm_bf16, "rc_gemm_bf16", gemm_defs(up, 2, 0, fuse ? 2 : 3, T, I, Hd)};
-            k1.grid = dim3((unsigned)((T / up.tm) * (I / up.tn)), 1, 1);
+            k1.grid = dim3((unsigned)(((T + up.tm - 1) / up.tm) * (I / up.tn)), 1, 1);
             k1.block = dim3(64 * up.wm * up.wn, 1, 1);
             k1.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
                 if (fuse)
@@ -332,7 +332,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             }
             Kern k2;
             k2.src = Source{SRC_gemm_bf16, "rc_gemm_bf16", gemm_defs(dn, 1, 0, 0, T, Hd, I)};
-            k2.grid = dim3((unsigned)((T / dn.tm) * (Hd / dn.tn)), 1, 1);
+            k2.grid = dim3((unsigned)(((T + dn.tm - 1) / dn.tm) * (Hd / dn.tn)), 1, 1);
             k2.block = dim3(64 * dn.wm * dn.wn, 1, 1);
             k2.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
                 put(b, GemmBf16Args{w + offH, a->in[3], nullptr, a->out[0], nullptr, nullptr,
@@ -419,7 +419,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             Kern k1;
             k1.src = Source{SRC_gemm_bf16, "rc_gemm_bf16",
                             gemm_defs(g, 1, 2, fuse ? 1 : 3, M, K, R * S * C) + cv};
-            k1.grid = dim3((unsigned)((M / g.tm) * (K / g.tn)), 1, 1);
+            k1.grid = dim3((unsigned)(((M + g.tm - 1) / g.tm) * (K / g.tn)), 1, 1);
             k1.block = dim3(64 * g.wm * g.wn, 1, 1);
             k1.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
                 if (fuse)

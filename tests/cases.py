@@ -18,14 +18,22 @@ SMALL = {
     # 16-row MFMA block, and 5 rows (padded inside the block)
     "gemm_skinny": (rc.RC_OP_GEMM_F32, (16, 256, 1024), 0),
     "gemm_skinny5": (rc.RC_OP_GEMM_F32, (5, 128, 512), 0),
+    # ragged tails: no tile size divides M, N or K
+    "gemm_ragged": (rc.RC_OP_GEMM_F32, (100, 72, 52), 0),
+    "gemm_ragged_odd": (rc.RC_OP_GEMM_F32, (37, 50, 30), 0),
     "attn_causal": (rc.RC_OP_ATTENTION, (1, 2, 256, 128), rc.RC_FLAG_CAUSAL),
     "attn_full": (rc.RC_OP_ATTENTION, (1, 2, 256, 128), 0),
     "attn_d64": (rc.RC_OP_ATTENTION, (2, 1, 128, 64), rc.RC_FLAG_CAUSAL),
     "mlp": (rc.RC_OP_GATED_MLP, (256, 256, 512), 0),
     # odd numbers of K tiles (3 for gate/up, 5 for down) for the ping-pong loop
     "mlp_odd": (rc.RC_OP_GATED_MLP, (256, 192, 320), 0),
+    # ragged token count: no tile_m divides T = 200, so every schedule ends
+    # in a partial M tile (both GEMMs)
+    "mlp_ragged": (rc.RC_OP_GATED_MLP, (200, 256, 512), 0),
     "moe": (rc.RC_OP_MOE, (256, 256, 8, 128, 2), 0),
     "conv": (rc.RC_OP_CONV2D, (2, 16, 12, 64, 64, 3, 3, 1), 0),
+    # 90 output pixels: a partial last M tile for every tile_m
+    "conv_ragged": (rc.RC_OP_CONV2D, (1, 10, 9, 64, 64, 3, 3, 1), 0),
 }
 
 _GEMM_BLOCK = ("tile_m", "tile_n", "tile_k", "waves_m", "waves_n", "mfma", "stages", "vec",
@@ -54,6 +62,19 @@ SCHEDULES = {
         "tile_m=64,tile_n=64,tile_k=32,waves_m=2,waves_n=2,vec=4,stages=2,unroll=2,layout=1",
         "tile_m=32,tile_n=64,tile_k=8,waves_m=2,waves_n=1,vec=1,stages=1,unroll=4,layout=1",
         "tile_m=64,tile_n=32,tile_k=4,waves_m=1,waves_n=2,vec=1,stages=2,unroll=1,layout=0",
+    ],
+    "gemm_ragged": [
+        "",
+        "tile_m=32,tile_n=32,tile_k=16,waves_m=1,waves_n=1,vec=4,stages=2,unroll=1,layout=0",
+        "tile_m=64,tile_n=64,tile_k=32,waves_m=2,waves_n=2,vec=4,stages=2,unroll=2,layout=1",
+        "tile_m=16,tile_n=16,tile_k=8,waves_m=1,waves_n=1,vec=1,stages=1,unroll=1,layout=0",
+        "tile_m=64,tile_n=32,tile_k=4,waves_m=1,waves_n=2,vec=1,stages=2,unroll=1,layout=0",
+    ],
+    "gemm_ragged_odd": [
+        "",
+        "tile_m=16,tile_n=16,tile_k=16,waves_m=1,waves_n=1,vec=1,stages=2,unroll=1,layout=0",
+        "tile_m=32,tile_n=64,tile_k=8,waves_m=2,waves_n=1,vec=1,stages=1,unroll=4,layout=0",
+        "tile_m=64,tile_n=32,tile_k=16,waves_m=2,waves_n=2,vec=1,stages=2,unroll=1,layout=1",
     ],
     "gemm_skinny": [
         "",
@@ -183,6 +204,10 @@ SCHEDULES = {
         _block("", 128, 64, 64, 2, 2, 16, 3, 8, 1, 1, 0, 2) + ",fuse=1",
     ],
 }
+
+# the ragged shapes run every schedule of their full-tile counterparts
+SCHEDULES["mlp_ragged"] = SCHEDULES["mlp"]
+SCHEDULES["conv_ragged"] = SCHEDULES["conv"]
 
 
 def small_op(key):

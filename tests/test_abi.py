@@ -91,8 +91,15 @@ def test_validate_rejects_with_reasons():
     assert "multiple of 16" in s.validate()
     s = g.schedule(tile_k=4, vec=4)
     assert "loads" in s.validate()
-    odd = rc.Op(rc.RC_OP_GEMM_F32, (96, 128, 128))
-    assert "does not divide M" in odd.schedule(tile_m=64).validate()
+    # tiles may cross the edges of the fp32 GEMM (96 = 1.5 tiles of 64), but a
+    # vector load may not cross the end of a row, and the streaming stage
+    # needs whole column tiles
+    odd = rc.Op(rc.RC_OP_GEMM_F32, (96, 100, 126))
+    assert odd.schedule(tile_m=64).validate() == ""
+    assert "rows of A" in odd.schedule(tile_k=16, vec=4).validate()
+    assert "rows of B" in rc.Op(rc.RC_OP_GEMM_F32, (96, 102, 128)).schedule(tile_k=16, vec=4).validate()
+    assert "does not divide N" in rc.Op(rc.RC_OP_GEMM_F32, (16, 100, 1024)).schedule(
+        tile_n=64, tile_k=16, vec=4, stages=3).validate()
     conv = W.workload_op("conv3x3_n2_64x64_c320_k320")
     assert "filter tap" in conv.schedule(tile_k=128).validate()
     mlp = W.workload_op("gated_mlp_t2048_h4096_i14336")
