@@ -34,7 +34,13 @@
 //                state (O, m, l) in the workspace and rc_attention_combine
 //                merges them, which shortens the longest workgroup's chain
 //                of dependent key tiles
-//   AB AH AS AD  batch, heads, sequence length, head dim
+//   AB AH AS AD  batch, heads, sequence length, head dim.  AS need not be a
+//                multiple of BM or BN: the last query tile's rows past AS
+//                read row AS - 1 of Q and are not stored; the last key
+//                tile's rows past AS load zeros (register staging) or
+//                repeat row AS - 1 (direct-to-LDS loads), and their scores
+//                are masked (the causal mask already hides them from every
+//                stored query)
 //   CAUSAL       top-left aligned causal mask (key j visible iff j <= i)
 //   SCALE_LOG2   log2(e) / sqrt(AD): scores are kept in log2 units
 //
@@ -58,7 +64,9 @@
 #define RING (STAGES == 5 || SPLITS == 2 ? 4 : 3)
 #define KB (BN / MF)
 #define DB (AD / MF)
-#define NQT (AS / BM)
+#define NQT ((AS + BM - 1) / BM)
+#define NKT ((AS + BN - 1) / BN)           // key tiles of the sequence
+#define RAGGED_S ((AS % BM) != 0 || (AS % BN) != 0)
 #define CPR (AD / 8)
 #define RPL ((16 / CPR) > 0 ? (16 / CPR) : 1)
 #define SWZ (CPR < 16 ? CPR : 16)
@@ -200,7 +208,9 @@ __device__ __forceinline__ float group_sum(float v) {
 }
 
 // Key tiles seen by query tile t, and the number of work items it is cut into.
-constexpr int tiles_of(int t) { return CAUSAL ? (t * BM + BM - 1) / BN + 1 : AS / BN; }
+constexpr int tiles_of(int t) {
+    return CAUSAL ? ((t * BM + BM - 1) / BN + 1 < NKT ? (t * BM + BM - 1) / BN + 1 : NKT) : NKT;
+}
 constexpr int chunks_of(int t) { return CHUNK > 0 ? (tiles_of(t) + CHUNK - 1) / CHUNK : 1; }
 constexpr int items_per_head() {
     int n = 0;
@@ -218,6 +228,10 @@ constexpr int order_tile(int k) {
     return ORDER == 1 ? NQT - 1 - k : ORDER == 2 ? (k < NQT / 2 ? NQT - 1 - k : k - NQT / 2) : k;
 }
 
+// Row of Q (or of K and V) that query (key) row q reads: rows past the
+// sequence read its last row, whose results are masked or never stored.
+__device__ __forceinline__ int qrow(int q) { return RAGGED_S && q >= AS ? AS - 1 : q; }
+
 // Exponential weight of a state with maximum x relative to the joint maximum
 // mt >= x; a state that saw no key (x = mt = -inf) gets weight 1 on its zero
 // sums instead of a NaN.
@@ -231,6 +245,7 @@ __device__ __forceinline__ void store_out(bf16_t *O, size_t base, int q0w, int l
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
         const int q = q0w + qb * MF + lane % MF;
+        if (RAGGED_S && q >= AS) continue;
         const float inv = 1.0f / l[qb];
         bf16_t *orow = O + base + (size_t)q * AD;
 #pragma unroll
@@ -318,12 +333,14 @@ void rc_attention(AttnArgs args) {
     // Each split's NW waves load that split's tiles.
     constexpr int WL = BN * AD / 512 / NW;            // wave-loads per wave and operand
     unsigned k_src[WL], v_src[WL];                    // byte offsets within a tile
+    int kv_row[RAGGED_S ? WL : 1];                    // key row of each offset
 #pragma unroll
     for (int j = 0; j < WL; ++j) {
         const int c = (rg * WL + j) * 64 + lane;
         const int row = c / CPR, pc = c % CPR;
         k_src[j] = 2u * (row * AD + ((pc ^ ((row / RPL) % SWZ)) << 3));
         v_src[j] = 2u * (row * AD + ((pc ^ VSWZ(row)) << 3));
+        if (RAGGED_S) kv_row[RAGGED_S ? j : 0] = row;
     }
     // LDS byte addresses of the ring buffers and this wave's first 1 KiB
     typedef __attribute__((address_space(3))) bf16_t *lds_p;
@@ -347,6 +364,21 @@ void rc_attention(AttnArgs args) {
     auto gload_lds = [&](int kt, int b) {
         const bf16_t *Kg = args.K + base + (size_t)(kt0 + kt) * BN * AD;
         const bf16_t *Vg = args.V + base + (size_t)(kt0 + kt) * BN * AD;
+        const int kvalid = AS - (kt0 + kt) * BN;     // wave-uniform
+        if (RAGGED_S && kvalid < BN) {
+            // last, partial tile: rows past the sequence fetch its last row
+#pragma unroll
+            for (int j = 0; j < WL; ++j) {
+                const unsigned back = 2u * AD * (unsigned)max(kv_row[RAGGED_S ? j : 0] - (kvalid - 1), 0);
+                dma(Kg, k_src[j] - back, KA[b] + j * 1024u);
+            }
+#pragma unroll
+            for (int j = 0; j < WL; ++j) {
+                const unsigned back = 2u * AD * (unsigned)max(kv_row[RAGGED_S ? j : 0] - (kvalid - 1), 0);
+                dma(Vg, v_src[j] - back, VA[b] + j * 1024u);
+            }
+            return;
+        }
 #pragma unroll
         for (int j = 0; j < WL; ++j) dma(Kg, k_src[j], KA[b] + j * 1024u);
 #pragma unroll
@@ -367,7 +399,7 @@ void rc_attention(AttnArgs args) {
     for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
         for (int ks = 0; ks < AD / KSTEP; ++ks)
-            qf[qb][ks] = *(const bf16x8 *)(args.Q + base + (size_t)(q0w + qb * MF + lane % MF) * AD +
+            qf[qb][ks] = *(const bf16x8 *)(args.Q + base + (size_t)qrow(q0w + qb * MF + lane % MF) * AD +
                                            ks * KSTEP + 8 * (lane / MF));
 #if STAGES >= 4
     // Consume Q here so that the compiler's wait for it (a full vmcnt drain,
@@ -403,10 +435,13 @@ void rc_attention(AttnArgs args) {
     auto gload = [&](int kt) {
         const bf16_t *Kg = args.K + base + (size_t)(kt0 + kt) * BN * AD;
         const bf16_t *Vg = args.V + base + (size_t)(kt0 + kt) * BN * AD;
+        // keys of this tile that lie inside the sequence (rows past it load zeros)
+        const int kvalid = AS - (kt0 + kt) * BN;
 #pragma unroll
         for (int i = 0; i < K_LOADS; ++i) {
             int idx = tids + i * NTS;
-            if ((BN * AD / VEC) % NTS == 0 || idx < BN * AD / VEC) rk[i] = *(const vecT *)(Kg + (size_t)idx * VEC);
+            if ((BN * AD / VEC) % NTS == 0 || idx < BN * AD / VEC)
+                rk[i] = (!RAGGED_S || idx / (AD / VEC) < kvalid) ? *(const vecT *)(Kg + (size_t)idx * VEC) : vecT{};
         }
 #pragma unroll
         for (int i = 0; i < V_BLKS; ++i) {
@@ -414,7 +449,9 @@ void rc_attention(AttnArgs args) {
             if ((BN * AD / 32) % NTS == 0 || blk < BN * AD / 32) {
                 int kr = (blk % (BN / 4)) * 4, dc = (blk / (BN / 4)) * 8;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) rv[i][j] = *(const u32x4 *)(Vg + (size_t)(kr + j) * AD + dc);
+                for (int j = 0; j < 4; ++j)
+                    rv[i][j] = (!RAGGED_S || kr + j < kvalid) ? *(const u32x4 *)(Vg + (size_t)(kr + j) * AD + dc)
+                                                             : u32x4{0u, 0u, 0u, 0u};
             }
         }
     };
@@ -555,6 +592,9 @@ void rc_attention(AttnArgs args) {
 #if CAUSAL
         // only a tile that crosses this wave's diagonal needs the mask
         const bool diag = (kt0 + kt) * BN + BN - 1 > q0w;
+#else
+        // only the last tile of a ragged sequence holds keys past its end
+        const bool tail = RAGGED_S && (kt0 + kt) * BN + BN > AS;
 #endif
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
@@ -567,6 +607,14 @@ void rc_attention(AttnArgs args) {
 #pragma unroll
                     for (int r = 0; r < ACCN; ++r)
                         if ((kt0 + kt) * BN + kb * MF + key_of(r, lane) > q) sc[qb][kb][r] = -__builtin_inff();
+            }
+#else
+            if (tail) {
+#pragma unroll
+                for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                    for (int r = 0; r < ACCN; ++r)
+                        if ((kt0 + kt) * BN + kb * MF + key_of(r, lane) >= AS) sc[qb][kb][r] = -__builtin_inff();
             }
 #endif
 #pragma unroll
@@ -753,25 +801,23 @@ void rc_attention(AttnArgs args) {
 #if CAUSAL
         return (kt0 + kt) * BN + BN - 1 > q0w;
 #else
-        (void)kt;
-        return false;
+        return RAGGED_S && (kt0 + kt) * BN + BN > AS;
 #endif
     };
     auto mask = [&](int kt, accT (&sc)[QB][KB]) {
-#if CAUSAL
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) {
+#if CAUSAL
             const int q = q0w + qb * MF + lane % MF;
+#else
+            const int q = AS - 1;      // keys past the sequence
+#endif
 #pragma unroll
             for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
                 for (int r = 0; r < ACCN; ++r)
                     if ((kt0 + kt) * BN + kb * MF + key_of(r, lane) > q) sc[qb][kb][r] = -__builtin_inff();
         }
-#else
-        (void)kt;
-        (void)sc;
-#endif
     };
     // row maximum of a tile in log2 units, identical on every lane of a query
     auto tile_max = [&](const accT (&sc)[QB][KB], float (&mx)[QB]) {

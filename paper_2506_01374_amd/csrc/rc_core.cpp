@@ -330,8 +330,11 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
             if (rpw % mf) return fmt("rows per wave %d is not a multiple of the %dx%d MFMA", rpw, mf, mf);
             if (rpw / mf > 2) return fmt("rows per wave %d exceeds two MFMA blocks", rpw);
             if (bn % 32) return fmt("block_n %d is not a multiple of 32", bn);
-            if (S % bm) return fmt("block_m %d does not divide S = %lld", bm, (long long)S);
-            if (S % bn) return fmt("block_n %d does not divide S = %lld", bn, (long long)S);
+            // the sequence need not fill the last query or key tile (rows
+            // past it are clamped on load, masked and not stored), but a
+            // block twice the sequence adds only empty work
+            if (bm > S && bm / 2 >= S) return fmt("block_m %d: block_m %d already covers S = %lld", bm, bm / 2, (long long)S);
+            if (bn > S && bn / 2 >= S) return fmt("block_n %d: block_n %d already covers S = %lld", bn, bn / 2, (long long)S);
             // the K tile's LDS swizzle XORs 16-byte chunk indices, so a row
             // must hold a power-of-two number of chunks
             if (Dh != 32 && Dh != 64 && Dh != 128 && Dh != 256)
@@ -371,9 +374,10 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
                     return fmt("%lld workgroups of %lld B LDS do not fit a CU", (long long)wgs, (long long)lds);
             }
             int ch = kv(d, s, "chunk");
-            if (ch > 0 && ch >= S / bn)
-                return fmt("chunk of %d key tiles covers all %lld key tiles (same as chunk 0)", ch, (long long)(S / bn));
-            if (kv(d, s, "order") == 2 && (S / bm) % 2)
+            if (ch > 0 && ch >= (S + bn - 1) / bn)
+                return fmt("chunk of %d key tiles covers all %lld key tiles (same as chunk 0)", ch,
+                           (long long)((S + bn - 1) / bn));
+            if (kv(d, s, "order") == 2 && ((S + bm - 1) / bm) % 2)
                 return "paired tile order needs an even number of query tiles";
             return "";
         }

@@ -450,9 +450,10 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             bool causal = (d->flags & RC_FLAG_CAUSAL) != 0;
             // work items: query tile t sees tiles(t) key tiles, cut into
             // chunks of at most `chunk` tiles
-            long nqt = S / bm, items = 0, maxch = 1;
+            // (the last query and key tiles may be partial)
+            long nqt = (S + bm - 1) / bm, nkt = (S + bn - 1) / bn, items = 0, maxch = 1;
             for (long t = 0; t < nqt; ++t) {
-                long tiles = causal ? (t * bm + bm - 1) / bn + 1 : S / bn;
+                long tiles = causal ? std::min(nkt, (t * bm + bm - 1) / bn + 1) : nkt;
                 long nc = chunk > 0 ? (tiles + chunk - 1) / chunk : 1;
                 items += nc;
                 maxch = std::max(maxch, nc);

@@ -24,6 +24,11 @@ SMALL = {
     "attn_causal": (rc.RC_OP_ATTENTION, (1, 2, 256, 128), rc.RC_FLAG_CAUSAL),
     "attn_full": (rc.RC_OP_ATTENTION, (1, 2, 256, 128), 0),
     "attn_d64": (rc.RC_OP_ATTENTION, (2, 1, 128, 64), rc.RC_FLAG_CAUSAL),
+    # ragged sequences: no block divides S, so the last query and key tiles
+    # are partial
+    "attn_ragged_causal": (rc.RC_OP_ATTENTION, (1, 2, 200, 128), rc.RC_FLAG_CAUSAL),
+    "attn_ragged_full": (rc.RC_OP_ATTENTION, (1, 2, 200, 128), 0),
+    "attn_ragged_d64": (rc.RC_OP_ATTENTION, (2, 1, 77, 64), rc.RC_FLAG_CAUSAL),
     "mlp": (rc.RC_OP_GATED_MLP, (256, 256, 512), 0),
     # odd numbers of K tiles (3 for gate/up, 5 for down) for the ping-pong loop
     "mlp_odd": (rc.RC_OP_GATED_MLP, (256, 192, 320), 0),
@@ -205,9 +210,21 @@ SCHEDULES = {
     ],
 }
 
-# the ragged shapes run every schedule of their full-tile counterparts
+# the ragged shapes run every schedule of their full-tile counterparts that
+# is legal for them (the paired order needs an even number of query tiles)
 SCHEDULES["mlp_ragged"] = SCHEDULES["mlp"]
 SCHEDULES["conv_ragged"] = SCHEDULES["conv"]
+
+
+def _legal_for(key, scheds):
+    kind, dims, flags = SMALL[key]
+    op = rc.Op(kind, dims, flags)
+    return [t for t in scheds if op.from_string(t).validate() == ""]
+
+
+SCHEDULES["attn_ragged_causal"] = _legal_for("attn_ragged_causal", SCHEDULES["attn_causal"])
+SCHEDULES["attn_ragged_full"] = _legal_for("attn_ragged_full", SCHEDULES["attn_full"])
+SCHEDULES["attn_ragged_d64"] = _legal_for("attn_ragged_d64", SCHEDULES["attn_d64"])
 
 
 def small_op(key):
