@@ -18,6 +18,8 @@ RC_OK = 0
 STATUS = {0: "RC_OK", 1: "RC_ERR_INVALID_ARGUMENT", 2: "RC_ERR_ILLEGAL_SCHEDULE",
           3: "RC_ERR_UNSUPPORTED", 4: "RC_ERR_COMPILE", 5: "RC_ERR_HIP",
           6: "RC_ERR_OUT_OF_MEMORY", 7: "RC_ERR_MISALIGNED", 8: "RC_ERR_BUDGET"}
+(RC_ERR_INVALID_ARGUMENT, RC_ERR_ILLEGAL_SCHEDULE, RC_ERR_UNSUPPORTED, RC_ERR_COMPILE, RC_ERR_HIP,
+ RC_ERR_OUT_OF_MEMORY, RC_ERR_MISALIGNED, RC_ERR_BUDGET) = range(1, 9)
 
 RC_OP_GEMM_F32, RC_OP_ATTENTION, RC_OP_GATED_MLP, RC_OP_MOE, RC_OP_CONV2D = 1, 2, 3, 4, 5
 RC_FLAG_CAUSAL = 1

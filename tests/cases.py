@@ -39,6 +39,14 @@ SMALL = {
     "conv": (rc.RC_OP_CONV2D, (2, 16, 12, 64, 64, 3, 3, 1), 0),
     # 90 output pixels: a partial last M tile for every tile_m
     "conv_ragged": (rc.RC_OP_CONV2D, (1, 10, 9, 64, 64, 3, 3, 1), 0),
+    # degenerate sizes: one row, one token, one key, one output pixel
+    "gemm_one": (rc.RC_OP_GEMM_F32, (1, 1, 1), 0),
+    "gemm_row": (rc.RC_OP_GEMM_F32, (1, 300, 77), 0),
+    "attn_one_causal": (rc.RC_OP_ATTENTION, (1, 2, 1, 128), rc.RC_FLAG_CAUSAL),
+    "attn_one_full": (rc.RC_OP_ATTENTION, (1, 2, 1, 128), 0),
+    "mlp_one": (rc.RC_OP_GATED_MLP, (1, 256, 512), 0),
+    "moe_one": (rc.RC_OP_MOE, (1, 256, 8, 128, 2), 0),
+    "conv_one": (rc.RC_OP_CONV2D, (1, 1, 1, 64, 64, 3, 3, 1), 0),
 }
 
 _GEMM_BLOCK = ("tile_m", "tile_n", "tile_k", "waves_m", "waves_n", "mfma", "stages", "vec",
@@ -226,6 +234,38 @@ SCHEDULES["attn_ragged_causal"] = _legal_for("attn_ragged_causal", SCHEDULES["at
 SCHEDULES["attn_ragged_full"] = _legal_for("attn_ragged_full", SCHEDULES["attn_full"])
 SCHEDULES["attn_ragged_d64"] = _legal_for("attn_ragged_d64", SCHEDULES["attn_d64"])
 
+# degenerate sizes: the smallest tiles, on every staging path they admit
+_ONE_ATTN = [
+    "",
+    "block_m=16,block_n=32,waves=1,mfma=16,stages=1,vec=4,unroll=1,order=0",
+    "block_m=16,block_n=32,waves=1,mfma=16,stages=3,vec=8,unroll=1,order=0",
+    "block_m=16,block_n=32,waves=1,mfma=16,stages=4,vec=8,unroll=1,order=0,occ=1,splits=2",
+]
+_ONE_MLP = [
+    "",
+    _block("up.", 16, 128, 64, 1, 2, 16, 4, 8, 1, 1, 1) + "," +
+    _block("down.", 16, 128, 64, 1, 2, 16, 4, 8, 1, 1, 1) + ",fuse=1",
+    _block("up.", 16, 64, 64, 1, 2, 16, 5, 8, 1, 1, 0) + "," +
+    _block("down.", 16, 64, 64, 1, 2, 16, 3, 8, 1, 1, 0) + ",fuse=0",
+]
+SCHEDULES["gemm_one"] = [
+    "", "tile_m=16,tile_n=16,tile_k=4,waves_m=1,waves_n=1,vec=1,stages=2,unroll=1,layout=1"]
+SCHEDULES["gemm_row"] = [
+    "",
+    "tile_m=16,tile_n=64,tile_k=16,waves_m=1,waves_n=2,vec=1,stages=2,unroll=1,layout=0",
+    "tile_m=16,tile_n=32,tile_k=8,waves_m=1,waves_n=1,vec=1,stages=1,unroll=2,layout=1",
+    "tile_m=16,tile_n=64,tile_k=32,waves_m=1,waves_n=1,vec=1,stages=2,unroll=1,layout=1",
+]
+SCHEDULES["attn_one_causal"] = _legal_for("attn_one_causal", _ONE_ATTN)
+SCHEDULES["attn_one_full"] = _legal_for("attn_one_full", _ONE_ATTN)
+SCHEDULES["mlp_one"] = _ONE_MLP
+SCHEDULES["moe_one"] = _ONE_MLP
+SCHEDULES["conv_one"] = [
+    "",
+    _block("", 16, 64, 64, 1, 2, 16, 5, 8, 1, 1, 1) + ",fuse=1",
+    _block("", 16, 64, 32, 1, 1, 16, 2, 8, 1, 0, 0) + ",fuse=0",
+]
+
 
 def small_op(key):
     kind, dims, flags = SMALL[key]
@@ -255,6 +295,16 @@ FULL_ALT = [
 ]
 
 
+# Benchmark-sized operators whose row count no tile divides, run in the
+# benchmark's tuned schedule (every tile but the last is full).
+RAGGED_FULL = [
+    ("attention_causal_b1_h32_s1024_d128", (1, 32, 1000, 128), rc.RC_FLAG_CAUSAL),
+    ("attention_noncausal_b1_h24_s4096_d128", (1, 24, 4000, 128), 0),
+    ("gated_mlp_t2048_h4096_i14336", (2000, 4096, 14336), 0),
+    ("conv3x3_n2_64x64_c320_k320", (2, 63, 63, 320, 320, 3, 3, 1), 0),
+    ("gemm_f32_128", (100, 120, 132), 0),
+]
+
 
 def all_compile_jobs():
     """(op, [schedules]) pairs for ahead-of-time compilation."""
@@ -268,4 +318,7 @@ def all_compile_jobs():
     for name, s in FULL_ALT:
         op = W.workload_op(name)
         jobs.append((op, [op.from_string(s)]))
+    for name, dims, flags in RAGGED_FULL:
+        op = rc.Op(W.workload_op(name).kind, dims, flags)
+        jobs.append((op, [op.from_string(TUNED[name])]))
     return jobs

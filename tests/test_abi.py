@@ -201,3 +201,29 @@ def test_precompile_reports_illegal_and_compiles_legal(tmp_path):
         assert any(f.endswith(".hsaco") for f in os.listdir(tmp_path))
     finally:
         rc.set_cache_dir(os.path.join(ROOT, "paper_2506_01374_amd", "jit_cache"))
+
+
+@pytest.mark.parametrize("kind,dims", [
+    (rc.RC_OP_GEMM_F32, (0, 16, 16)),
+    (rc.RC_OP_GEMM_F32, (16, 16, 0)),
+    (rc.RC_OP_ATTENTION, (1, 2, 0, 128)),
+    (rc.RC_OP_GATED_MLP, (0, 256, 512)),
+    (rc.RC_OP_MOE, (0, 256, 8, 128, 2)),
+    (rc.RC_OP_CONV2D, (1, 0, 4, 64, 64, 3, 3, 1)),
+])
+def test_empty_operators_are_rejected_when_described(kind, dims):
+    # An operator with a zero extent has nothing to launch: the descriptor is
+    # refused with RC_ERR_INVALID_ARGUMENT before any plan exists.
+    with pytest.raises(rc.RCError) as e:
+        rc.Op(kind, dims)
+    assert e.value.status == rc.RC_ERR_INVALID_ARGUMENT
+    assert "positive" in str(e.value)
+
+
+def test_convolution_with_no_output_pixel_has_no_schedule():
+    # a 3x3 filter over a 1x1 image without padding leaves no output pixel:
+    # no schedule is legal, so not even P0 exists
+    op = rc.Op(rc.RC_OP_CONV2D, (1, 1, 1, 64, 64, 3, 3, 0))
+    with pytest.raises(rc.RCError) as e:
+        op.default()
+    assert e.value.status == rc.RC_ERR_UNSUPPORTED and "empty output" in str(e.value)

@@ -219,6 +219,21 @@ def test_full_size_alternative_paths(name, sched_text):
     assert np.all(np.isfinite(y))
 
 
+@pytest.mark.parametrize("name,dims,flags", cases.RAGGED_FULL,
+                         ids=[f"{n.split('_')[0]}-{d[2] if len(d) > 3 else d[0]}" for n, d, _ in cases.RAGGED_FULL])
+def test_ragged_near_full_size(name, dims, flags):
+    kind = W.workload_op(name).kind
+    op = rc.Op(kind, dims, flags)
+    sched = op.from_string(cases.TUNED[name])
+    assert sched.validate() == "", sched.validate()
+    host = W.host_inputs(op, seed=3)
+    y, _ = run(op, sched, host)
+    n = {rc.RC_OP_GEMM_F32: 0, rc.RC_OP_ATTENTION: 96, rc.RC_OP_GATED_MLP: 12, rc.RC_OP_CONV2D: 64}[kind]
+    rows = None if kind == rc.RC_OP_GEMM_F32 else _sample_rows(op, n, seed=11)
+    assert_parity(op, y, host, rows=rows, label=f"{name} {dims}")
+    assert np.all(np.isfinite(y))
+
+
 @pytest.mark.parametrize("key", ["attn_causal", "mlp", "moe"])
 def test_graph_replay_matches_eager(key):
     # The benchmark replays captured launches.  Capture one execution on a
