@@ -642,7 +642,9 @@ void rc_attention(AttnArgs args) {
                     sc[qb][kb][r] = p;
                     ps += p;
                 }
-            l[qb] += group_sum(ps);
+            // per-lane partial row sums; the lanes of a query apply the same
+            // rescale factors, so they are added across lanes once, at the end
+            l[qb] += ps;
         }
         // O^T += V^T P^T, KSTEP keys per MFMA; each V^T fragment is read once
 #pragma unroll
@@ -1050,6 +1052,11 @@ void rc_attention(AttnArgs args) {
         if (nk < n_kt) swrite((it + 1) & 1);
         __syncthreads();
     }
+#endif
+
+#if STAGES != 5
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) l[qb] = group_sum(l[qb]);
 #endif
 
 #if SPLITS > 1
