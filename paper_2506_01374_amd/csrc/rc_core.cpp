@@ -151,6 +151,18 @@ int32_t kv(const rc_op_desc *d, const rc_schedule *s, const char *name) {
     return i < 0 ? -1 : s->knob[i];
 }
 
+// A tile value v of knob `name` over an extent it need not fill is redundant
+// when half of it is also an allowed value and still covers the extent: the
+// larger tile only adds empty work.
+static bool redundant_tile(const rc_op_desc *d, const char *name, int v, int64_t extent) {
+    if (v <= extent || v / 2 < extent) return false;
+    const int i = knob_index(d->kind, name);
+    if (i < 0) return false;
+    for (int32_t a : knobs_for(d->kind)[i].values)
+        if (a == v / 2) return true;
+    return false;
+}
+
 static std::string fmt(const char *f, ...) {
     char buf[256];
     va_list ap;
@@ -183,7 +195,7 @@ static std::string check_bf16_block(const rc_op_desc *d, const rc_schedule *s,
     if (tk % 32) return fmt("%s: tile_k %d is not a multiple of 32", tag, tk);
     // rows need not fill the last M tile (predicated, for dense and ragged
     // rows alike); a tile twice the rows it covers adds only empty work
-    if (M > 0 && tm > M && tm / 2 >= M)
+    if (M > 0 && redundant_tile(d, names[0], tm, M))
         return fmt("%s: tile_m %d: tile_m %d already covers M = %lld", tag, tm, tm / 2, (long long)M);
     if (N % tn) return fmt("%s: tile_n %d does not divide N = %lld", tag, tn, (long long)N);
     if (K % tk) return fmt("%s: tile_k %d does not divide K = %lld", tag, tk, (long long)K);
@@ -304,9 +316,9 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
             // predicated stores), but a tile twice the extent it covers adds
             // only empty work (the halved tile covers it too); a vector load
             // must not cross a row end
-            if (tm > M && tm / 2 >= M) return fmt("tile_m %d: tile_m %d already covers M = %lld", tm, tm / 2, (long long)M);
-            if (tn > N && tn / 2 >= N) return fmt("tile_n %d: tile_n %d already covers N = %lld", tn, tn / 2, (long long)N);
-            if (tk > K && tk / 2 >= K) return fmt("tile_k %d: tile_k %d already covers K = %lld", tk, tk / 2, (long long)K);
+            if (redundant_tile(d, "tile_m", tm, M)) return fmt("tile_m %d: tile_m %d already covers M = %lld", tm, tm / 2, (long long)M);
+            if (redundant_tile(d, "tile_n", tn, N)) return fmt("tile_n %d: tile_n %d already covers N = %lld", tn, tn / 2, (long long)N);
+            if (redundant_tile(d, "tile_k", tk, K)) return fmt("tile_k %d: tile_k %d already covers K = %lld", tk, tk / 2, (long long)K);
             if (K % vec) return fmt("vec %d does not divide the rows of A (K = %lld)", vec, (long long)K);
             if (lay == 0 && N % vec) return fmt("vec %d does not divide the rows of B (N = %lld)", vec, (long long)N);
             if ((tm * tk) % (vec * nt))
@@ -333,8 +345,8 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
             // the sequence need not fill the last query or key tile (rows
             // past it are clamped on load, masked and not stored), but a
             // block twice the sequence adds only empty work
-            if (bm > S && bm / 2 >= S) return fmt("block_m %d: block_m %d already covers S = %lld", bm, bm / 2, (long long)S);
-            if (bn > S && bn / 2 >= S) return fmt("block_n %d: block_n %d already covers S = %lld", bn, bn / 2, (long long)S);
+            if (redundant_tile(d, "block_m", bm, S)) return fmt("block_m %d: block_m %d already covers S = %lld", bm, bm / 2, (long long)S);
+            if (redundant_tile(d, "block_n", bn, S)) return fmt("block_n %d: block_n %d already covers S = %lld", bn, bn / 2, (long long)S);
             // the K tile's LDS swizzle XORs 16-byte chunk indices, so a row
             // must hold a power-of-two number of chunks
             if (Dh != 32 && Dh != 64 && Dh != 128 && Dh != 256)
