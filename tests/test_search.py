@@ -345,3 +345,18 @@ def test_surrogate_replay_spends_nothing_outside_the_measured_space():
     invalid = sum(1 for h in srch.history() if not h["valid"])
     assert len(looked) == sur.measured + spills
     assert sur.calls == sur.measured + sur.predicted + invalid and invalid > spills
+
+
+def test_measured_gemm_table_is_the_whole_space_and_its_optimum_is_tuned():
+    # The committed fp32 GEMM 128^3 table holds every legal schedule once (the
+    # enumeration of the space), and its cold optimum is the tuned schedule.
+    import json
+    from paper_2506_01374_amd import workloads as W
+    from paper_2506_01374_amd.tune import TableEvaluator, legal_space
+    op = W.workload_op("gemm_f32_128")
+    tab = TableEvaluator(os.path.join(HERE, "..", "results", "gemm_f32_128.space.tsv"), op)
+    assert set(tab.table) == {str(s) for s in legal_space(op)}
+    valid = [r for r in tab.table.values() if r["valid"]]
+    assert len(valid) == 1714
+    tuned = json.load(open(os.path.join(HERE, "..", "paper_2506_01374_amd", "tuned.json")))["gemm_f32_128"]
+    assert max(valid, key=lambda r: r["reward"])["schedule"] == str(op.from_string(tuned))
