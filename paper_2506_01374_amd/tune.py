@@ -225,7 +225,9 @@ class SurrogateEvaluator:
     rollout reward and no sample is spent.  Only measurements are samples:
     `curve` is the best measured reward after each of them.  A schedule the
     inner evaluator places outside its space (a replayed table's `contains`)
-    is invalid at no cost, as it is without the surrogate."""
+    is invalid at no cost, as it is without the surrogate.  A schedule
+    measured before (by an earlier tree of the same run) returns its
+    measurement again at no cost."""
 
     def __init__(self, op: rc.Op, inner, seed: int, warm: int = 16, refit: int = 8,
                  margin: float = 0.9, explore: float = 0.05):
@@ -240,6 +242,7 @@ class SurrogateEvaluator:
         self.measured = 0
         self.predicted = 0
         self.calls = 0
+        self.known: Dict[str, Optional[float]] = {}
         self.best = 0.0
         self.best_text: Optional[str] = None
         self.curve: List[float] = []
@@ -258,6 +261,7 @@ class SurrogateEvaluator:
     def _measure(self, sched: rc.Schedule) -> Optional[float]:
         r = self.inner.measure(sched)
         reward = r["reward"] if r.get("valid") else None
+        self.known[str(sched)] = reward
         self.X.append(self.features(sched))
         self.y.append(reward if reward is not None else 0.0)   # invalid: learn it as worthless
         if reward is not None:
@@ -272,6 +276,8 @@ class SurrogateEvaluator:
         contains = getattr(self.inner, "contains", None)
         if contains is not None and not contains(sched):
             return None
+        if str(sched) in self.known:
+            return self.known[str(sched)]
         if len(self.y) < self.warm:
             return self._measure(sched)
         if self.model is None or len(self.y) - self.fitted_at >= self.refit:
@@ -301,17 +307,27 @@ def run_search(op, evaluator, policy: str, budget: int, seed: int, horizon=12, b
 
     # with a surrogate only measurements count, so the driver's own budget
     # (which counts every rollout reward) is a loose cap
-    srch = rc.Search(op, ev, policy=POLICIES[policy], budget=budget * (40 if sur else 1), horizon=horizon,
-                     branching=branching, c=c, seed=seed, propose=prop)
+    def new_tree(k):
+        return rc.Search(op, ev, policy=POLICIES[policy], budget=budget * (40 if sur else 1), horizon=horizon,
+                         branching=branching, c=c, seed=seed + 7919 * k, propose=prop)
+    srch = new_tree(0)
+    trees = 1
     if sur is None:
         srch.run()
     else:
-        # stop when the measurements are spent, or when the tree has stopped
-        # reaching schedules it has not scored (every rollout a repeat)
-        last, idle = sur.calls, 0
-        while sur.measured < budget and idle < 20 * budget and not srch.step():
-            idle = 0 if sur.calls != last else idle + 1
-            last = sur.calls
+        # With free rollouts a tree of at most B children per node and depth T
+        # runs out of unscored schedules long before the measurements are
+        # spent: when 20 x budget rollouts bring nothing new, a fresh tree
+        # (another seed; the surrogate and the measurements carry over) takes
+        # over, up to 16 trees.
+        while sur.measured < budget and trees <= 16:
+            last, idle = sur.calls, 0
+            while sur.measured < budget and idle < 20 * budget and not srch.step():
+                idle = 0 if sur.calls != last else idle + 1
+                last = sur.calls
+            if sur.measured < budget and trees < 16:
+                srch = new_tree(trees)
+            trees += 1
     hist = srch.history()
     if sur is None:
         try:
@@ -325,7 +341,7 @@ def run_search(op, evaluator, policy: str, budget: int, seed: int, horizon=12, b
         curve = sur.curve
     # samples to reach the run's best (within 1%)
     to_best = next((i + 1 for i, v in enumerate(curve) if v >= 0.99 * reward), None) if curve else None
-    return {"policy": policy, "proposer": proposer, "surrogate": surrogate,
+    return {"policy": policy, "proposer": proposer, "surrogate": surrogate, "trees": min(trees, 16),
             "fallbacks": srch.fallbacks() if prop else None,
             "seed": seed, "budget": budget, "valid": len(curve) if sur else sum(h["valid"] for h in hist),
             "invalid": sum(not h["valid"] for h in hist), "predicted": sur.predicted if sur else 0,
