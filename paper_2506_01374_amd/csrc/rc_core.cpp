@@ -44,7 +44,8 @@ static std::vector<KnobDef> gemm_f32_knobs() {
 // One bf16 GEMM stage's knobs, names prefixed ("" / "up." / "down.").
 static void add_gemm_block(std::vector<KnobDef> &v, const char *const names[12],
                            std::vector<int32_t> tile_n_vals, std::vector<int32_t> tile_k_vals) {
-    v.push_back({names[0], "TileSize", {16, 32, 64, 128, 256}, 16});
+    // 96 and 192 rows fit ragged row groups (MoE experts) of ~3 x 64 rows
+    v.push_back({names[0], "TileSize", {16, 32, 64, 96, 128, 192, 256}, 16});
     v.push_back({names[1], "TileSize", tile_n_vals, 16});
     v.push_back({names[2], "TileSize", tile_k_vals, 32});
     v.push_back({names[3], "Parallel", {1, 2, 4}, 1});

@@ -173,6 +173,8 @@ SCHEDULES = {
         _block("down.", 128, 128, 64, 2, 2, 16, 4, 8, 1, 1, 1) + ",fuse=1",
         _block("up.", 64, 128, 32, 2, 2, 32, 4, 8, 1, 1, 0) + "," +
         _block("down.", 256, 64, 32, 4, 1, 16, 4, 8, 1, 1, 0) + ",fuse=0",
+        _block("up.", 192, 128, 64, 2, 4, 16, 3, 8, 1, 1, 1, 2) + "," +
+        _block("down.", 192, 128, 64, 2, 4, 16, 4, 8, 1, 1, 1, 2) + ",fuse=1",
         # ping-pong staging
         _block("up.", 256, 128, 32, 4, 2, 32, 6, 8, 1, 1, 1, 2) + "," +
         _block("down.", 128, 256, 64, 2, 4, 32, 6, 8, 1, 1, 1, 2) + ",fuse=1",
@@ -201,6 +203,12 @@ SCHEDULES = {
         _block("down.", 128, 128, 64, 2, 2, 16, 4, 8, 1, 1, 1) + ",fuse=1",
         _block("up.", 32, 128, 64, 1, 2, 16, 4, 8, 1, 1, 0) + "," +
         _block("down.", 64, 64, 64, 2, 1, 32, 4, 8, 1, 1, 0) + ",fuse=0",
+        # 192-row tiles (three 64-row bands) on the register-staged and the
+        # direct-to-LDS paths
+        _block("up.", 192, 128, 64, 2, 4, 16, 3, 8, 1, 1, 1, 2) + "," +
+        _block("down.", 192, 128, 64, 2, 4, 16, 4, 8, 1, 1, 1, 2) + ",fuse=1",
+        _block("up.", 192, 64, 64, 4, 2, 16, 4, 8, 1, 1, 0) + "," +
+        _block("down.", 192, 64, 32, 4, 1, 16, 2, 8, 1, 1, 0) + ",fuse=0",
         # ping-pong staging over gathered (gate/up) and grouped (down) rows
         _block("up.", 128, 128, 64, 4, 2, 16, 6, 8, 1, 1, 1, 2) + "," +
         _block("down.", 128, 256, 64, 2, 4, 16, 6, 8, 1, 1, 1, 2) + ",fuse=1",
