@@ -133,10 +133,12 @@ class GpuEvaluator:
 class TableEvaluator:
     """Measured samples replayed from a table: a previous run's JSONL, or a
     TSV of one sub-space (comment lines, a '# fixed: knob=v,...' line, a
-    header of the varying knobs and 'us', then one row per schedule with its
-    median microseconds or the reason it was rejected)."""
+    header of the varying knobs and one or more timing columns named 'us' or
+    '*_us', then one row per schedule with its median microseconds or the
+    reason it was rejected).  `column` picks the timing column (default: the
+    last)."""
 
-    def __init__(self, path: str, op: Optional[rc.Op] = None):
+    def __init__(self, path: str, op: Optional[rc.Op] = None, column: Optional[str] = None):
         self.table: Dict[str, dict] = {}
         if path.endswith(".tsv"):
             if op is None:
@@ -150,14 +152,16 @@ class TableEvaluator:
                     continue
                 elif header is None:
                     header = line.split("\t")
+                    nk = sum(1 for h in header if not (h == "us" or h.endswith("_us")))
+                    col = header.index(column) if column else len(header) - 1
                 else:
                     vals = line.split("\t")
-                    text = ",".join([fixed] + [f"{k}={v}" for k, v in zip(header[:-1], vals[:-1])])
+                    text = ",".join([fixed] + [f"{k}={v}" for k, v in zip(header[:nk], vals[:nk])])
                     key = str(op.from_string(text))
-                    if vals[-1] in ("spill", "error"):
-                        self.table[key] = {"schedule": key, "valid": False, "error": vals[-1]}
+                    if vals[col] in ("spill", "error"):
+                        self.table[key] = {"schedule": key, "valid": False, "error": vals[col]}
                     else:
-                        ms = float(vals[-1]) * 1e-3
+                        ms = float(vals[col]) * 1e-3
                         self.table[key] = {"schedule": key, "valid": True, "ms": ms,
                                            "reward": reward_of(op, ms)}
             return
@@ -379,7 +383,8 @@ def main(argv=None):
     ap.add_argument("--walks", type=int, default=0, help="list N random-walk schedules")
     ap.add_argument("--precompile", action="store_true", help="compile the listed schedules (CPU)")
     ap.add_argument("--list-file", default=None, help="measure the schedules in this file (policy list)")
-    ap.add_argument("--replay", default=None, help="evaluate against a measured JSONL table")
+    ap.add_argument("--replay", default=None, help="evaluate against a measured table (JSONL or TSV)")
+    ap.add_argument("--column", default=None, help="timing column of a TSV table (default: the last)")
     ap.add_argument("--threads", type=int, default=os.cpu_count() or 8)
     ap.add_argument("--cache-dir", default=os.path.join(HERE, "jit_cache"))
     args = ap.parse_args(argv)
@@ -409,7 +414,7 @@ def main(argv=None):
     tag = args.policy + (f"+{args.proposer}" if args.proposer else "") + ("+surrogate" if args.surrogate else "")
     log = open(os.path.join(args.out, f"{args.workload}.{tag}.jsonl"), "a")
     if args.replay:
-        evaluator = TableEvaluator(args.replay, op)
+        evaluator = TableEvaluator(args.replay, op, args.column)
     else:
         evaluator = GpuEvaluator(op, repeat=args.repeat, log=log)
 

@@ -360,3 +360,25 @@ def test_measured_gemm_table_is_the_whole_space_and_its_optimum_is_tuned():
     assert len(valid) == 1714
     tuned = json.load(open(os.path.join(HERE, "..", "paper_2506_01374_amd", "tuned.json")))["gemm_f32_128"]
     assert max(valid, key=lambda r: r["reward"])["schedule"] == str(op.from_string(tuned))
+
+
+def test_flux_table_columns_and_the_warm_optimum_is_tuned():
+    # The bidirectional-attention table carries a warm and a cold timing per
+    # schedule; the benchmark runs warm and its tuned schedule is the warm
+    # optimum.
+    import json
+    from paper_2506_01374_amd import workloads as W
+    from paper_2506_01374_amd.tune import TableEvaluator
+    name = "attention_noncausal_b1_h24_s4096_d128"
+    op = W.workload_op(name)
+    path = os.path.join(HERE, "..", "results", f"{name}.vec8.tsv")
+    warm = TableEvaluator(path, op, column="warm_us")
+    cold = TableEvaluator(path, op)
+    assert len(warm.table) == len(cold.table) == 2808
+    assert sum(r["valid"] for r in warm.table.values()) == 2343
+    assert all(op.from_string(k).validate() == "" for k in warm.table)
+    tuned = json.load(open(os.path.join(HERE, "..", "paper_2506_01374_amd", "tuned.json")))[name]
+    best = max((r for r in warm.table.values() if r["valid"]), key=lambda r: r["reward"])
+    assert best["schedule"] == str(op.from_string(tuned))
+    k = str(op.from_string(tuned))
+    assert cold.table[k]["ms"] > warm.table[k]["ms"]
