@@ -382,3 +382,23 @@ def test_flux_table_columns_and_the_warm_optimum_is_tuned():
     assert best["schedule"] == str(op.from_string(tuned))
     k = str(op.from_string(tuned))
     assert cold.table[k]["ms"] > warm.table[k]["ms"]
+
+
+def test_causal_vec8_table_warm_optimum_is_tuned():
+    # Every 16-byte-vector, unchunked causal schedule timed warm and cold: the
+    # tuned schedule is the warm optimum; the cold optimum is a one-split
+    # pipelined schedule (one tile in flight per split costs more from HBM).
+    import json
+    from paper_2506_01374_amd import workloads as W
+    from paper_2506_01374_amd.tune import TableEvaluator
+    name = "attention_causal_b1_h32_s1024_d128"
+    op = W.workload_op(name)
+    path = os.path.join(HERE, "..", "results", f"{name}.vec8.tsv")
+    warm = TableEvaluator(path, op, column="warm_us")
+    cold = TableEvaluator(path, op, column="cold_us")
+    assert len(warm.table) == 2808 and sum(r["valid"] for r in warm.table.values()) == 2366
+    tuned = json.load(open(os.path.join(HERE, "..", "paper_2506_01374_amd", "tuned.json")))[name]
+    bw = max((r for r in warm.table.values() if r["valid"]), key=lambda r: r["reward"])
+    bc = max((r for r in cold.table.values() if r["valid"]), key=lambda r: r["reward"])
+    assert bw["schedule"] == str(op.from_string(tuned))
+    assert op.from_string(bc["schedule"]).as_dict()["splits"] == 1
