@@ -163,7 +163,13 @@ rc_status rc_knob_values(const rc_op_desc *d, int32_t knob, int32_t *vals, int32
 rc_status rc_default_schedule(const rc_op_desc *d, rc_schedule *out);
 
 /* Legality check, host only.  Returns RC_OK or RC_ERR_ILLEGAL_SCHEDULE with
- * the first violated rule written to `why` (may be NULL). */
+ * the first violated rule written to `why` (may be NULL).  Tiles may end
+ * partially over the extents that vary with the input (every fp32 GEMM
+ * dimension; the rows of the bf16 GEMMs: tokens, routed rows, output
+ * pixels; the attention sequence length): such tiles are predicated, and a
+ * tile twice the extent it covers is rejected as redundant.  Weight extents
+ * (the N and K of the bf16 GEMMs, the channels of the convolution) must be
+ * whole tiles.  (App. A's perfect-tile decisions.) */
 rc_status rc_validate(const rc_op_desc *d, const rc_schedule *s, char *why, size_t why_len);
 
 /* Apply one transformation: out = t(in).  If the result is illegal, returns
