@@ -181,6 +181,37 @@ def conv2d_bf16(x, w, bias, pad=1, act=True, pixels=None, want_f64=False):
     return (y, y64) if want_f64 else y
 
 
+def moe_routing_prep(ids, E, tile_up, tile_down):
+    """Routing preparation of the MoE layer (integer index work): the routed
+    rows (token, slot), flattened as r = token * topk + slot, grouped by
+    expert.
+
+    Returns a dict of int32 arrays:
+      offsets [E + 1]   offsets[e] = number of routed rows of experts < e
+                        (the exclusive prefix sum of the expert histogram);
+      perm [R]          the rows sorted by expert, rows of one expert in
+                        increasing r (a stable sort by expert id);
+      pos [R]           the inverse permutation: perm[pos[r]] = r;
+      tile_up, tile_down [E + 1]
+                        first M tile of each expert when each expert's rows
+                        are cut into tiles of tile_up / tile_down rows: the
+                        exclusive prefix sum of ceil(count_e / tile).
+    ids must lie in [0, E).
+    """
+    ids = np.asarray(ids, dtype=np.int64).reshape(-1)
+    assert ids.size == 0 or (ids.min() >= 0 and ids.max() < E)
+    counts = np.bincount(ids, minlength=E)
+    offsets = np.concatenate([[0], np.cumsum(counts)])
+    perm = np.argsort(ids, kind="stable")
+    pos = np.empty_like(perm)
+    pos[perm] = np.arange(ids.size)
+    tu = np.concatenate([[0], np.cumsum(-(-counts // tile_up))])
+    td = np.concatenate([[0], np.cumsum(-(-counts // tile_down))])
+    i32 = lambda a: np.asarray(a, dtype=np.int32)
+    return {"offsets": i32(offsets), "perm": i32(perm), "pos": i32(pos),
+            "tile_up": i32(tu), "tile_down": i32(td)}
+
+
 def compare(y, r, tol):
     """Parity rule: max |y - r| / max(|r|, rms(r)) <= tol, all outputs finite.
 

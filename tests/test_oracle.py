@@ -267,6 +267,37 @@ def test_routing_invariants():
     assert np.allclose(w3[0], [p[1], p[3]])
 
 
+def test_routing_prep_brute_force_and_invariants():
+    # Sorting the routed rows by expert, written out by hand: for each expert
+    # in order, the rows routed to it in order of r = token * topk + slot.
+    for seed, (T, E, k, tu, td) in enumerate([(37, 8, 2, 4, 3), (512, 64, 6, 256, 128),
+                                              (5, 16, 3, 16, 16), (64, 3, 1, 1, 2)]):
+        ids = gen.moe_inputs(T, 4, E, 4, k, seed=seed)["ids"]
+        got = orc.moe_routing_prep(ids, E, tu, td)
+        flat = ids.reshape(-1).tolist()
+        perm = [r for e in range(E) for r in range(len(flat)) if flat[r] == e]
+        assert got["perm"].tolist() == perm
+        off, t_up, t_dn = [0], [0], [0]
+        for e in range(E):
+            c = flat.count(e)
+            off.append(off[-1] + c)
+            t_up.append(t_up[-1] + (c + tu - 1) // tu)
+            t_dn.append(t_dn[-1] + (c + td - 1) // td)
+        assert got["offsets"].tolist() == off
+        assert got["tile_up"].tolist() == t_up and got["tile_down"].tolist() == t_dn
+        # invariants: offsets monotone, perm a bijection, pos its inverse,
+        # each expert's rows in its own range
+        assert np.all(np.diff(got["offsets"]) >= 0) and got["offsets"][-1] == T * k
+        assert sorted(got["perm"].tolist()) == list(range(T * k))
+        assert np.array_equal(got["perm"][got["pos"]], np.arange(T * k))
+        for e in range(E):
+            rows = got["perm"][off[e]:off[e + 1]]
+            assert all(flat[r] == e for r in rows) and np.all(np.diff(rows) > 0)
+    # a planted mistake (an unstable order) is caught by the stability check
+    ids = np.array([[1, 0], [1, 0]], dtype=np.int32)
+    assert orc.moe_routing_prep(ids, 2, 1, 1)["perm"].tolist() == [1, 3, 0, 2]
+
+
 def test_moe_forced_routing_equals_dense_mlp():
     T, Hd, E, I = 8, 32, 4, 16
     d = gen.moe_inputs(T, Hd, E, I, 1, seed=2, wsigma=0.2)
