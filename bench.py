@@ -5,7 +5,10 @@ One step is one execution of the workload's operator in its tuned schedule
 (every kernel of the operator: for attention the single fused kernel) over
 inputs already resident in HBM.  W untimed warm-up steps, then exactly K
 steps back to back, bracketed by torch.cuda.synchronize(); value = the
-operator's algorithmic FLOPs x K / elapsed wall time.
+operator's algorithmic FLOPs x K / elapsed wall time.  The default workload
+is the largest: the gated MLP 2048 x 4096 x 14336.  The steps cycle through
+R copies of the inputs, R chosen so that R x the input bytes is at least
+twice the 256 MB last-level cache: each step reads its operands from HBM.
 
 roofline: HIP events recorded on the launch stream around every kernel of
 every timed step give the dominant kernel's mean duration; achieved =
@@ -31,7 +34,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "best-schedule TFLOP/s and % of MFMA peak per operator; samples to reach it"
-DEFAULT_WORKLOAD = "attention_causal_b1_h32_s1024_d128"
+DEFAULT_WORKLOAD = "gated_mlp_t2048_h4096_i14336"
+MALL_BYTES = 256 << 20            # MI355X last-level cache (Infinity Cache)
 HBM_PEAK_GBS = 8000.0
 
 DTYPE = {"gemm_f32_128": "f32", "gemm_f32_m16_n2048_k7168": "f32"}   # the others: bf16 (fp32 accumulation)
@@ -92,6 +96,31 @@ def _oracle_baseline(name, op, host, budget_s):
             "sample": f"{sample}, {reps} repetition(s) in {dt:.2f} s"}
 
 
+def _output_bytes(op):
+    from paper_2506_01374_amd import workloads as W
+    shape, dt = W.output_shape(op)
+    return float(np.prod(shape)) * (4 if dt == "float32" else 2)
+
+
+def _search_summary(name, tuned_text):
+    """Samples the search needed to reach the tuned schedule, from the
+    committed campaign record of this workload (results/), if any."""
+    path = os.path.join(ROOT, "results", f"{name}.campaign.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    summ = rec.get("summary")
+    if not summ:
+        return None
+    return {"source": os.path.relpath(path, ROOT), "reference_schedule": rec.get("reference_schedule"),
+            "reference_is_tuned": rec.get("reference_schedule") == tuned_text,
+            "measurement": rec.get("measurement"), "budget": rec.get("budget"),
+            "seeds": rec.get("seeds"), "policies": summ}
+
+
 def _kernel_source(name):
     from paper_2506_01374_amd import rc, workloads as W
     kind = W.workload_op(name).kind
@@ -128,9 +157,10 @@ def main():
     ap.add_argument("--eager", action="store_true",
                     help="launch each step from the host instead of replaying a captured HIP graph")
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle work")
-    ap.add_argument("--rotate", type=int, default=1, metavar="R",
-                    help="cycle the steps through R copies of the inputs (R x the working set "
-                         "above the 256 MB MALL measures HBM rather than cache bandwidth)")
+    ap.add_argument("--rotate", type=int, default=0, metavar="R",
+                    help="cycle the steps through R copies of the inputs; 0 (default) picks the "
+                         "smallest R >= 2 with R x the input bytes >= 2 x the 256 MB MALL, so "
+                         "every step reads its operands from HBM, not from the cache")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES, --steps times "
                          "(the reference reading for HBM traffic counters)")
@@ -165,7 +195,8 @@ def main():
     tuned = json.load(open(os.path.join(ROOT, "paper_2506_01374_amd", "tuned.json")))
     sched = op.from_string(args.schedule if args.schedule else tuned[name])
     host = W.host_inputs(op, seed=0)
-    R = max(1, args.rotate)
+    in_bytes = op.bytes() - _output_bytes(op)
+    R = args.rotate if args.rotate > 0 else int(min(64, max(2, -(-2 * MALL_BYTES // int(in_bytes)))))
     devs = [W.to_device(W.stored_inputs(op, sched, host)) for _ in range(R)]
     out = W.empty_output(op)
     plan = rc.Plan(op, sched)
@@ -257,6 +288,14 @@ def main():
                       "kernel split from an eager per-kernel event pass" if graph is not None
                       else "HIP events around every kernel of every timed step")
     roof["mfma_frac"] = (flops / (sum(kern_ms) * 1e-3)) / op.peak_flops()
+    # the whole operator (every kernel of the step) against the same roof
+    op_s = step_ms * 1e-3
+    if bound == "hbm":
+        roof["operator"] = {"achieved": op.bytes() / op_s / 1e9, "frac": op.bytes() / op_s / 1e9 / HBM_PEAK_GBS,
+                            "step_ms": step_ms}
+    else:
+        roof["operator"] = {"achieved": flops / op_s / 1e12, "frac": flops / op_s / op.peak_flops(),
+                            "step_ms": step_ms}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -270,9 +309,10 @@ def main():
         "config": {"workload": name, "dims": list(op.dims), "flags": op.flags,
                    "schedule": str(sched), "parallelism": "single GPU",
                    "launch": "hip_graph" if graph is not None else "eager",
-                   "input_copies": R,
+                   "input_copies": R, "input_bytes_per_copy": in_bytes,
                    "frac_of_mfma_peak": value * 1e12 / op.peak_flops()},
         "roofline": roof, "cpu_baseline": cpu,
+        "search": _search_summary(name, str(sched)),
     }
     print(json.dumps(rec), flush=True)
 

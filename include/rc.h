@@ -91,7 +91,11 @@ typedef enum rc_op_kind {
     RC_OP_MOE = 4,
     /* 2-D convolution, stride 1, zero padding, bias and SiLU (the
      * convolution layer of Sec. 4.1), as an implicit GEMM:
-     *   y = bf16( SiLU( conv(x, w) + bias ) ).
+     *   y = bf16( SiLU( conv(x, w) + bias ) ),
+     * or y = bf16( conv(x, w) + bias ) with flags & RC_FLAG_NO_ACT (the
+     * same contraction without the activation; with 1 x 1 filters and no
+     * padding it is a plain bf16 GEMM, and with integer-valued inputs every
+     * output is exact in any accumulation order).
      * dim = {N, H, W, C, K, R, S, pad}.  in[0] = x [N][H][W][C] bf16;
      * in[1] = w stored [K][R][S][C] (layout 1) or [R][S][C][K] (layout 0)
      * bf16; in[2] = bias [K] fp32; out[0] = y [N][P][Q][K] bf16 with
@@ -99,7 +103,8 @@ typedef enum rc_op_kind {
     RC_OP_CONV2D = 5
 } rc_op_kind;
 
-#define RC_FLAG_CAUSAL 1
+#define RC_FLAG_CAUSAL 1   /* RC_OP_ATTENTION only */
+#define RC_FLAG_NO_ACT 2   /* RC_OP_CONV2D only: bias, no SiLU */
 #define RC_MAX_DIMS 8
 
 typedef struct rc_op_desc {
@@ -111,7 +116,9 @@ typedef struct rc_op_desc {
 } rc_op_desc;
 
 /* Fill *d for `kind` with `ndims` dimensions.  Checks the kind, the number
- * of dimensions and that every dimension is positive (pad may be 0). */
+ * of dimensions, that every dimension is positive (pad may be 0) and that
+ * `flags` holds only flags defined for the kind; RC_ERR_INVALID_ARGUMENT
+ * otherwise. */
 rc_status rc_op_init(rc_op_desc *d, int32_t kind, const int64_t *dims, int32_t ndims,
                      int32_t flags);
 
@@ -226,6 +233,26 @@ rc_status rc_plan_workspace(const rc_plan *p, size_t *bytes);
  * most of the FLOPs (the contraction). */
 rc_status rc_plan_kernels(const rc_plan *p, int32_t *nkernels, int32_t *dominant);
 
+/* Byte offset and size of a named part of the workspace, so that a caller
+ * can read intermediate results after a launch (each part starts on a
+ * 256-byte boundary).  Parts by operator:
+ *   RC_OP_MOE: "offsets" int32 [E + 1] (first permuted row of each expert,
+ *     offsets[E] = T * topk); "perm" int32 [T * topk] (permuted row ->
+ *     token * topk + slot, rows of one expert in increasing token * topk +
+ *     slot order); "pos" int32 [T * topk] (the inverse of perm);
+ *     "tile_up" / "tile_down" int32 [E + 1] (first M tile of each expert in
+ *     the gate/up and down GEMMs: exclusive prefix sums of
+ *     ceil(count_e / tile_m)); "hidden" bf16 [T * topk][I] (permuted
+ *     rows); "expert_out" bf16 [T * topk][Hd] (permuted rows);
+ *   RC_OP_GATED_MLP: "hidden" bf16 [T][I];
+ *   unfused epilogues: "gate.f32", "up.f32" or "pre.f32" (fp32 [rows][cols]);
+ *   RC_OP_ATTENTION with chunk > 0: "partials"; RC_OP_GEMM_F32 streaming
+ *   stage with splits > 1: "splitk.partials".
+ * RC_ERR_INVALID_ARGUMENT if the plan has no part of that name.  (The
+ * routing preparation of the MoE layer of Sec. 4.1 is integer index work:
+ * these parts let it be checked exactly.) */
+rc_status rc_plan_buffer(const rc_plan *p, const char *name, size_t *offset, size_t *bytes);
+
 /* Resources of one kernel of a variant, read from its gfx950 code object. */
 typedef struct rc_kernel_info {
     uint32_t struct_size;
@@ -241,7 +268,8 @@ typedef struct rc_kernel_info {
 } rc_kernel_info;
 
 /* Compile (or fetch from the cache) the kernels of a schedule and report
- * their launch shape and resources; needs no GPU.  Writes min(count, cap)
+ * their launch shape and resources, read from each kernel's own entry in
+ * the code object's metadata; needs no GPU.  Writes min(count, cap)
  * entries and the count. */
 rc_status rc_describe(const rc_op_desc *d, const rc_schedule *s, rc_kernel_info *buf,
                       int32_t cap, int32_t *n);
@@ -285,11 +313,23 @@ typedef struct rc_timing {
 
 void rc_time_opts_init(rc_time_opts *o);
 
-/* Time a plan: warm-ups, then `repeat` launches each bracketed by HIP
- * events on `stream` (flush outside the brackets).  Synchronises the
- * stream. */
+/* Time a plan (the objective f of Sec. 2, measured on the target):
+ * `warmup` launches, then `repeat` launches each bracketed by HIP events on
+ * `stream`; with `flush`, a 512 MiB device buffer (twice the MI355X's
+ * 256 MB last-level cache) is overwritten before each timed launch, outside
+ * the brackets.  The flush buffer is allocated on the current device at its
+ * first flushed timing and kept for later calls (rc_time_release frees it).
+ * Returns the median, quartiles, minimum and mean of the timed launches,
+ * the median duration of each kernel, and the derived rates against
+ * rc_op_flops / rc_op_bytes and the peaks.  Synchronises the stream; every
+ * event it created is destroyed on every path. */
 rc_status rc_time(const rc_plan *p, const rc_args *a, void *workspace, size_t ws_bytes,
                   void *stream, const rc_time_opts *o, rc_timing *out);
+
+/* Free the flush buffers rc_time allocated (on every device it used).  The
+ * caller makes sure no rc_time call is running; a later flushed rc_time
+ * allocates again. */
+rc_status rc_time_release(void);
 
 /* ------------------------------------------------------------------ */
 /* Search (Sec. 3.2): UCT tree search, random sampling, exhaustive     */

@@ -39,15 +39,26 @@ extern "C" __global__ __launch_bounds__(256) void rc_swiglu_f32(EwArgs a) {
     *(u32x2 *)(a.out + i) = p;
 }
 
-// out[m][n] = bf16(SiLU(G[m][n] + bias[n])), four elements per thread.
+// out[m][n] = bf16(SiLU(G[m][n] + bias[n])) (EW_ACT 1) or
+// bf16(G[m][n] + bias[n]) (EW_ACT 0), four elements per thread.
+#ifndef EW_ACT
+#define EW_ACT 1
+#endif
+__device__ __forceinline__ float ew_act(float x) {
+#if EW_ACT
+    return silu(x);
+#else
+    return x;
+#endif
+}
 extern "C" __global__ __launch_bounds__(256) void rc_bias_silu_f32(EwArgs a) {
     const long i = ((long)blockIdx.x * 256 + threadIdx.x) * 4;
     if (i >= EW_N) return;
     const int n = (int)(i % EW_COLS);
     f32x4 g = *(const f32x4 *)(a.G + i);
     u32x2 p;
-    p[0] = (unsigned)f2bf(silu(g[0] + a.bias[n])) | ((unsigned)f2bf(silu(g[1] + a.bias[n + 1])) << 16);
-    p[1] = (unsigned)f2bf(silu(g[2] + a.bias[n + 2])) | ((unsigned)f2bf(silu(g[3] + a.bias[n + 3])) << 16);
+    p[0] = (unsigned)f2bf(ew_act(g[0] + a.bias[n])) | ((unsigned)f2bf(ew_act(g[1] + a.bias[n + 1])) << 16);
+    p[1] = (unsigned)f2bf(ew_act(g[2] + a.bias[n + 2])) | ((unsigned)f2bf(ew_act(g[3] + a.bias[n + 3])) << 16);
     *(u32x2 *)(a.out + i) = p;
 }
 #endif
@@ -64,91 +75,114 @@ struct MoePrepArgs {
     int *tile_down;        // [E + 1] first M tile of each expert, down GEMM
 };
 
-// Grid: MOE_E workgroups of PREP_T threads.  Every workgroup copies all
-// expert ids into LDS (ids out of range are clamped to expert 0 so that no
-// write can leave its buffer), builds the expert histogram from per-wave
-// sub-histograms, derives the exclusive prefix offsets and the per-expert
-// tile starts, and then workgroup e writes the rows routed to expert e in
-// token order (a stable counting sort): each thread owns a contiguous chunk
-// of entries, counts its hits, and one block-wide exclusive scan of those
-// counts gives every thread its first output row.  Workgroup 0 also
-// publishes offsets and tile starts.
+// Routing preparation in one workgroup of PREP_T threads: a stable counting
+// sort of the routed rows by expert, reading the expert ids twice.
+//   1. Wave w owns the contiguous segment w of the rows and counts its
+//      rows per expert into cnt[w][*] (LDS atomics; only wave w touches
+//      row w of cnt).
+//   2. Thread x (one per expert) sums column x of cnt and turns it into
+//      the exclusive prefix over the waves; a block-wide exclusive scan of
+//      the column sums gives offsets[] and, from ceil(count / tile), the
+//      tile starts of both expert GEMMs; cnt[w][x] becomes the first
+//      permuted row of wave w's rows routed to expert x.
+//   3. Each wave walks its segment again in order, 64 rows at a time.  The
+//      lanes holding the same expert are found with one ballot per bit of
+//      the expert id; a lane's permuted row is cnt[w][x] plus the number of
+//      such lanes below it, and the lowest of them advances cnt[w][x].
+// Rows keep their order within an expert (wave segments in order, lanes in
+// order within a group), so the result is deterministic.  Expert ids out of
+// range are clamped to expert 0 so that no write can leave its buffer.
+// Loads are issued PREP_G groups at a time so that their latencies overlap.
 #define PREP_T 1024
 #define PREP_W (PREP_T / 64)
-#define PREP_CHUNK ((MOE_ROWS + PREP_T - 1) / PREP_T)
+#define PREP_G 8
+#define PREP_SEG ((((MOE_ROWS + PREP_W - 1) / PREP_W) + 63) / 64 * 64)
+#define PREP_BITS (MOE_E <= 1 ? 1 : 32 - __builtin_clz(MOE_E - 1))
+
+__device__ __forceinline__ int prep_id(const int *ids, int i, int end) {
+    if (i >= end) return -1;
+    const int x = ids[i];
+    return (x < 0 || x >= MOE_E) ? 0 : x;
+}
 
 extern "C" __global__ __launch_bounds__(PREP_T) void rc_moe_prep(MoePrepArgs a) {
-    __shared__ int ids[PREP_CHUNK * PREP_T];
-    __shared__ int sub[PREP_W][MOE_E];
-    __shared__ int offs[MOE_E + 1];
-    __shared__ int wsum[PREP_W];
-    const int tid = threadIdx.x, e = blockIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
-    for (int i = tid; i < PREP_W * MOE_E; i += PREP_T) (&sub[0][0])[i] = 0;
-    for (int i = tid; i < PREP_CHUNK * PREP_T; i += PREP_T) {
-        int x = i < MOE_ROWS ? a.ids[i] : -1;
-        if (i < MOE_ROWS && (x < 0 || x >= MOE_E)) x = 0;
-        ids[i] = x;
+    __shared__ int cnt[PREP_W][MOE_E];
+    __shared__ int wsum[3][PREP_W];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    for (int i = tid; i < PREP_W * MOE_E; i += PREP_T) (&cnt[0][0])[i] = 0;
+    const int seg0 = wave * PREP_SEG;
+    const int seg1 = min(seg0 + PREP_SEG, MOE_ROWS);
+    __syncthreads();
+
+    // 1. per-wave histogram of the wave's segment
+    for (int g0 = seg0; g0 < seg1; g0 += 64 * PREP_G) {
+        int x[PREP_G];
+#pragma unroll
+        for (int g = 0; g < PREP_G; ++g) x[g] = prep_id(a.ids, g0 + g * 64 + lane, seg1);
+#pragma unroll
+        for (int g = 0; g < PREP_G; ++g)
+            if (x[g] >= 0) atomicAdd(&cnt[wave][x[g]], 1);
     }
     __syncthreads();
-    for (int i = tid; i < MOE_ROWS; i += PREP_T) atomicAdd(&sub[wave][ids[i]], 1);
-    __syncthreads();
-    if (wave == 0) {
-        // lane x sums expert x over the sub-histograms; one wave scans 64 bins
-        int run = 0, tu = 0, td = 0;
-        for (int base = 0; base < MOE_E; base += 64) {
-            int x = base + lane;
-            int h = 0;
-            if (x < MOE_E)
-                for (int w = 0; w < PREP_W; ++w) h += sub[w][x];
-            int hu = (h + MOE_TM_UP - 1) / MOE_TM_UP, hd = (h + MOE_TM_DOWN - 1) / MOE_TM_DOWN;
-            int ih = h, iu = hu, id = hd;          // inclusive scans across the wave
-            for (int d = 1; d < 64; d <<= 1) {
-                int th = __shfl_up(ih, d), tu2 = __shfl_up(iu, d), td2 = __shfl_up(id, d);
-                if (lane >= d) { ih += th; iu += tu2; id += td2; }
-            }
-            if (x < MOE_E) {
-                offs[x] = run + ih - h;
-                if (e == 0) {
-                    a.offsets[x] = run + ih - h;
-                    a.tile_up[x] = tu + iu - hu;
-                    a.tile_down[x] = td + id - hd;
-                }
-            }
-            run += __shfl(ih, 63);
-            tu += __shfl(iu, 63);
-            td += __shfl(id, 63);
-        }
-        if (lane == 0) {
-            offs[MOE_E] = run;
-            if (e == 0) {
-                a.offsets[MOE_E] = run;
-                a.tile_up[MOE_E] = tu;
-                a.tile_down[MOE_E] = td;
-            }
+
+    // 2. per-expert totals, exclusive prefixes over waves and experts
+    int h = 0;
+    if (tid < MOE_E) {
+        for (int w = 0; w < PREP_W; ++w) {
+            const int c = cnt[w][tid];
+            cnt[w][tid] = h;
+            h += c;
         }
     }
-    __syncthreads();
-    // stable compaction of the entries routed to expert e
-    const int c0 = tid * PREP_CHUNK;
-    int cnt = 0;
-    for (int j = 0; j < PREP_CHUNK; ++j) cnt += (c0 + j < MOE_ROWS && ids[c0 + j] == e);
-    int inc = cnt;
+    const int hu = (h + MOE_TM_UP - 1) / MOE_TM_UP, hd = (h + MOE_TM_DOWN - 1) / MOE_TM_DOWN;
+    int ih = h, iu = hu, id = hd;              // inclusive scans within the wave
     for (int d = 1; d < 64; d <<= 1) {
-        int t = __shfl_up(inc, d);
-        if (lane >= d) inc += t;
+        const int th = __shfl_up(ih, d), tu = __shfl_up(iu, d), td = __shfl_up(id, d);
+        if (lane >= d) { ih += th; iu += tu; id += td; }
     }
-    if (lane == 63) wsum[wave] = inc;
+    if (lane == 63) { wsum[0][wave] = ih; wsum[1][wave] = iu; wsum[2][wave] = id; }
     __syncthreads();
-    int before = 0;
-    for (int w = 0; w < wave; ++w) before += wsum[w];
-    int p = offs[e] + before + inc - cnt;
-    for (int j = 0; j < PREP_CHUNK; ++j) {
-        int i = c0 + j;
-        if (i < MOE_ROWS && ids[i] == e) {
-            a.perm[p] = i;
-            a.pos[i] = p;
-            ++p;
+    int bh = 0, bu = 0, bd = 0;
+    for (int w = 0; w < wave; ++w) { bh += wsum[0][w]; bu += wsum[1][w]; bd += wsum[2][w]; }
+    if (tid < MOE_E) {
+        const int off = bh + ih - h;
+        a.offsets[tid] = off;
+        a.tile_up[tid] = bu + iu - hu;
+        a.tile_down[tid] = bd + id - hd;
+        for (int w = 0; w < PREP_W; ++w) cnt[w][tid] += off;
+        if (tid == MOE_E - 1) {
+            a.offsets[MOE_E] = bh + ih;
+            a.tile_up[MOE_E] = bu + iu;
+            a.tile_down[MOE_E] = bd + id;
+        }
+    }
+    __syncthreads();
+
+    // 3. stable scatter of the wave's segment
+    const unsigned long long below = (1ull << lane) - 1ull;
+    for (int g0 = seg0; g0 < seg1; g0 += 64 * PREP_G) {
+        int x[PREP_G];
+#pragma unroll
+        for (int g = 0; g < PREP_G; ++g) x[g] = prep_id(a.ids, g0 + g * 64 + lane, seg1);
+#pragma unroll
+        for (int g = 0; g < PREP_G; ++g) {
+            const bool valid = x[g] >= 0;
+            unsigned long long m = __ballot(valid);
+#pragma unroll
+            for (int b = 0; b < PREP_BITS; ++b) {
+                const bool bit = valid && ((x[g] >> b) & 1);
+                const unsigned long long bb = __ballot(bit);
+                m &= bit ? bb : ~bb;
+            }
+            if (valid) {
+                const int i = g0 + g * 64 + lane;
+                const int base = cnt[wave][x[g]];
+                const int p = base + __popcll(m & below);
+                a.perm[p] = i;
+                a.pos[i] = p;
+                // the lowest lane of the group advances the expert's next row
+                if ((m & below) == 0ull) cnt[wave][x[g]] = base + __popcll(m);
+            }
         }
     }
 }

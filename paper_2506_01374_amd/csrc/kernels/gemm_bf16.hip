@@ -34,7 +34,8 @@
 //                image; 3 MoE grouped dense rows (row p of the permuted
 //                hidden matrix)
 //   EPI          0 store bf16; 1 + bias, SiLU, store bf16; 2 SiLU(acc0) *
-//                acc1, store bf16; 3 store fp32 accumulators (unfused)
+//                acc1, store bf16; 3 store fp32 accumulators (unfused);
+//                4 + bias, store bf16 (no activation)
 //   GM GN GK     GEMM sizes (GM = rows for AMODE 0/2, total routed rows for
 //                AMODE 1/3).  Dense rows (AMODE 0/2) need not fill the last
 //                M tile: its missing rows load zeros (register staging) or
@@ -728,6 +729,9 @@ void rc_gemm_bf16(GemmBf16Args args) {
 #elif EPI == 2
 #pragma unroll
                 for (int r = 0; r < 4; ++r) v[r] = silu(v[r]) * acc[1][i][j][g * 4 + r];
+#elif EPI == 4
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] = v[r] + args.bias[n + r];
 #endif
                 u32x2 packed;
                 packed[0] = pack2(v[0], v[1]);

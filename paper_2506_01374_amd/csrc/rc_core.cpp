@@ -7,6 +7,7 @@
 // and a transformation sets one knob.  The knob classes are the
 // transformation names of App. A (TileSize, Parallel, ComputeLocation,
 // Unroll) plus the vectorisation and layout changes named in Sec. 1.
+#include <climits>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -403,8 +404,11 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
         case RC_OP_MOE: {
             int64_t Hd = D[1], E = D[2], I = D[3], topk = D[4];
             if (topk > E) return "topk exceeds the number of experts";
-            // the routing kernel stages every expert id in LDS
-            if (D[0] * topk > 32768) return "more than 32768 routed rows";
+            // the routing kernel (one workgroup of 1024 threads) keeps one
+            // thread per expert and per-wave row counts of every expert in
+            // LDS (16 x E x 4 B)
+            if (E > 1024) return fmt("%lld experts exceed the routing kernel's 1024", (long long)E);
+            if (D[0] * topk > INT32_MAX / 2) return "routed rows exceed the 32-bit row indices";
             std::string r = check_bf16_block(d, s, UP, -1, I, Hd, 2, "up");
             if (!r.empty()) return r;
             return check_bf16_block(d, s, DOWN, -1, Hd, I, 1, "down");
@@ -458,6 +462,8 @@ rc_status rc_op_init(rc_op_desc *d, int32_t kind, const int64_t *dims, int32_t n
     for (int i = 0; i < nd; ++i) t.dim[i] = dims[i];
     t.flags = flags;
     if (!desc_ok(&t)) return fail(RC_ERR_INVALID_ARGUMENT, "dimensions must be positive");
+    const int32_t allowed = kind == RC_OP_ATTENTION ? RC_FLAG_CAUSAL : kind == RC_OP_CONV2D ? RC_FLAG_NO_ACT : 0;
+    if (flags & ~allowed) return fail(RC_ERR_INVALID_ARGUMENT, fmt("flags 0x%x not defined for kind %d", flags, kind));
     if (kind == RC_OP_MOE && t.dim[4] > t.dim[2])
         return fail(RC_ERR_INVALID_ARGUMENT, "topk exceeds the number of experts");
     *d = t;

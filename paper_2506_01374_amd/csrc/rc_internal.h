@@ -34,4 +34,9 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s);
 // Directory holding the kernel sources' embedded copy and the cache.
 std::string cache_dir();
 
+// rc_launch with the workspace given by the caller of this function (no
+// allocation on any path that succeeds).
+rc_status launch_plan(const rc_plan *p, const rc_args *a, void *workspace, size_t ws_bytes,
+                      void *stream);
+
 }  // namespace rc

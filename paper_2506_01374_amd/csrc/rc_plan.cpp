@@ -62,6 +62,13 @@ struct AttnArgs {
     void *P;   // partial states of query tiles cut into several work items
 };
 
+// A kernel's by-value argument block (fixed storage: launching allocates
+// nothing on the host).
+struct ArgBlob {
+    alignas(16) char data[128];
+    size_t size = 0;
+};
+
 struct Source {
     const char *file;     // kernel source text
     const char *entry;    // kernel function name
@@ -167,22 +174,169 @@ rc_status compile(const Source &s, std::vector<char> &code, std::string &key) {
     return RC_OK;
 }
 
-// Integer value following a metadata key in the code object's msgpack note.
-long meta_int(const std::vector<char> &code, const char *key) {
-    size_t kl = strlen(key);
-    for (size_t i = 0; i + kl + 1 < code.size(); ++i) {
-        if ((unsigned char)code[i] != (0xa0 | kl) || memcmp(&code[i + 1], key, kl) != 0) continue;
-        size_t j = i + 1 + kl;
-        unsigned char t = (unsigned char)code[j];
-        if (t <= 0x7f) return t;
-        if (t == 0xcc) return (unsigned char)code[j + 1];
-        if (t == 0xcd) return ((unsigned char)code[j + 1] << 8) | (unsigned char)code[j + 2];
-        if (t == 0xce)
-            return ((long)(unsigned char)code[j + 1] << 24) | ((unsigned char)code[j + 2] << 16) |
-                   ((unsigned char)code[j + 3] << 8) | (unsigned char)code[j + 4];
-        return -1;
+// ---------------------------------------------------------------------
+// Code-object metadata: the AMDGPU note (type 32) of the ELF holds a
+// msgpack document whose "amdhsa.kernels" array has one map per kernel.
+// KernelMeta reads the integer keys of the map whose ".name" is the entry.
+// ---------------------------------------------------------------------
+struct MsgReader {
+    const unsigned char *p, *end;
+    bool ok = true;
+    uint64_t be(int n) {
+        if (end - p < n) { ok = false; p = end; return 0; }
+        uint64_t v = 0;
+        for (int i = 0; i < n; ++i) v = (v << 8) | p[i];
+        p += n;
+        return v;
     }
-    return -1;
+    // Reads one value; strings go to *str, integers to *num (when non-null).
+    // Returns the msgpack family: 'i' integer, 's' string, 'm' map (count in
+    // *num, entries follow), 'a' array (count in *num), 'o' anything else
+    // (consumed).
+    char next(int64_t *num, std::string *str) {
+        if (p >= end) { ok = false; return 'o'; }
+        unsigned t = *p++;
+        auto sized_str = [&](uint64_t n) {
+            if ((uint64_t)(end - p) < n) { ok = false; p = end; return 'o'; }
+            if (str) str->assign((const char *)p, (size_t)n);
+            p += n;
+            return 's';
+        };
+        if (t <= 0x7f) { if (num) *num = t; return 'i'; }
+        if (t >= 0xe0) { if (num) *num = (int8_t)t; return 'i'; }
+        if ((t & 0xf0) == 0x80) { if (num) *num = t & 0x0f; return 'm'; }
+        if ((t & 0xf0) == 0x90) { if (num) *num = t & 0x0f; return 'a'; }
+        if ((t & 0xe0) == 0xa0) return sized_str(t & 0x1f);
+        switch (t) {
+            case 0xc0: case 0xc2: case 0xc3: return 'o';
+            case 0xc4: p += be(1); return 'o';
+            case 0xc5: p += be(2); return 'o';
+            case 0xc6: p += be(4); return 'o';
+            case 0xca: p += 4; return 'o';
+            case 0xcb: p += 8; return 'o';
+            case 0xcc: { int64_t v = (int64_t)be(1); if (num) *num = v; return 'i'; }
+            case 0xcd: { int64_t v = (int64_t)be(2); if (num) *num = v; return 'i'; }
+            case 0xce: { int64_t v = (int64_t)be(4); if (num) *num = v; return 'i'; }
+            case 0xcf: { int64_t v = (int64_t)be(8); if (num) *num = v; return 'i'; }
+            case 0xd0: { int64_t v = (int8_t)be(1); if (num) *num = v; return 'i'; }
+            case 0xd1: { int64_t v = (int16_t)be(2); if (num) *num = v; return 'i'; }
+            case 0xd2: { int64_t v = (int32_t)be(4); if (num) *num = v; return 'i'; }
+            case 0xd3: { int64_t v = (int64_t)be(8); if (num) *num = v; return 'i'; }
+            case 0xd9: return sized_str(be(1));
+            case 0xda: return sized_str(be(2));
+            case 0xdb: return sized_str(be(4));
+            case 0xdc: { int64_t v = (int64_t)be(2); if (num) *num = v; return 'a'; }
+            case 0xdd: { int64_t v = (int64_t)be(4); if (num) *num = v; return 'a'; }
+            case 0xde: { int64_t v = (int64_t)be(2); if (num) *num = v; return 'm'; }
+            case 0xdf: { int64_t v = (int64_t)be(4); if (num) *num = v; return 'm'; }
+        }
+        ok = false;   // ext types do not occur in the metadata
+        return 'o';
+    }
+    void skip() {
+        int64_t n = 0;
+        char k = next(&n, nullptr);
+        if (k == 'm') n *= 2;
+        if (k == 'm' || k == 'a')
+            for (int64_t i = 0; i < n && ok; ++i) skip();
+    }
+};
+
+struct KernelMeta {
+    std::map<std::string, int64_t> ints;
+    long get(const char *key) const {
+        auto it = ints.find(key);
+        return it == ints.end() ? -1 : (long)it->second;
+    }
+};
+
+// Locate the metadata note of a 64-bit little-endian ELF code object.
+bool metadata_note(const std::vector<char> &code, const unsigned char **b, const unsigned char **e) {
+    const unsigned char *c = (const unsigned char *)code.data();
+    const size_t n = code.size();
+    if (n < 64 || memcmp(c, "\x7f" "ELF", 4) != 0 || c[4] != 2) return false;
+    auto rd = [&](size_t off, int bytes) -> uint64_t {
+        uint64_t v = 0;
+        if (off + bytes > n) return 0;
+        for (int i = bytes - 1; i >= 0; --i) v = (v << 8) | c[off + i];
+        return v;
+    };
+    const uint64_t shoff = rd(0x28, 8), shentsize = rd(0x3a, 2), shnum = rd(0x3c, 2);
+    for (uint64_t i = 0; i < shnum; ++i) {
+        const size_t sh = (size_t)(shoff + i * shentsize);
+        if (rd(sh + 4, 4) != 7) continue;   // SHT_NOTE
+        size_t off = (size_t)rd(sh + 0x18, 8), end = off + (size_t)rd(sh + 0x20, 8);
+        if (end > n) continue;
+        while (off + 12 <= end) {
+            const uint64_t namesz = rd(off, 4), descsz = rd(off + 4, 4), type = rd(off + 8, 4);
+            const size_t name = off + 12, desc = name + ((namesz + 3) & ~3ull);
+            if (desc + descsz > end) break;
+            if (type == 32 && namesz >= 6 && memcmp(c + name, "AMDGPU", 6) == 0) {
+                *b = c + desc;
+                *e = c + desc + descsz;
+                return true;
+            }
+            off = desc + ((descsz + 3) & ~3ull);
+        }
+    }
+    return false;
+}
+
+// Integer keys of the metadata map of kernel `entry` (empty if not found).
+KernelMeta kernel_meta(const std::vector<char> &code, const char *entry) {
+    KernelMeta out;
+    const unsigned char *b = nullptr, *e = nullptr;
+    if (!metadata_note(code, &b, &e)) return out;
+    MsgReader r{b, e};
+    int64_t n = 0;
+    if (r.next(&n, nullptr) != 'm') return out;
+    for (int64_t i = 0; i < n && r.ok; ++i) {
+        std::string key;
+        if (r.next(nullptr, &key) != 's') return out;
+        if (key != "amdhsa.kernels") {
+            r.skip();
+            continue;
+        }
+        int64_t nk = 0;
+        if (r.next(&nk, nullptr) != 'a') return out;
+        for (int64_t k = 0; k < nk && r.ok; ++k) {
+            int64_t nf = 0;
+            if (r.next(&nf, nullptr) != 'm') return out;
+            KernelMeta m;
+            std::string name;
+            for (int64_t f = 0; f < nf && r.ok; ++f) {
+                std::string fk;
+                if (r.next(nullptr, &fk) != 's') return out;
+                int64_t v = 0;
+                std::string sv;
+                const unsigned char *at = r.p;
+                char kind = r.next(&v, &sv);
+                if (kind == 'i') {
+                    m.ints[fk] = v;
+                } else if (kind == 's') {
+                    if (fk == ".name") name = sv;
+                } else if (kind == 'm' || kind == 'a') {
+                    r.p = at;
+                    r.skip();
+                }
+            }
+            if (name == entry) return m;
+        }
+        return out;
+    }
+    return out;
+}
+
+// A kernel that needs private (scratch) memory spills registers: the
+// schedule is illegal.  Missing metadata is a compile error.
+rc_status check_spill(const std::vector<char> &code, const char *entry) {
+    const KernelMeta m = kernel_meta(code, entry);
+    const long scratch = m.get(".private_segment_fixed_size");
+    if (scratch < 0) return fail(RC_ERR_COMPILE, std::string("no metadata for kernel ") + entry);
+    if (scratch > 0)
+        return fail(RC_ERR_ILLEGAL_SCHEDULE, std::string("spill: ") + entry + " needs " +
+                                                 std::to_string(scratch) + " B of scratch memory per lane");
+    return RC_OK;
 }
 
 std::string def(const char *name, long long v) {
@@ -196,15 +350,17 @@ struct Kern {
     Source src;
     dim3 grid, block;
     // fills the argument block from the caller's buffers and the workspace
-    std::function<void(const rc_args *, char *ws, std::vector<char> &blob)> bind;
+    std::function<void(const rc_args *, char *ws, ArgBlob &blob)> bind;
     hipFunction_t fn = nullptr;
 };
 
 struct WsLayout {
     size_t total = 0;
-    size_t add(size_t bytes) {
+    std::map<std::string, std::pair<size_t, size_t>> parts;
+    size_t add(size_t bytes, const char *name) {
         size_t off = total;
         total += (bytes + 255) & ~(size_t)255;
+        parts[name] = {off, bytes};
         return off;
     }
 };
@@ -229,9 +385,10 @@ std::string gemm_defs(const GemmCfg &g, int nb, int amode, int epi, long gm, lon
 }
 
 template <class T>
-void put(std::vector<char> &blob, const T &v) {
-    blob.resize(sizeof(T));
-    memcpy(blob.data(), &v, sizeof(T));
+void put(ArgBlob &blob, const T &v) {
+    static_assert(sizeof(T) <= sizeof(blob.data), "kernel argument block too large");
+    blob.size = sizeof(T);
+    memcpy(blob.data, &v, sizeof(T));
 }
 
 }  // namespace
@@ -242,6 +399,8 @@ struct rc_plan {
     std::vector<Kern> kerns;
     size_t workspace = 0;
     int dominant = 0;
+    // named parts of the workspace: name -> (byte offset, bytes)
+    std::map<std::string, std::pair<size_t, size_t>> parts;
 };
 
 namespace rc {
@@ -277,13 +436,13 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             // streaming stage: one workgroup per (64-column tile, K split);
             // with K splits the per-split partial sums live in the workspace
             const bool split = st == 3 && sp > 1;
-            size_t offP = split ? ws.add((size_t)sp * D[0] * D[1] * 4) : 0;
+            size_t offP = split ? ws.add((size_t)sp * D[0] * D[1] * 4, "splitk.partials") : 0;
             if (st == 3)
                 k.grid = dim3((unsigned)(D[1] / 64 * sp), 1, 1);
             else
                 k.grid = dim3((unsigned)((D[1] + tn - 1) / tn), (unsigned)((D[0] + tm - 1) / tm), 1);
             k.block = dim3(nt, 1, 1);
-            k.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
+            k.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
                 put(b, GemmF32Args{a->in[0], a->in[1], a->out[0], split ? w + offP : nullptr});
             };
             p.kerns.push_back(k);
@@ -301,17 +460,17 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             long T = D[0], Hd = D[1], I = D[2];
             GemmCfg up = read_block(d, s, "up."), dn = read_block(d, s, "down.");
             int fuse = kv(d, s, "fuse");
-            size_t offH = ws.add((size_t)T * I * 2);
+            size_t offH = ws.add((size_t)T * I * 2, "hidden");
             size_t offG = 0, offU = 0;
             if (!fuse) {
-                offG = ws.add((size_t)T * I * 4);
-                offU = ws.add((size_t)T * I * 4);
+                offG = ws.add((size_t)T * I * 4, "gate.f32");
+                offU = ws.add((size_t)T * I * 4, "up.f32");
             }
             Kern k1;
             k1.src = Source{SRC_gemm_bf16, "rc_gemm_bf16", gemm_defs(up, 2, 0, fuse ? 2 : 3, T, I, Hd)};
             k1.grid = dim3((unsigned)(((T + up.tm - 1) / up.tm) * (I / up.tn)), 1, 1);
             k1.block = dim3(64 * up.wm * up.wn, 1, 1);
-            k1.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
+            k1.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
                 if (fuse)
                     put(b, GemmBf16Args{a->in[0], a->in[1], a->in[2], w + offH, nullptr, nullptr,
                                         nullptr, nullptr, nullptr});
@@ -325,7 +484,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
                 ke.src = Source{SRC_aux, "rc_swiglu_f32", def("EW_N", T * I) + def("EW_COLS", I)};
                 ke.grid = dim3((unsigned)((T * I / 4 + 255) / 256), 1, 1);
                 ke.block = dim3(256, 1, 1);
-                ke.bind = [=](const rc_args *, char *w, std::vector<char> &b) {
+                ke.bind = [=](const rc_args *, char *w, ArgBlob &b) {
                     put(b, EwArgs{w + offG, w + offU, nullptr, w + offH});
                 };
                 p.kerns.push_back(ke);
@@ -334,7 +493,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             k2.src = Source{SRC_gemm_bf16, "rc_gemm_bf16", gemm_defs(dn, 1, 0, 0, T, Hd, I)};
             k2.grid = dim3((unsigned)(((T + dn.tm - 1) / dn.tm) * (Hd / dn.tn)), 1, 1);
             k2.block = dim3(64 * dn.wm * dn.wn, 1, 1);
-            k2.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
+            k2.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
                 put(b, GemmBf16Args{w + offH, a->in[3], nullptr, a->out[0], nullptr, nullptr,
                                     nullptr, nullptr, nullptr});
             };
@@ -346,21 +505,22 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             long T = D[0], Hd = D[1], E = D[2], I = D[3], topk = D[4], R = T * topk;
             GemmCfg up = read_block(d, s, "up."), dn = read_block(d, s, "down.");
             int fuse = kv(d, s, "fuse");
-            size_t offOff = ws.add((E + 1) * 4), offPerm = ws.add(R * 4), offPos = ws.add(R * 4);
-            size_t offTu = ws.add((E + 1) * 4), offTd = ws.add((E + 1) * 4);
-            size_t offH = ws.add((size_t)R * I * 2), offY = ws.add((size_t)R * Hd * 2);
+            size_t offOff = ws.add((E + 1) * 4, "offsets"), offPerm = ws.add(R * 4, "perm");
+            size_t offPos = ws.add(R * 4, "pos");
+            size_t offTu = ws.add((E + 1) * 4, "tile_up"), offTd = ws.add((E + 1) * 4, "tile_down");
+            size_t offH = ws.add((size_t)R * I * 2, "hidden"), offY = ws.add((size_t)R * Hd * 2, "expert_out");
             size_t offG = 0, offU = 0;
             if (!fuse) {
-                offG = ws.add((size_t)R * I * 4);
-                offU = ws.add((size_t)R * I * 4);
+                offG = ws.add((size_t)R * I * 4, "gate.f32");
+                offU = ws.add((size_t)R * I * 4, "up.f32");
             }
             std::string moe = def("MOE_T", T) + def("MOE_TOPK", topk) + def("MOE_E", E) +
                               def("MOE_H", Hd) + def("MOE_TM_UP", up.tm) + def("MOE_TM_DOWN", dn.tm);
             Kern k0;
             k0.src = Source{SRC_aux, "rc_moe_prep", moe};
-            k0.grid = dim3((unsigned)E, 1, 1);
+            k0.grid = dim3(1, 1, 1);            // one workgroup: a stable counting sort
             k0.block = dim3(1024, 1, 1);
-            k0.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
+            k0.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
                 put(b, MoePrepArgs{a->in[1], w + offOff, w + offPerm, w + offPos, w + offTu, w + offTd});
             };
             p.kerns.push_back(k0);
@@ -371,7 +531,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             long ntm_up = (R + up.tm - 1) / up.tm + E;
             k1.grid = dim3((unsigned)(ntm_up * (I / up.tn)), 1, 1);
             k1.block = dim3(64 * up.wm * up.wn, 1, 1);
-            k1.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
+            k1.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
                 put(b, GemmBf16Args{a->in[0], a->in[3], a->in[4], w + (fuse ? offH : offG),
                                     fuse ? nullptr : w + offU, nullptr, w + offPerm, w + offOff,
                                     w + offTu});
@@ -383,7 +543,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
                 ke.src = Source{SRC_aux, "rc_swiglu_f32", def("EW_N", R * I) + def("EW_COLS", I)};
                 ke.grid = dim3((unsigned)((R * I / 4 + 255) / 256), 1, 1);
                 ke.block = dim3(256, 1, 1);
-                ke.bind = [=](const rc_args *, char *w, std::vector<char> &b) {
+                ke.bind = [=](const rc_args *, char *w, ArgBlob &b) {
                     put(b, EwArgs{w + offG, w + offU, nullptr, w + offH});
                 };
                 p.kerns.push_back(ke);
@@ -393,7 +553,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             long ntm_dn = (R + dn.tm - 1) / dn.tm + E;
             k2.grid = dim3((unsigned)(ntm_dn * (Hd / dn.tn)), 1, 1);
             k2.block = dim3(64 * dn.wm * dn.wn, 1, 1);
-            k2.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
+            k2.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
                 put(b, GemmBf16Args{w + offH, a->in[5], nullptr, w + offY, nullptr, nullptr,
                                     w + offPerm, w + offOff, w + offTd});
             };
@@ -402,7 +562,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             k3.src = Source{SRC_aux, "rc_moe_combine", moe};
             k3.grid = dim3((unsigned)((T * (Hd / 8) + 255) / 256), 1, 1);
             k3.block = dim3(256, 1, 1);
-            k3.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
+            k3.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
                 put(b, MoeCombineArgs{w + offY, w + offPos, a->in[2], a->out[0]});
             };
             p.kerns.push_back(k3);
@@ -413,15 +573,16 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             long P = H + 2 * pad - R + 1, Q = W + 2 * pad - S + 1, M = N * P * Q;
             GemmCfg g = read_block(d, s, "");
             int fuse = kv(d, s, "fuse");
-            size_t offPre = fuse ? 0 : ws.add((size_t)M * K * 4);
+            const bool act = (d->flags & RC_FLAG_NO_ACT) == 0;
+            size_t offPre = fuse ? 0 : ws.add((size_t)M * K * 4, "pre.f32");
             std::string cv = def("CV_H", H) + def("CV_W", W) + def("CV_C", C) + def("CV_P", P) +
                              def("CV_Q", Q) + def("CV_S", S) + def("CV_PAD", pad);
             Kern k1;
             k1.src = Source{SRC_gemm_bf16, "rc_gemm_bf16",
-                            gemm_defs(g, 1, 2, fuse ? 1 : 3, M, K, R * S * C) + cv};
+                            gemm_defs(g, 1, 2, fuse ? (act ? 1 : 4) : 3, M, K, R * S * C) + cv};
             k1.grid = dim3((unsigned)(((M + g.tm - 1) / g.tm) * (K / g.tn)), 1, 1);
             k1.block = dim3(64 * g.wm * g.wn, 1, 1);
-            k1.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
+            k1.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
                 if (fuse)
                     put(b, GemmBf16Args{a->in[0], a->in[1], nullptr, a->out[0], nullptr, a->in[2],
                                         nullptr, nullptr, nullptr});
@@ -432,10 +593,11 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             p.kerns.push_back(k1);
             if (!fuse) {
                 Kern ke;
-                ke.src = Source{SRC_aux, "rc_bias_silu_f32", def("EW_N", M * K) + def("EW_COLS", K)};
+                ke.src = Source{SRC_aux, "rc_bias_silu_f32",
+                                def("EW_N", M * K) + def("EW_COLS", K) + def("EW_ACT", act ? 1 : 0)};
                 ke.grid = dim3((unsigned)((M * K / 4 + 255) / 256), 1, 1);
                 ke.block = dim3(256, 1, 1);
-                ke.bind = [=](const rc_args *a, char *w, std::vector<char> &b) {
+                ke.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
                     put(b, EwArgs{w + offPre, nullptr, a->in[2], a->out[0]});
                 };
                 p.kerns.push_back(ke);
@@ -462,7 +624,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             // and l of its rows, then its output accumulators
             long qb = bm / w / mf, accn = mf == 16 ? 4 : 16;
             long wslot = qb * 2 * mf + qb * (Dh / mf) * accn * 64;
-            size_t offP = chunk > 0 ? ws.add((size_t)B * Hh * nqt * maxch * w * wslot * 4) : 0;
+            size_t offP = chunk > 0 ? ws.add((size_t)B * Hh * nqt * maxch * w * wslot * 4, "partials") : 0;
             Kern k;
             double scale_log2 = 1.4426950408889634 / std::sqrt((double)Dh);
             char sbuf[64];
@@ -478,7 +640,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
                                def("CAUSAL", causal ? 1 : 0) + sbuf};
             k.grid = dim3((unsigned)(B * Hh * items), 1, 1);
             k.block = dim3(64 * w * kv(d, s, "splits"), 1, 1);
-            k.bind = [=](const rc_args *a, char *ws_base, std::vector<char> &b) {
+            k.bind = [=](const rc_args *a, char *ws_base, ArgBlob &b) {
                 put(b, AttnArgs{a->in[0], a->in[1], a->in[2], a->out[0], chunk > 0 ? ws_base + offP : nullptr});
             };
             p.kerns.push_back(k);
@@ -495,6 +657,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
         default: return fail(RC_ERR_UNSUPPORTED, "unknown operator kind");
     }
     p.workspace = ws.total;
+    p.parts = ws.parts;
     return RC_OK;
 }
 
@@ -513,8 +676,28 @@ rc_status hip_fail(hipError_t e, const char *what) {
     return fail(RC_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
-void *g_flush = nullptr;
+// Cache-flush buffers of rc_time, one per device (allocated on the first
+// flushed timing on that device, freed by rc_time_release).
+std::map<int, void *> g_flush;
 const size_t FLUSH_BYTES = (size_t)512 << 20;
+
+rc_status flush_buffer(void **out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    std::lock_guard<std::mutex> g(g_mu);
+    auto it = g_flush.find(dev);
+    if (it != g_flush.end()) {
+        *out = it->second;
+        return RC_OK;
+    }
+    void *p = nullptr;
+    e = hipMalloc(&p, FLUSH_BYTES);
+    if (e != hipSuccess) return hip_fail(e, "hipMalloc(flush buffer)");
+    g_flush[dev] = p;
+    *out = p;
+    return RC_OK;
+}
 
 }  // namespace
 
@@ -549,8 +732,7 @@ rc_status rc_precompile(const rc_op_desc *d, const rc_schedule *s, int32_t n, in
                 std::vector<char> code;
                 std::string key;
                 r = compile(k.src, code, key);
-                if (r == RC_OK && meta_int(code, ".private_segment_fixed_size") > 0)
-                    r = RC_ERR_ILLEGAL_SCHEDULE;
+                if (r == RC_OK) r = check_spill(code, k.src.entry);
             }
             st[i] = r;
             if (r != RC_OK) ++nfail;
@@ -589,11 +771,14 @@ rc_status rc_describe(const rc_op_desc *d, const rc_schedule *s, rc_kernel_info 
         const Kern &kk = p.kerns[i];
         k.grid = (int32_t)(kk.grid.x * kk.grid.y * kk.grid.z);
         k.block = (int32_t)(kk.block.x * kk.block.y * kk.block.z);
-        k.lds_bytes = (int32_t)meta_int(code, ".group_segment_fixed_size");
-        k.vgprs = (int32_t)meta_int(code, ".vgpr_count");
-        k.agprs = (int32_t)meta_int(code, ".agpr_count");
-        k.sgprs = (int32_t)meta_int(code, ".sgpr_count");
-        k.scratch_bytes = (int32_t)meta_int(code, ".private_segment_fixed_size");
+        const KernelMeta m = kernel_meta(code, p.kerns[i].src.entry);
+        if (m.ints.empty())
+            return fail(RC_ERR_COMPILE, std::string("no metadata for kernel ") + p.kerns[i].src.entry);
+        k.lds_bytes = (int32_t)m.get(".group_segment_fixed_size");
+        k.vgprs = (int32_t)m.get(".vgpr_count");
+        k.agprs = (int32_t)m.get(".agpr_count");
+        k.sgprs = (int32_t)m.get(".sgpr_count");
+        k.scratch_bytes = (int32_t)m.get(".private_segment_fixed_size");
         // Occupancy on gfx950: 512 registers per lane per SIMD shared by the
         // resident waves (the metadata's vgpr_count is the combined VGPR +
         // AGPR allocation), allocated in blocks of 8, at most 8 waves per
@@ -625,9 +810,8 @@ rc_status rc_plan_create(const rc_op_desc *d, const rc_schedule *s, rc_plan **ou
         std::string key;
         r = compile(k.src, code, key);
         if (r != RC_OK) return r;
-        if (meta_int(code, ".private_segment_fixed_size") > 0)
-            return fail(RC_ERR_ILLEGAL_SCHEDULE, std::string("spill: ") + k.src.entry +
-                                                     " needs scratch memory");
+        r = check_spill(code, k.src.entry);
+        if (r != RC_OK) return r;
         hipModule_t mod;
         {
             std::lock_guard<std::mutex> g(g_mu);
@@ -666,6 +850,30 @@ rc_status rc_plan_kernels(const rc_plan *p, int32_t *nkernels, int32_t *dominant
     return RC_OK;
 }
 
+rc_status rc_plan_buffer(const rc_plan *p, const char *name, size_t *offset, size_t *bytes) {
+    if (!p || !name || !offset || !bytes) return fail(RC_ERR_INVALID_ARGUMENT, "null argument");
+    auto it = p->parts.find(name);
+    if (it == p->parts.end()) return fail(RC_ERR_INVALID_ARGUMENT, std::string("no workspace part named ") + name);
+    *offset = it->second.first;
+    *bytes = it->second.second;
+    return RC_OK;
+}
+
+rc_status rc_time_release(void) {
+    std::lock_guard<std::mutex> g(g_mu);
+    int cur = 0;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    rc_status r = RC_OK;
+    for (auto &kv : g_flush) {
+        if ((e = hipSetDevice(kv.first)) != hipSuccess || (e = hipFree(kv.second)) != hipSuccess)
+            r = hip_fail(e, "hipFree(flush buffer)");
+    }
+    g_flush.clear();
+    (void)hipSetDevice(cur);
+    return r;
+}
+
 static rc_status check_args(const rc_plan *p, const rc_args *a, void *ws, size_t ws_bytes) {
     if (!p || !a || a->struct_size < sizeof(rc_args)) return fail(RC_ERR_INVALID_ARGUMENT, "null plan or args");
     int ni = n_inputs(p->desc.kind);
@@ -690,12 +898,12 @@ static rc_status launch_impl(const rc_plan *p, const rc_args *a, void *ws, size_
     if (events && nevents < (int32_t)p->kerns.size() + 1)
         return fail(RC_ERR_INVALID_ARGUMENT, "need nkernels + 1 events");
     hipStream_t st = (hipStream_t)stream;
-    std::vector<char> blob;
+    ArgBlob blob;
     for (size_t i = 0; i < p->kerns.size(); ++i) {
         const Kern &k = p->kerns[i];
         k.bind(a, (char *)ws, blob);
-        size_t sz = blob.size();
-        void *cfg[] = {HIP_LAUNCH_PARAM_BUFFER_POINTER, blob.data(), HIP_LAUNCH_PARAM_BUFFER_SIZE, &sz,
+        size_t sz = blob.size;
+        void *cfg[] = {HIP_LAUNCH_PARAM_BUFFER_POINTER, blob.data, HIP_LAUNCH_PARAM_BUFFER_SIZE, &sz,
                        HIP_LAUNCH_PARAM_END};
         if (events) {
             hipError_t e = hipEventRecord((hipEvent_t)events[i], st);
@@ -716,6 +924,16 @@ rc_status rc_launch(const rc_plan *p, const rc_args *a, void *workspace, size_t 
                     void *stream) {
     return launch_impl(p, a, workspace, ws_bytes, stream, nullptr, 0);
 }
+
+}  // extern "C"
+
+namespace rc {
+rc_status launch_plan(const rc_plan *p, const rc_args *a, void *workspace, size_t ws_bytes, void *stream) {
+    return launch_impl(p, a, workspace, ws_bytes, stream, nullptr, 0);
+}
+}  // namespace rc
+
+extern "C" {
 
 rc_status rc_launch_timed(const rc_plan *p, const rc_args *a, void *workspace, size_t ws_bytes,
                           void *stream, void **events, int32_t nevents) {
@@ -749,28 +967,35 @@ rc_status rc_time(const rc_plan *p, const rc_args *a, void *ws, size_t ws_bytes,
     if (o) opt = *o;
     if (opt.repeat < 1 || opt.warmup < 0) return fail(RC_ERR_INVALID_ARGUMENT, "repeat must be >= 1");
     hipStream_t st = (hipStream_t)stream;
-    if (opt.flush && !g_flush) {
-        hipError_t e = hipMalloc(&g_flush, FLUSH_BYTES);
-        if (e != hipSuccess) return hip_fail(e, "hipMalloc(flush buffer)");
+    void *flush = nullptr;
+    if (opt.flush) {
+        rc_status r = flush_buffer(&flush);
+        if (r != RC_OK) return r;
     }
     for (int i = 0; i < opt.warmup; ++i) {
         rc_status r = rc_launch(p, a, ws, ws_bytes, stream);
         if (r != RC_OK) return r;
     }
     int nk = (int)p->kerns.size();
-    std::vector<hipEvent_t> ev((size_t)opt.repeat * (nk + 1));
-    for (auto &e : ev) {
-        hipError_t he = hipEventCreate(&e);
-        if (he != hipSuccess) return hip_fail(he, "hipEventCreate");
-    }
+    std::vector<hipEvent_t> ev;
+    ev.reserve((size_t)opt.repeat * (nk + 1));
     rc_status r = RC_OK;
+    for (size_t i = 0; i < (size_t)opt.repeat * (nk + 1) && r == RC_OK; ++i) {
+        hipEvent_t e;
+        hipError_t he = hipEventCreate(&e);
+        if (he != hipSuccess)
+            r = hip_fail(he, "hipEventCreate");
+        else
+            ev.push_back(e);
+    }
     for (int i = 0; i < opt.repeat && r == RC_OK; ++i) {
         if (opt.flush) {
-            hipError_t e = hipMemsetAsync(g_flush, i & 0xFF, FLUSH_BYTES, st);
+            hipError_t e = hipMemsetAsync(flush, i & 0xFF, FLUSH_BYTES, st);
             if (e != hipSuccess) r = hip_fail(e, "flush");
         }
         if (r == RC_OK) r = launch_impl(p, a, ws, ws_bytes, stream, (void **)&ev[(size_t)i * (nk + 1)], nk + 1);
     }
+    // the events must have completed before they are read or destroyed
     hipError_t se = hipStreamSynchronize(st);
     if (r == RC_OK && se != hipSuccess) r = hip_fail(se, "hipStreamSynchronize");
     if (r == RC_OK) {

@@ -23,6 +23,7 @@ STATUS = {0: "RC_OK", 1: "RC_ERR_INVALID_ARGUMENT", 2: "RC_ERR_ILLEGAL_SCHEDULE"
 
 RC_OP_GEMM_F32, RC_OP_ATTENTION, RC_OP_GATED_MLP, RC_OP_MOE, RC_OP_CONV2D = 1, 2, 3, 4, 5
 RC_FLAG_CAUSAL = 1
+RC_FLAG_NO_ACT = 2
 RC_POLICY_RANDOM, RC_POLICY_UCT, RC_POLICY_EXHAUSTIVE = 0, 1, 2
 MAX_DIMS, MAX_KNOBS = 8, 32
 
@@ -132,6 +133,9 @@ _SIGS = [
     ("rc_plan_workspace", ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_size_t)]),
     ("rc_plan_kernels", ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32),
                                        ctypes.POINTER(ctypes.c_int32)]),
+    ("rc_plan_buffer", ctypes.c_int, [ctypes.c_void_p, ctypes.c_char_p, ctypes.POINTER(ctypes.c_size_t),
+                                      ctypes.POINTER(ctypes.c_size_t)]),
+    ("rc_time_release", ctypes.c_int, []),
     ("rc_launch", ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(rc_args), ctypes.c_void_p,
                                  ctypes.c_size_t, ctypes.c_void_p]),
     ("rc_launch_timed", ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(rc_args), ctypes.c_void_p,
@@ -416,6 +420,13 @@ class Plan:
             _lib.rc_plan_destroy(self.h)
             self.h = None
 
+    def buffer(self, name: str):
+        """(byte offset, bytes) of a named part of the workspace."""
+        off, n = ctypes.c_size_t(), ctypes.c_size_t()
+        _check(lib().rc_plan_buffer(self.h, name.encode(), ctypes.byref(off), ctypes.byref(n)),
+               "rc_plan_buffer")
+        return off.value, n.value
+
     def workspace(self, device="cuda"):
         import torch
         if self.workspace_bytes == 0:
@@ -488,6 +499,11 @@ class Plan:
         _check(lib().rc_time(self.h, ctypes.byref(a), _ptr(workspace), wsz, _stream_ptr(stream),
                              ctypes.byref(o), ctypes.byref(t)), "rc_time")
         return t
+
+
+def time_release() -> None:
+    """Free rc_time's cache-flush buffers."""
+    _check(lib().rc_time_release(), "rc_time_release")
 
 
 # ---------------------------------------------------------------------------

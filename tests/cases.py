@@ -39,6 +39,11 @@ SMALL = {
     "conv": (rc.RC_OP_CONV2D, (2, 16, 12, 64, 64, 3, 3, 1), 0),
     # 90 output pixels: a partial last M tile for every tile_m
     "conv_ragged": (rc.RC_OP_CONV2D, (1, 10, 9, 64, 64, 3, 3, 1), 0),
+    # 320 output channels: the tile_n values 80, 160 and 320 that only
+    # this channel count admits
+    "conv_k320": (rc.RC_OP_CONV2D, (1, 8, 8, 64, 320, 3, 3, 1), 0),
+    # 512 keys: work items of 8 key tiles
+    "attn_causal_512": (rc.RC_OP_ATTENTION, (1, 2, 512, 128), rc.RC_FLAG_CAUSAL),
     # degenerate sizes: one row, one token, one key, one output pixel
     "gemm_one": (rc.RC_OP_GEMM_F32, (1, 1, 1), 0),
     "gemm_row": (rc.RC_OP_GEMM_F32, (1, 300, 77), 0),
@@ -226,6 +231,24 @@ SCHEDULES = {
     ],
 }
 
+SCHEDULES["conv_k320"] = [
+    _block("", 64, 80, 64, 1, 1, 16, 2, 8, 1, 1, 0) + ",fuse=1",
+    _block("", 32, 160, 64, 1, 2, 16, 5, 8, 1, 1, 1) + ",fuse=1",
+    _block("", 64, 320, 32, 2, 2, 16, 3, 8, 1, 1, 0) + ",fuse=0",
+    _block("", 16, 320, 64, 1, 4, 16, 2, 4, 1, 0, 0) + ",fuse=1",
+    _block("", 64, 320, 64, 2, 2, 32, 2, 8, 1, 1, 1) + ",fuse=1",
+    _block("", 64, 160, 64, 2, 2, 16, 1, 8, 1, 1, 0, 2) + ",fuse=0",
+]
+SCHEDULES["attn_causal_512"] = [
+    "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=2,occ=2,chunk=8",
+    "block_m=64,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=1,order=0,chunk=8",
+    "block_m=32,block_n=32,waves=2,mfma=16,stages=2,vec=8,unroll=1,order=1,chunk=8",
+    "block_m=64,block_n=32,waves=2,mfma=32,stages=2,vec=8,unroll=1,order=0,splits=4,chunk=8",
+    "block_m=64,block_n=64,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=1,occ=1,splits=2,chunk=4",
+]
+SCHEDULES["gemm_skinny"].append(
+    "tile_m=16,tile_n=64,tile_k=16,waves_m=1,waves_n=2,vec=4,stages=3,unroll=1,layout=0,splits=32")
+
 # the ragged shapes run every schedule of their full-tile counterparts that
 # is legal for them (the paired order needs an even number of query tiles)
 SCHEDULES["mlp_ragged"] = SCHEDULES["mlp"]
@@ -314,9 +337,60 @@ RAGGED_FULL = [
 ]
 
 
+# Plain bf16 GEMMs (1 x 1 convolutions without padding or activation,
+# M = 512 pixels, C = 256 -> K = 128) for integer-input bitwise checks.
+GEMM_1X1 = [
+    "",
+    _block("", 64, 64, 64, 2, 2, 16, 2, 8, 1, 1, 1) + ",fuse=1",
+    _block("", 128, 128, 32, 2, 2, 32, 3, 8, 1, 1, 0) + ",fuse=1",
+    _block("", 32, 64, 128, 1, 2, 16, 5, 8, 2, 1, 1) + ",fuse=0",
+    _block("", 64, 32, 64, 2, 1, 16, 1, 4, 1, 0, 0) + ",fuse=1",
+    _block("", 256, 128, 64, 4, 2, 16, 2, 8, 1, 1, 1, 2) + ",fuse=1",
+]
+GEMM_1X1_OP = (rc.RC_OP_CONV2D, (2, 16, 16, 256, 128, 1, 1, 0), rc.RC_FLAG_NO_ACT)
+CONV_FULL_ALT = _block("", 64, 64, 64, 4, 2, 16, 2, 8, 1, 1, 1) + ",fuse=1"
+
+
+# Schedules the search can emit: random legal transformation sequences of
+# length 12 from P0 (the rollouts of Sec. 3.2), seeded, at the small shapes.
+WALK_KEYS = ("gemm", "attn_causal", "mlp", "moe", "conv")
+WALK_COUNT = 40
+
+
+def random_walks(key, n=WALK_COUNT, seed=20260):
+    from paper_2506_01374_amd import tune
+    op = small_op(key)
+    return [str(s) for s in tune.random_walk_space(op, n, seed + WALK_KEYS.index(key), horizon=12)]
+
+
+def walk_compile_jobs():
+    """(op, [schedules]) of the random-walk cases; some may spill (rejected
+    at compile time, which the tests accept)."""
+    jobs = []
+    for key in WALK_KEYS:
+        op = small_op(key)
+        jobs.append((op, [op.from_string(s) for s in random_walks(key)]))
+    return jobs
+
+
 def all_compile_jobs():
     """(op, [schedules]) pairs for ahead-of-time compilation."""
     jobs = []
+    # the convolutions without activation (integer and closed-form checks)
+    for key in ("conv", "conv_ragged", "conv_k320"):
+        kind, dims, _ = SMALL[key]
+        op = rc.Op(kind, dims, rc.RC_FLAG_NO_ACT)
+        jobs.append((op, [op.from_string(t) for t in SCHEDULES[key] if op.from_string(t).validate() == ""]))
+    op = rc.Op(*GEMM_1X1_OP)
+    jobs.append((op, [op.from_string(t) for t in GEMM_1X1]))
+    op = rc.Op(rc.RC_OP_CONV2D, W.workload_op("conv3x3_n2_64x64_c320_k320").dims, rc.RC_FLAG_NO_ACT)
+    jobs.append((op, [op.from_string(TUNED["conv3x3_n2_64x64_c320_k320"]), op.default(),
+                      op.from_string(CONV_FULL_ALT)]))
+    moe = W.workload_op("moe_t4096_h2048_e64_i1408_top6")
+    for dims in ((256, 256, 8, 128, 2), (256, 256, 8, 128, 1), (8192, 256, 64, 128, 6)):
+        op = rc.Op(rc.RC_OP_MOE, dims)
+        jobs.append((op, [op.from_string(t) for t in SCHEDULES["moe"][:4]]))
+    del moe
     for key, lst in SCHEDULES.items():
         op = small_op(key)
         jobs.append((op, [op.from_string(s) for s in lst]))
