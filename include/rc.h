@@ -291,6 +291,23 @@ rc_status rc_launch(const rc_plan *p, const rc_args *a, void *workspace, size_t 
 rc_status rc_launch_timed(const rc_plan *p, const rc_args *a, void *workspace,
                           size_t ws_bytes, void *stream, void **events, int32_t nevents);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): rc_launch
+ * with the workspace taken from a static device array inside the library
+ * instead of a caller buffer.  The caller still passes inputs and outputs.
+ * The array holds rc_static_scratch_bytes() bytes (64 MiB) on each device
+ * the library runs on, from the first call on that device until the process
+ * ends; a plan whose workspace is larger is rejected with
+ * RC_ERR_OUT_OF_MEMORY before any GPU work (use rc_launch).  The call
+ * allocates nothing: no hipMalloc, hipFree or other allocating routine
+ * (its first call on a device looks the array's address up once).  Every
+ * call on one device shares that device's array and leaves its contents
+ * behind; calls that overlap on one device (concurrent streams or host
+ * threads) race, so the caller serialises them.  No kernel needs the
+ * array cleared. */
+rc_status rc_launch_static(const rc_plan *p, const rc_args *a, void *stream);
+size_t rc_static_scratch_bytes(void);
+
 typedef struct rc_time_opts {
     uint32_t struct_size;
     int32_t warmup;   /* untimed launches first (default 3) */

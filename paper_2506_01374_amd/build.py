@@ -35,15 +35,32 @@ def gen_kernel_sources() -> str:
     return out
 
 
+def build_static_object(verbose: bool = False) -> str:
+    """rc_static.hip holds a file-scope device array (the no-allocation
+    launch's workspace), so hipcc compiles it for gfx950 and the host."""
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    obj = os.path.join(HERE, "rc_static.o")
+    cmd = [os.path.join(rocm, "bin", "hipcc"), "-c", "-fPIC", "-O2", "-std=c++17",
+           "--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           "-I", os.path.join(ROOT, "include"), "-I", CSRC, os.path.join(CSRC, "rc_static.hip"),
+           "-o", obj]
+    if verbose:
+        print(" ".join(cmd))
+    subprocess.check_call(cmd)
+    return obj
+
+
 def build_lib(verbose: bool = False) -> str:
     gen_kernel_sources()
     lib = os.path.join(HERE, "librc.so")
     srcs = [os.path.join(CSRC, f) for f in ("rc_core.cpp", "rc_plan.cpp", "rc_search.cpp")]
+    obj = build_static_object(verbose)
     rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
-    # Host-only C++: the kernels are compiled for gfx950 by hipRTC per schedule.
+    # Host C++: the operator kernels are compiled for gfx950 by hipRTC per
+    # schedule; rc_static.o carries the static workspace array.
     cmd = ["g++", "-O2", "-std=c++17", "-fPIC", "-shared", "-Wall", "-D__HIP_PLATFORM_AMD__",
            "-I", os.path.join(ROOT, "include"), "-I", CSRC, "-I", os.path.join(rocm, "include"),
-           *srcs, "-o", lib + ".tmp", "-L", os.path.join(rocm, "lib"),
+           *srcs, obj, "-o", lib + ".tmp", "-L", os.path.join(rocm, "lib"),
            "-Wl,-rpath," + os.path.join(rocm, "lib"), "-lamdhip64", "-lhiprtc", "-ldl",
            "-lpthread"]
     if verbose:

@@ -141,6 +141,8 @@ _SIGS = [
     ("rc_launch_timed", ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(rc_args), ctypes.c_void_p,
                                        ctypes.c_size_t, ctypes.c_void_p,
                                        ctypes.POINTER(ctypes.c_void_p), ctypes.c_int32]),
+    ("rc_launch_static", ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(rc_args), ctypes.c_void_p]),
+    ("rc_static_scratch_bytes", ctypes.c_size_t, []),
     ("rc_time_opts_init", None, [ctypes.POINTER(rc_time_opts)]),
     ("rc_time", ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(rc_args), ctypes.c_void_p,
                                ctypes.c_size_t, ctypes.c_void_p, ctypes.POINTER(rc_time_opts),
@@ -475,6 +477,11 @@ class Plan:
         wsz = 0 if workspace is None else workspace.numel() * workspace.element_size()
         _check(lib().rc_launch(self.h, ctypes.byref(a), _ptr(workspace), wsz, _stream_ptr(stream)),
                "rc_launch")
+
+    def launch_static(self, inputs, output, stream=None) -> None:
+        """rc_launch_static: the workspace is the library's static array."""
+        a = self._args(inputs, output)
+        _check(lib().rc_launch_static(self.h, ctypes.byref(a), _stream_ptr(stream)), "rc_launch_static")
 
     def launch_timed(self, inputs, output, events, workspace=None, stream=None) -> None:
         """events: list of nkernels + 1 torch.cuda.Event(enable_timing=True),

@@ -363,6 +363,20 @@ def random_walks(key, n=WALK_COUNT, seed=20260):
     return [str(s) for s in tune.random_walk_space(op, n, seed + WALK_KEYS.index(key), horizon=12)]
 
 
+# The no-allocation launch against the workspace launch: (kind, larger
+# dims, smaller dims, flags, schedule) for every operator whose kernels use
+# a workspace.
+NOALLOC_PAIRS = [
+    (rc.RC_OP_GATED_MLP, (256, 256, 512), (200, 256, 512), 0, SCHEDULES["mlp"][1]),
+    (rc.RC_OP_GATED_MLP, (256, 256, 512), (40, 256, 512), 0, SCHEDULES["mlp"][3]),
+    (rc.RC_OP_MOE, (256, 256, 8, 128, 2), (64, 256, 8, 128, 2), 0, SCHEDULES["moe"][1]),
+    (rc.RC_OP_MOE, (256, 256, 8, 128, 2), (1, 256, 8, 128, 2), 0, SCHEDULES["moe"][3]),
+    (rc.RC_OP_ATTENTION, (1, 2, 512, 128), (1, 2, 384, 128), rc.RC_FLAG_CAUSAL, SCHEDULES["attn_causal_512"][0]),
+    (rc.RC_OP_GEMM_F32, (16, 256, 1024), (5, 128, 512), 0, SCHEDULES["gemm_skinny"][3]),
+    (rc.RC_OP_CONV2D, (2, 16, 12, 64, 64, 3, 3, 1), (1, 10, 9, 64, 64, 3, 3, 1), 0, SCHEDULES["conv"][3]),
+]
+
+
 def walk_compile_jobs():
     """(op, [schedules]) of the random-walk cases; some may spill (rejected
     at compile time, which the tests accept)."""
@@ -386,6 +400,10 @@ def all_compile_jobs():
     op = rc.Op(rc.RC_OP_CONV2D, W.workload_op("conv3x3_n2_64x64_c320_k320").dims, rc.RC_FLAG_NO_ACT)
     jobs.append((op, [op.from_string(TUNED["conv3x3_n2_64x64_c320_k320"]), op.default(),
                       op.from_string(CONV_FULL_ALT)]))
+    for kind, big, small, flags, text in NOALLOC_PAIRS:
+        for dims in (big, small):
+            op = rc.Op(kind, dims, flags)
+            jobs.append((op, [op.from_string(text)]))
     moe = W.workload_op("moe_t4096_h2048_e64_i1408_top6")
     for dims in ((256, 256, 8, 128, 2), (256, 256, 8, 128, 1), (8192, 256, 64, 128, 6)):
         op = rc.Op(rc.RC_OP_MOE, dims)
