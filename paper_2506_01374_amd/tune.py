@@ -130,6 +130,206 @@ class GpuEvaluator:
         return rec
 
 
+def _compile_one(job):
+    """Worker process: compile one schedule into the code-object cache."""
+    kind, dims, flags, text, cache = job
+    if cache:
+        rc.set_cache_dir(cache)
+    op = rc.Op(kind, dims, flags)
+    return rc.precompile(op, [op.from_string(text)], nthreads=1)[0]
+
+
+class ParallelGpuEvaluator:
+    """GpuEvaluator shared by several searches running in threads: each
+    schedule is compiled in a pool of worker processes (hipRTC serialises
+    the compilations of one process), and the GPU measurements are
+    serialised by a lock so that no two timings overlap.  A schedule
+    requested by several searches is compiled and measured once.
+
+    A schedule whose first timed launch takes longer than `slow_ms` is
+    recorded from that launch alone (marked "coarse"): its reward is far
+    below the best and more repeats would only spend GPU time."""
+
+    def __init__(self, op: rc.Op, jobs: int = 8, repeat: int = 10, warmup: int = 2,
+                 slow_ms: float = 50.0, cache_dir: Optional[str] = None, log=None,
+                 time_fn=None, compile_fn=None):
+        import threading
+        from concurrent.futures import ProcessPoolExecutor
+        import multiprocessing as mp
+        self.op, self.slow_ms, self.cache_dir = op, slow_ms, cache_dir
+        # time_fn / compile_fn replace the GPU timing and the worker-process
+        # compilation (CPU tests of the bookkeeping)
+        self.inner = None if time_fn else GpuEvaluator(op, repeat=repeat, warmup=warmup, log=None)
+        self._time_fn = time_fn or self._time
+        self._compile_fn = compile_fn
+        self.pool = None if compile_fn else ProcessPoolExecutor(max_workers=jobs,
+                                                                mp_context=mp.get_context("spawn"))
+        self.gpu = threading.Lock()
+        self.mu = threading.Lock()
+        self.pending: Dict[str, "threading.Event"] = {}
+        self.cache: Dict[str, dict] = {}
+        self.log = log
+        self.order: List[str] = []     # distinct schedules in measurement order
+
+    def _time(self, sched: rc.Schedule) -> dict:
+        inner = self.inner
+        rec = {"schedule": str(sched)}
+        try:
+            plan = rc.Plan(self.op, sched)
+            ws = plan.workspace()
+            ins = inner._inputs(sched)
+            t = plan.time(ins, inner.out, ws, warmup=0, repeat=1, flush=True)
+            if t.median_ms > self.slow_ms:
+                rec.update(coarse=True)
+            else:
+                t = plan.time(ins, inner.out, ws, warmup=inner.warmup, repeat=inner.repeat, flush=True)
+            rec.update(valid=True, ms=t.median_ms, q1_ms=t.q1_ms, q3_ms=t.q3_ms, tflops=t.tflops,
+                       gbps=t.gbps, reward=reward_of(self.op, t.median_ms),
+                       kernel_ms=list(t.kernel_ms)[: t.nkernels])
+            del plan, ws
+        except rc.RCError as e:
+            rec.update(valid=False, error=str(e)[:300])
+        return rec
+
+    def measure(self, sched: rc.Schedule) -> dict:
+        import threading
+        text = str(sched)
+        with self.mu:
+            if text in self.cache:
+                return self.cache[text]
+            ev = self.pending.get(text)
+            owner = ev is None
+            if owner:
+                ev = self.pending[text] = threading.Event()
+        if not owner:
+            ev.wait()
+            return self.cache[text]
+        t0 = time.time()
+        job = (self.op.kind, self.op.dims, self.op.flags, text, self.cache_dir)
+        st = self._compile_fn(job) if self._compile_fn else self.pool.submit(_compile_one, job).result()
+        t1 = time.time()
+        if st != 0:
+            why = "spill" if st == rc.RC_ERR_ILLEGAL_SCHEDULE else f"compile status {st}"
+            rec = {"schedule": text, "valid": False, "error": why}
+        else:
+            with self.gpu:
+                rec = self._time_fn(sched)
+        rec["compile_s"], rec["eval_s"] = t1 - t0, time.time() - t0
+        with self.mu:
+            self.cache[text] = rec
+            self.order.append(text)
+            del self.pending[text]
+            if self.log:
+                self.log.write(json.dumps({"kind": "measure", **rec}) + "\n")
+                self.log.flush()
+        ev.set()
+        return rec
+
+    def close(self):
+        if self.pool is not None:
+            self.pool.shutdown()
+
+
+PAPER_AXES = (18, 36, 72, 150, 200)   # sample counts of the paper's best-vs-samples table
+
+
+def _policy_args(name: str):
+    """'random', 'uct', 'uct+feedback', 'uct+feedback+surrogate' (B = 4 with
+    the surrogate, as in the replay study), ..."""
+    parts = name.split("+")
+    return {"policy": parts[0], "proposer": "feedback" if "feedback" in parts else None,
+            "surrogate": "surrogate" in parts, "branching": 4 if "surrogate" in parts else 2}
+
+
+def summarize_campaign(runs: List[dict], ref_reward: float, budget: int) -> Dict[str, dict]:
+    """Per policy: mean best-so-far (as a fraction of the reference reward)
+    at the paper's sample counts, and samples to reach 90 % / 99 % of the
+    reference per seed."""
+    import statistics
+    out: Dict[str, dict] = {}
+    by: Dict[str, List[dict]] = {}
+    for r in runs:
+        by.setdefault(r["policy_name"], []).append(r)
+    for name, rs in by.items():
+        rs = sorted(rs, key=lambda r: r["seed"])
+        at = {}
+        for n in PAPER_AXES:
+            if n > budget:
+                continue
+            vals = [(r["curve"][min(n, len(r["curve"])) - 1] if r["curve"] else 0.0) / ref_reward for r in rs]
+            at[str(n)] = {"mean": statistics.fmean(vals),
+                          "stderr": statistics.stdev(vals) / math.sqrt(len(vals)) if len(vals) > 1 else 0.0}
+
+        def reach(frac):
+            got = []
+            for r in rs:
+                k = next((i + 1 for i, v in enumerate(r["curve"]) if v >= frac * ref_reward), None)
+                got.append(k)
+            hit = [k for k in got if k is not None]
+            return {"per_seed": got, "reached": len(hit), "of": len(got),
+                    "median": statistics.median(hit) if hit else None}
+        best = max(rs, key=lambda r: r["best_reward"])
+        out[name] = {"best_so_far_over_reference": at, "samples_to_90pct": reach(0.90),
+                     "samples_to_99pct": reach(0.99),
+                     "best_over_reference": best["best_reward"] / ref_reward,
+                     "best_schedule": best["best"], "seeds": [r["seed"] for r in rs]}
+    return out
+
+
+def run_campaign(op: rc.Op, name: str, policies: List[str], seeds: List[int], budget: int,
+                 reference: str, jobs: int, out_path: str, cache_dir: Optional[str],
+                 repeat: int = 10, slow_ms: float = 50.0, log=None, time_fn=None, compile_fn=None) -> dict:
+    """Every (policy, seed) search in its own thread against one shared
+    ParallelGpuEvaluator; the reference (tuned) schedule is measured the
+    same way before and after."""
+    import threading
+    ev = ParallelGpuEvaluator(op, jobs=jobs, repeat=repeat, slow_ms=slow_ms, cache_dir=cache_dir, log=log,
+                              time_fn=time_fn, compile_fn=compile_fn)
+    ref_sched = op.from_string(reference)
+    ref0 = ev._time_fn(ref_sched)
+    runs: List[dict] = []
+    errors: List[str] = []
+    t0 = time.time()
+
+    def one(pname, seed):
+        try:
+            a = _policy_args(pname)
+            r = run_search(op, ev, a["policy"], budget, seed, branching=a["branching"],
+                           proposer=a["proposer"], surrogate=a["surrogate"])
+            r["policy_name"] = pname
+            r["wall_s"] = time.time() - t0
+            runs.append(r)
+            print(f"[campaign] {name} {pname} seed {seed}: best {r['best_reward']:.4f} "
+                  f"after {r['valid']} samples ({time.time() - t0:.0f}s)", flush=True)
+        except Exception as e:      # noqa: BLE001 - reported in the record
+            errors.append(f"{pname} seed {seed}: {e!r}")
+            print(f"[campaign] {name} {pname} seed {seed} failed: {e!r}", flush=True)
+
+    threads = [threading.Thread(target=one, args=(p, s)) for p in policies for s in seeds]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    ref1 = ev._time_fn(ref_sched)
+    ev.close()
+    ref_reward = max(ref0.get("reward", 0.0), ref1.get("reward", 0.0))
+    rec = {"workload": name, "dims": list(op.dims), "flags": op.flags, "budget": budget,
+           "seeds": seeds, "policies": policies,
+           "measurement": (f"cold: a 512 MiB buffer overwritten before each timed launch; median of "
+                           f"{repeat} launches (one launch when it exceeds {slow_ms:g} ms)"),
+           "reward": "fraction of the binding roofline (bf16 MFMA peak or HBM bandwidth) at the median",
+           "reference_schedule": reference,
+           "reference_reward": ref_reward, "reference_us": [ref0.get("ms", 0) * 1e3, ref1.get("ms", 0) * 1e3],
+           "distinct_schedules": len(ev.order),
+           "invalid": sum(1 for r in ev.cache.values() if not r.get("valid")),
+           "wall_s": time.time() - t0, "errors": errors,
+           "summary": summarize_campaign(runs, ref_reward, budget) if runs else {},
+           "runs": [{k: v for k, v in r.items()} for r in sorted(runs, key=lambda r: (r["policy_name"], r["seed"]))]}
+    with open(out_path, "w") as f:
+        json.dump(rec, f, indent=1)
+    return rec
+
+
 class TableEvaluator:
     """Measured samples replayed from a table: a previous run's JSONL, or a
     TSV of one sub-space (comment lines, a '# fixed: knob=v,...' line, a
@@ -387,6 +587,13 @@ def main(argv=None):
     ap.add_argument("--column", default=None, help="timing column of a TSV table (default: the last)")
     ap.add_argument("--threads", type=int, default=os.cpu_count() or 8)
     ap.add_argument("--cache-dir", default=os.path.join(HERE, "jit_cache"))
+    ap.add_argument("--campaign", default=None, metavar="POLICIES",
+                    help="comma-separated policies (random, uct, uct+feedback, uct+feedback+surrogate) "
+                         "searched concurrently over --seeds with parallel compilation; writes "
+                         "<out>/<workload>.campaign.json")
+    ap.add_argument("--jobs", type=int, default=12, help="compile worker processes (--campaign)")
+    ap.add_argument("--slow-ms", type=float, default=50.0,
+                    help="a schedule slower than this on its first launch is timed once (--campaign)")
     args = ap.parse_args(argv)
 
     rc.set_cache_dir(args.cache_dir)
@@ -409,6 +616,21 @@ def main(argv=None):
                 bad += sum(1 for x in st if x != 0)
                 print(f"compiled {min(i + chunk, len(space))}/{len(space)} ({bad} rejected) "
                       f"{time.time() - t0:.0f}s", flush=True)
+        return
+
+    if args.campaign:
+        tuned = json.load(open(os.path.join(HERE, "tuned.json")))
+        pols = [p for p in args.campaign.split(",") if p]
+        path = os.path.join(args.out, f"{args.workload}.campaign.json")
+        log = open(os.path.join(args.out, f"{args.workload}.campaign.jsonl"), "a")
+        rec = run_campaign(op, args.workload, pols, _parse_seeds(args.seeds), args.budget,
+                           tuned[args.workload], args.jobs, path, args.cache_dir, repeat=args.repeat,
+                           slow_ms=args.slow_ms, log=log)
+        print(json.dumps({k: rec[k] for k in ("workload", "reference_reward", "distinct_schedules",
+                                               "invalid", "wall_s", "errors")}), flush=True)
+        for pname, sm in rec["summary"].items():
+            print(pname, json.dumps({k: sm[k] for k in ("best_over_reference", "samples_to_90pct",
+                                                         "samples_to_99pct")}), flush=True)
         return
 
     tag = args.policy + (f"+{args.proposer}" if args.proposer else "") + ("+surrogate" if args.surrogate else "")

@@ -402,3 +402,38 @@ def test_causal_vec8_table_warm_optimum_is_tuned():
     bc = max((r for r in cold.table.values() if r["valid"]), key=lambda r: r["reward"])
     assert bw["schedule"] == str(op.from_string(tuned))
     assert op.from_string(bc["schedule"]).as_dict()["splits"] == 1
+
+
+def test_campaign_threads_share_measurements_and_summarise(tmp_path):
+    # Several searches in threads against one evaluator: each distinct
+    # schedule is measured once, the record holds one run per (policy,
+    # seed), and samples-to-reach counts follow the curves.
+    import json
+    import threading
+    from paper_2506_01374_amd import tune
+    op = rc.Op(rc.RC_OP_GEMM_F32, (128, 128, 128))
+    calls = {}
+    lock = threading.Lock()
+
+    def fake_time(sched):
+        d = sched.as_dict()
+        with lock:
+            calls[str(sched)] = calls.get(str(sched), 0) + 1
+        score = (d["tile_m"] + d["tile_n"]) / 128.0 + 0.1 * d["vec"] + 0.05 * d["waves_m"]
+        return {"schedule": str(sched), "valid": True, "ms": 1.0 / score, "reward": score / 2.0}
+
+    ref = "tile_m=64,tile_n=64,tile_k=16,waves_m=2,waves_n=1,vec=4,stages=2,unroll=1,layout=0"
+    out = tmp_path / "c.json"
+    rec = tune.run_campaign(op, "gemm_f32_128", ["random", "uct"], [0, 1, 2], 24, ref, 1, str(out), None,
+                            time_fn=fake_time, compile_fn=lambda job: 0)
+    assert not rec["errors"], rec["errors"]
+    assert len(rec["runs"]) == 6
+    assert all(n == 1 for s, n in calls.items() if s != str(op.from_string(ref))), calls
+    saved = json.load(open(out))
+    for pname in ("random", "uct"):
+        sm = saved["summary"][pname]
+        assert set(sm["best_so_far_over_reference"]) == {"18"}
+        for r in (r for r in saved["runs"] if r["policy_name"] == pname):
+            k = next((i + 1 for i, v in enumerate(r["curve"]) if v >= 0.9 * saved["reference_reward"]), None)
+            assert k == sm["samples_to_90pct"]["per_seed"][sm["seeds"].index(r["seed"])]
+            assert all(b >= a for a, b in zip(r["curve"], r["curve"][1:]))
