@@ -244,6 +244,8 @@ rc_status rc_plan_kernels(const rc_plan *p, int32_t *nkernels, int32_t *dominant
  *     the gate/up and down GEMMs: exclusive prefix sums of
  *     ceil(count_e / tile_m)); "hidden" bf16 [T * topk][I] (permuted
  *     rows); "expert_out" bf16 [T * topk][Hd] (permuted rows);
+ *     "block_counts" int32 [ceil(T * topk / 1024)][E] (routed rows per
+ *     block of 1024 consecutive rows and expert);
  *   RC_OP_GATED_MLP: "hidden" bf16 [T][I];
  *   unfused epilogues: "gate.f32", "up.f32" or "pre.f32" (fp32 [rows][cols]);
  *   RC_OP_ATTENTION with chunk > 0: "partials"; RC_OP_GEMM_F32 streaming
@@ -325,7 +327,7 @@ typedef struct rc_timing {
     double gbps;          /* rc_op_bytes / median */
     double frac_flops;    /* tflops / peak */
     double frac_bytes;    /* gbps / HBM peak */
-    double kernel_ms[4];  /* median duration of each kernel */
+    double kernel_ms[8];  /* median duration of each kernel (the first 8) */
 } rc_timing;
 
 void rc_time_opts_init(rc_time_opts *o);

@@ -66,8 +66,54 @@ extern "C" __global__ __launch_bounds__(256) void rc_bias_silu_f32(EwArgs a) {
 #ifdef MOE_T
 #define MOE_ROWS (MOE_T * MOE_TOPK)
 
+// Routing preparation: a stable counting sort of the routed rows by expert
+// in two kernels over blocks of PREP_T consecutive rows (one row per
+// thread; expert ids out of range are clamped to expert 0 so that no write
+// can leave its buffer).
+//   rc_moe_hist: block b counts its rows per expert (LDS atomics) and
+//     writes the counts to counts[b][*].
+//   rc_moe_prep: block b reads the whole counts table; thread e sums
+//     column e (all blocks: the expert's total; blocks before b: the rows
+//     of expert e that precede this block).  A block-wide exclusive scan of
+//     the totals gives offsets[] and, from ceil(count / tile), the tile
+//     starts of both expert GEMMs (block 0 writes them).  Within the block,
+//     the lanes of a wave holding the same expert are found with one
+//     ballot per bit of the expert id, the lowest of them records the
+//     group's size for its wave, and an exclusive prefix over the waves
+//     gives each wave's first row per expert.  A row's permuted position is
+//     offsets[e] + (rows of e in earlier blocks) + (rows of e in earlier
+//     waves of the block) + (lanes of e below it in its wave): rows keep
+//     their order within an expert, so the result is deterministic.
+#define PREP_T 1024
+#define PREP_W (PREP_T / 64)
+#define PREP_NB ((MOE_ROWS + PREP_T - 1) / PREP_T)
+#define PREP_BITS (MOE_E <= 1 ? 1 : 32 - __builtin_clz(MOE_E - 1))
+
+struct MoeHistArgs {
+    const int *ids;
+    int *counts;           // [PREP_NB][E]
+};
+
+__device__ __forceinline__ int prep_id(const int *ids, int i) {
+    if (i >= MOE_ROWS) return -1;
+    const int x = ids[i];
+    return (x < 0 || x >= MOE_E) ? 0 : x;
+}
+
+extern "C" __global__ __launch_bounds__(PREP_T) void rc_moe_hist(MoeHistArgs a) {
+    __shared__ int hist[MOE_E];
+    const int tid = threadIdx.x;
+    const int x = prep_id(a.ids, blockIdx.x * PREP_T + tid);
+    for (int e = tid; e < MOE_E; e += PREP_T) hist[e] = 0;
+    __syncthreads();
+    if (x >= 0) atomicAdd(&hist[x], 1);
+    __syncthreads();
+    for (int e = tid; e < MOE_E; e += PREP_T) a.counts[(size_t)blockIdx.x * MOE_E + e] = hist[e];
+}
+
 struct MoePrepArgs {
     const int *ids;        // [T][TOPK] expert of each (token, slot)
+    const int *counts;     // [PREP_NB][E] rows per block and expert
     int *offsets;          // [E + 1] first permuted row of each expert
     int *perm;             // [T * TOPK] permuted row -> token * TOPK + slot
     int *pos;              // [T * TOPK] token * TOPK + slot -> permuted row
@@ -75,63 +121,45 @@ struct MoePrepArgs {
     int *tile_down;        // [E + 1] first M tile of each expert, down GEMM
 };
 
-// Routing preparation in one workgroup of PREP_T threads: a stable counting
-// sort of the routed rows by expert, reading the expert ids twice.
-//   1. Wave w owns the contiguous segment w of the rows and counts its
-//      rows per expert into cnt[w][*] (LDS atomics; only wave w touches
-//      row w of cnt).
-//   2. Thread x (one per expert) sums column x of cnt and turns it into
-//      the exclusive prefix over the waves; a block-wide exclusive scan of
-//      the column sums gives offsets[] and, from ceil(count / tile), the
-//      tile starts of both expert GEMMs; cnt[w][x] becomes the first
-//      permuted row of wave w's rows routed to expert x.
-//   3. Each wave walks its segment again in order, 64 rows at a time.  The
-//      lanes holding the same expert are found with one ballot per bit of
-//      the expert id; a lane's permuted row is cnt[w][x] plus the number of
-//      such lanes below it, and the lowest of them advances cnt[w][x].
-// Rows keep their order within an expert (wave segments in order, lanes in
-// order within a group), so the result is deterministic.  Expert ids out of
-// range are clamped to expert 0 so that no write can leave its buffer.
-// Loads are issued PREP_G groups at a time so that their latencies overlap.
-#define PREP_T 1024
-#define PREP_W (PREP_T / 64)
-#define PREP_G 8
-#define PREP_SEG ((((MOE_ROWS + PREP_W - 1) / PREP_W) + 63) / 64 * 64)
-#define PREP_BITS (MOE_E <= 1 ? 1 : 32 - __builtin_clz(MOE_E - 1))
-
-__device__ __forceinline__ int prep_id(const int *ids, int i, int end) {
-    if (i >= end) return -1;
-    const int x = ids[i];
-    return (x < 0 || x >= MOE_E) ? 0 : x;
-}
-
 extern "C" __global__ __launch_bounds__(PREP_T) void rc_moe_prep(MoePrepArgs a) {
-    __shared__ int cnt[PREP_W][MOE_E];
+    __shared__ int wcnt[PREP_W][MOE_E];      // rows per (wave, expert), then first rows
     __shared__ int wsum[3][PREP_W];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    for (int i = tid; i < PREP_W * MOE_E; i += PREP_T) (&cnt[0][0])[i] = 0;
-    const int seg0 = wave * PREP_SEG;
-    const int seg1 = min(seg0 + PREP_SEG, MOE_ROWS);
-    __syncthreads();
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, b = blockIdx.x;
+    const int i = b * PREP_T + tid;
+    const int x = prep_id(a.ids, i);
+    for (int k = tid; k < PREP_W * MOE_E; k += PREP_T) (&wcnt[0][0])[k] = 0;
 
-    // 1. per-wave histogram of the wave's segment
-    for (int g0 = seg0; g0 < seg1; g0 += 64 * PREP_G) {
-        int x[PREP_G];
+    // lanes of this wave holding the same expert
+    const bool valid = x >= 0;
+    unsigned long long m = __ballot(valid);
 #pragma unroll
-        for (int g = 0; g < PREP_G; ++g) x[g] = prep_id(a.ids, g0 + g * 64 + lane, seg1);
-#pragma unroll
-        for (int g = 0; g < PREP_G; ++g)
-            if (x[g] >= 0) atomicAdd(&cnt[wave][x[g]], 1);
+    for (int bit = 0; bit < PREP_BITS; ++bit) {
+        const bool on = valid && ((x >> bit) & 1);
+        const unsigned long long bb = __ballot(on);
+        m &= on ? bb : ~bb;
     }
-    __syncthreads();
+    const unsigned long long below = m & ((1ull << lane) - 1ull);
+    __syncthreads();                          // wcnt cleared
+    if (valid && below == 0ull) wcnt[wave][x] = __popcll(m);
 
-    // 2. per-expert totals, exclusive prefixes over waves and experts
-    int h = 0;
+    // expert totals and the rows of each expert in earlier blocks
+    int h = 0, before = 0;
     if (tid < MOE_E) {
-        for (int w = 0; w < PREP_W; ++w) {
-            const int c = cnt[w][tid];
-            cnt[w][tid] = h;
+        int blk = 0;
+        for (; blk + 8 <= PREP_NB; blk += 8) {
+            int c[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) c[j] = a.counts[(size_t)(blk + j) * MOE_E + tid];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                h += c[j];
+                before += (blk + j < b) ? c[j] : 0;
+            }
+        }
+        for (; blk < PREP_NB; ++blk) {
+            const int c = a.counts[(size_t)blk * MOE_E + tid];
             h += c;
+            before += blk < b ? c : 0;
         }
     }
     const int hu = (h + MOE_TM_UP - 1) / MOE_TM_UP, hd = (h + MOE_TM_DOWN - 1) / MOE_TM_DOWN;
@@ -141,49 +169,34 @@ extern "C" __global__ __launch_bounds__(PREP_T) void rc_moe_prep(MoePrepArgs a) 
         if (lane >= d) { ih += th; iu += tu; id += td; }
     }
     if (lane == 63) { wsum[0][wave] = ih; wsum[1][wave] = iu; wsum[2][wave] = id; }
-    __syncthreads();
-    int bh = 0, bu = 0, bd = 0;
-    for (int w = 0; w < wave; ++w) { bh += wsum[0][w]; bu += wsum[1][w]; bd += wsum[2][w]; }
+    __syncthreads();                          // wsum and the wave group sizes are in
     if (tid < MOE_E) {
+        int bh = 0, bu = 0, bd = 0;
+        for (int w = 0; w < wave; ++w) { bh += wsum[0][w]; bu += wsum[1][w]; bd += wsum[2][w]; }
         const int off = bh + ih - h;
-        a.offsets[tid] = off;
-        a.tile_up[tid] = bu + iu - hu;
-        a.tile_down[tid] = bd + id - hd;
-        for (int w = 0; w < PREP_W; ++w) cnt[w][tid] += off;
-        if (tid == MOE_E - 1) {
-            a.offsets[MOE_E] = bh + ih;
-            a.tile_up[MOE_E] = bu + iu;
-            a.tile_down[MOE_E] = bd + id;
+        if (b == 0) {
+            a.offsets[tid] = off;
+            a.tile_up[tid] = bu + iu - hu;
+            a.tile_down[tid] = bd + id - hd;
+            if (tid == MOE_E - 1) {
+                a.offsets[MOE_E] = bh + ih;
+                a.tile_up[MOE_E] = bu + iu;
+                a.tile_down[MOE_E] = bd + id;
+            }
+        }
+        // first permuted row of each wave's rows of expert tid
+        int run = off + before;
+        for (int w = 0; w < PREP_W; ++w) {
+            const int c = wcnt[w][tid];
+            wcnt[w][tid] = run;
+            run += c;
         }
     }
     __syncthreads();
-
-    // 3. stable scatter of the wave's segment
-    const unsigned long long below = (1ull << lane) - 1ull;
-    for (int g0 = seg0; g0 < seg1; g0 += 64 * PREP_G) {
-        int x[PREP_G];
-#pragma unroll
-        for (int g = 0; g < PREP_G; ++g) x[g] = prep_id(a.ids, g0 + g * 64 + lane, seg1);
-#pragma unroll
-        for (int g = 0; g < PREP_G; ++g) {
-            const bool valid = x[g] >= 0;
-            unsigned long long m = __ballot(valid);
-#pragma unroll
-            for (int b = 0; b < PREP_BITS; ++b) {
-                const bool bit = valid && ((x[g] >> b) & 1);
-                const unsigned long long bb = __ballot(bit);
-                m &= bit ? bb : ~bb;
-            }
-            if (valid) {
-                const int i = g0 + g * 64 + lane;
-                const int base = cnt[wave][x[g]];
-                const int p = base + __popcll(m & below);
-                a.perm[p] = i;
-                a.pos[i] = p;
-                // the lowest lane of the group advances the expert's next row
-                if ((m & below) == 0ull) cnt[wave][x[g]] = base + __popcll(m);
-            }
-        }
+    if (valid) {
+        const int p = wcnt[wave][x] + __popcll(below);
+        a.perm[p] = i;
+        a.pos[i] = p;
     }
 }
 

@@ -21,7 +21,11 @@
 //                group issues a whole K tile of MFMAs from registers, the
 //                other reads its next K tile's fragments from LDS and issues
 //                the direct-to-LDS loads of a later tile; the groups swap
-//                roles at each barrier (three LDS buffers)
+//                roles at each barrier (three LDS buffers); 7: a ring of
+//                NSTAGE buffers filled by direct-to-LDS buffer loads issued
+//                NSTAGE - 1 tiles ahead (range-checked: padded and missing
+//                rows load zeros), the next tile's first fragments read
+//                during the current tile's last k-step
 //   VEC          bf16 elements per global load: 2, 4 or 8 (Vectorize)
 //   UNROLL       unroll factor of the K-tile loop (Unroll)
 //   LAYOUT       weights stored 0: [K][N], 1: [N][K] (Layout)
@@ -61,8 +65,10 @@
 #define RPL ((16 / CPR) > 0 ? (16 / CPR) : 1)
 #define KTILES (GK / TK)
 #define RAGGED_M ((AMODE == 0 || AMODE == 2) && (GM % TM) != 0)
-#define A_LOADS ((TM * TK) / (VEC * NT))
-#define B_LOADS ((TN * TK) / (VEC * NT))
+// register-staged vectors per thread (the direct-to-LDS stages do not use
+// them; at least 1 keeps their unused arrays well formed)
+#define A_LOADS ((TM * TK) / (VEC * NT) > 0 ? (TM * TK) / (VEC * NT) : 1)
+#define B_LOADS ((TN * TK) / (VEC * NT) > 0 ? (TN * TK) / (VEC * NT) : 1)
 #define NTN (GN / TN)
 
 typedef unsigned short bf16_t;
@@ -149,6 +155,13 @@ void rc_gemm_bf16(GemmBf16Args args) {
     __shared__ __attribute__((aligned(16))) bf16_t Bs0[NB][TN * TK], Bs1[NB][TN * TK], Bs2[NB][TN * TK];
 #define NBUF 2
     bf16_t (*As)[TM * TK] = nullptr;           // unused with the DMA ring
+    bf16_t (*Bs)[NB][TN * TK] = nullptr;
+#elif STAGES == 7
+    // NSTAGE-deep ring; stage s holds the A tile, then the NB weight tiles
+#define STAGE_ELEMS (TM * TK + NB * TN * TK)
+    __shared__ __attribute__((aligned(16))) bf16_t ring[NSTAGE * STAGE_ELEMS];
+#define NBUF 2
+    bf16_t (*As)[TM * TK] = nullptr;           // unused with the ring
     bf16_t (*Bs)[NB][TN * TK] = nullptr;
 #elif STAGES == 6
     // three distinct LDS objects per operand (tile t in buffer t % 3)
@@ -459,6 +472,204 @@ void rc_gemm_bf16(GemmBf16Args args) {
         body(kt, As0, Bs0, As2, Bs2);
         if (kt + 1 < KTILES) body(kt + 1, As1, Bs1, As0, Bs0);
         if (kt + 2 < KTILES) body(kt + 2, As2, Bs2, As1, Bs1);
+    }
+#undef WAIT_VM
+#elif STAGES == 7
+    // Deep direct-to-LDS ring.  buffer_load_dwordx4 ... lds moves 64 lanes x
+    // 16 B into 1 KiB of LDS at a wave-uniform base (M0); the swizzle is
+    // applied by choosing which global chunk each lane fetches, as for
+    // stages 4.  The loads go through buffer resources whose range checking
+    // returns zeros for an offset past the buffer: rows past the operator's
+    // rows and taps of an im2col window that fall in the padding get offset
+    // OOB and load zeros.  Tile t goes to stage t % NSTAGE and is issued
+    // NSTAGE - 1 tiles ahead; the fragments of tile t + 1's first k-step are
+    // read during tile t's last k-step, so each tile starts its MFMAs at
+    // once after the one barrier per tile (which also frees the stage of
+    // tile t - 1 for tile t + NSTAGE - 1).  The loads are inline assembly,
+    // invisible to the compiler's wait-count bookkeeping; the waits below
+    // order the ring (loads complete in order).
+    typedef int i32x4 __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) bf16_t *lds_p;
+    constexpr int NWV = WM * WN;
+    constexpr int A_WL = TM * TK / 512 / NWV;        // wave-loads per wave, A tile
+    constexpr int B_WL = TN * TK / 512 / NWV;        // per weight operand
+    constexpr int LPT = A_WL + NB * B_WL;            // loads per lane per tile
+    constexpr int KS = TK / KSTEP;
+    constexpr unsigned OOB = 0x80000000u;            // past every operand: loads zeros
+    auto rsrc = [](const void *base, unsigned long long bytes) {
+        const unsigned long long a = (unsigned long long)base;
+        i32x4 r;
+        r[0] = __builtin_amdgcn_readfirstlane((int)(unsigned)a);
+        r[1] = __builtin_amdgcn_readfirstlane((int)((unsigned)(a >> 32) & 0xFFFFu));   // stride 0
+        r[2] = __builtin_amdgcn_readfirstlane((int)(unsigned)(bytes < 0xFFFFFFFFull ? bytes : 0xFFFFFFFFull));
+        r[3] = 0x00020000;                                                             // raw dword access
+        return r;
+    };
+#if AMODE == 1
+    const i32x4 rsA = rsrc(args.A, (unsigned long long)(GM / TOPK) * GK * 2);
+#elif AMODE == 2
+    const i32x4 rsA = rsrc(args.A, (unsigned long long)(GM / (CV_P * CV_Q)) * CV_H * CV_W * CV_C * 2);
+#else
+    const i32x4 rsA = rsrc(args.A, (unsigned long long)GM * GK * 2);
+#endif
+    i32x4 rsB[NB];
+    rsB[0] = rsrc(B0, (unsigned long long)GN * GK * 2);
+#if NB == 2
+    rsB[1] = rsrc(B1, (unsigned long long)GN * GK * 2);
+#endif
+    // per-lane byte offsets of each wave-load at k0 = 0
+    unsigned a_off7[A_WL];
+    bool a_ok7[A_WL];
+#if AMODE == 2
+    int a_cor7[A_WL];                                 // window corner (may lie in the padding), bytes
+    unsigned a_msk7[A_WL];
+#endif
+#pragma unroll
+    for (int j = 0; j < A_WL; ++j) {
+        const int c = (wave * A_WL + j) * 64 + lane;
+        const int row = c / CPR, lc = (c % CPR) ^ ((row / RPL) % CPR);
+#if AMODE == 0 || AMODE == 3
+        a_ok7[j] = row < rows_valid;
+        a_off7[j] = (unsigned)(((size_t)(row_base + row) * GK + lc * 8) * 2);
+#elif AMODE == 1
+        a_ok7[j] = row < rows_valid;
+        const int tok = args.perm[row_base + (a_ok7[j] ? row : 0)] / TOPK;
+        a_off7[j] = (unsigned)(((size_t)tok * GK + lc * 8) * 2);
+#else
+        const int m = row_base + row;
+        a_ok7[j] = m < GM;
+        const int n = m / (CV_P * CV_Q), p = (m / CV_Q) % CV_P, q = m % CV_Q;
+        a_cor7[j] = 2 * (((n * CV_H + p - CV_PAD) * CV_W + (q - CV_PAD)) * CV_C + lc * 8);
+        unsigned mask = 0;
+#pragma unroll
+        for (int tap = 0; tap < GK / CV_C; ++tap) {
+            const int ih = p + tap / CV_S - CV_PAD, iw = q + tap % CV_S - CV_PAD;
+            if (ih >= 0 && ih < CV_H && iw >= 0 && iw < CV_W) mask |= 1u << tap;
+        }
+        a_msk7[j] = a_ok7[j] ? mask : 0u;
+        a_off7[j] = 0;
+#endif
+    }
+    unsigned b_off7[B_WL];
+#pragma unroll
+    for (int j = 0; j < B_WL; ++j) {
+        const int c = (wave * B_WL + j) * 64 + lane;
+        const int row = c / CPR, lc = (c % CPR) ^ ((row / RPL) % CPR);
+        b_off7[j] = (unsigned)(((size_t)(n0 + row) * GK + lc * 8) * 2);
+    }
+    auto dma = [&](unsigned off, const i32x4 &rs, unsigned lds_addr) {
+        asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+                     :: "v"(off), "s"(rs), "s"(lds_addr) : "memory", "m0");
+    };
+    const unsigned ring0 = (unsigned)(size_t)(lds_p)ring;
+    const int wv = __builtin_amdgcn_readfirstlane(wave);      // wave-uniform, in a scalar register
+    auto issue = [&](int kt, int st) {
+        const int k0 = kt * TK;
+        const unsigned sb = ring0 + (unsigned)(st * STAGE_ELEMS * 2);
+#if AMODE == 2
+        const int tap = k0 / CV_C;
+        const int tap_off = 2 * (((tap / CV_S) * CV_W + tap % CV_S) * CV_C + (k0 - tap * CV_C));
+#endif
+#pragma unroll
+        for (int j = 0; j < A_WL; ++j) {
+#if AMODE == 2
+            const unsigned off = ((a_msk7[j] >> tap) & 1u) ? (unsigned)(a_cor7[j] + tap_off) : OOB;
+#else
+            const unsigned off = a_ok7[j] ? a_off7[j] + 2u * k0 : OOB;
+#endif
+            dma(off, rsA, sb + (unsigned)((wv * A_WL + j) * 1024));
+        }
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int j = 0; j < B_WL; ++j)
+                dma(b_off7[j] + 2u * k0, rsB[b],
+                    sb + (unsigned)(TM * TK * 2 + b * TN * TK * 2 + (wv * B_WL + j) * 1024));
+    };
+    // s_waitcnt with only the vector-memory count constrained
+#define WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | ((((n) >> 4) & 3) << 14) | (7 << 4) | (15 << 8))
+    // wait until at most `newer` tiles' loads of this wave are in flight
+    auto wait_tiles = [&](int newer) {
+        switch (newer) {
+            case 1: WAIT_VM(LPT); break;
+#if NSTAGE > 3
+            case 2: WAIT_VM(2 * LPT); break;
+#endif
+#if NSTAGE > 4
+            case 3: WAIT_VM(3 * LPT); break;
+#endif
+#if NSTAGE > 5
+            case 4: WAIT_VM(4 * LPT); break;
+#endif
+#if NSTAGE > 6
+            case 5: WAIT_VM(5 * LPT); break;
+#endif
+#if NSTAGE > 7
+            case 6: WAIT_VM(6 * LPT); break;
+#endif
+#if NSTAGE > 8
+            case 7: WAIT_VM(7 * LPT); break;
+#endif
+#if NSTAGE > 9
+            case 8: WAIT_VM(8 * LPT); break;
+#endif
+#if NSTAGE > 10
+            case 9: WAIT_VM(9 * LPT); break;
+#endif
+#if NSTAGE > 11
+            case 10: WAIT_VM(10 * LPT); break;
+#endif
+            default: WAIT_VM(0); break;
+        }
+    };
+    auto stage_a = [&](int t) { return (const bf16_t *)(ring + (t % NSTAGE) * STAGE_ELEMS); };
+    auto stage_b = [&](const bf16_t *la) { return (const bf16_t (*)[TN * TK])(la + TM * TK); };
+    // MFMAs of one k-step interleaved with the next k-step's fragment reads
+    constexpr int NMF = NB * FM * FN, NRD = FM + NB * FN;
+    auto kstep = [&](const Frags &cur, const bf16_t *ln, int ksn, Frags &nxt) {
+        load_frags(ln, stage_b(ln), ksn, nxt);
+        mfmas(cur);
+#pragma unroll
+        for (int r = 0; r < NRD; ++r) {
+            __builtin_amdgcn_sched_group_barrier(0x008, NMF / NRD > 0 ? NMF / NRD : 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, NMF, 0);
+    };
+    Frags f7[2];
+#pragma unroll
+    for (int u = 0; u < NSTAGE - 1; ++u)
+        if (u < KTILES) issue(u, u);
+    wait_tiles(min(NSTAGE - 2, KTILES - 1));
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    asm volatile("s_barrier" ::: "memory");
+    load_frags(stage_a(0), stage_b(stage_a(0)), 0, f7[0]);
+    auto body7 = [&](int t, auto par) {
+        constexpr int P = decltype(par)::value;
+        if (t + 1 < KTILES) {
+            // tile t + 1 has landed; every wave is done with tile t - 1's stage
+            wait_tiles(min(KTILES - 1, t + NSTAGE - 2) - (t + 1));
+            __builtin_amdgcn_s_waitcnt(0xC07F);
+            asm volatile("s_barrier" ::: "memory");
+            if (t + NSTAGE - 1 < KTILES) issue(t + NSTAGE - 1, (t + NSTAGE - 1) % NSTAGE);
+        }
+        const bf16_t *la = stage_a(t);
+        const bf16_t *ln = stage_a(t + 1);   // the last tile reads a stale stage; unused
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const int ci = (P * KS + ks) & 1;          // a constant once unrolled
+            if (ks + 1 < KS) {
+                if (ci == 0) kstep(f7[0], la, ks + 1, f7[1]);
+                else kstep(f7[1], la, ks + 1, f7[0]);
+            } else {
+                if (ci == 0) kstep(f7[0], ln, 0, f7[1]);
+                else kstep(f7[1], ln, 0, f7[0]);
+            }
+        }
+    };
+    for (int t = 0; t < KTILES; t += 2) {
+        body7(t, IntC<0>{});
+        if (t + 1 < KTILES) body7(t + 1, IntC<1>{});
     }
 #undef WAIT_VM
 #elif STAGES == 6

@@ -52,7 +52,7 @@ static void add_gemm_block(std::vector<KnobDef> &v, const char *const names[12],
     v.push_back({names[3], "Parallel", {1, 2, 4}, 1});
     v.push_back({names[4], "Parallel", {1, 2, 4}, 1});
     v.push_back({names[5], "TileSize", {16, 32}, 16});          // MFMA instruction shape
-    v.push_back({names[6], "ComputeLocation", {1, 2, 3, 4, 5, 6}, 1});   // LDS staging of the next K tile
+    v.push_back({names[6], "ComputeLocation", {1, 2, 3, 4, 5, 6, 7}, 1});   // LDS staging of the next K tile
     v.push_back({names[7], "Vectorize", {2, 4, 8}, 2});         // bf16 per global load
     v.push_back({names[8], "Unroll", {1, 2}, 1});
     v.push_back({names[9], "Layout", {0, 1}, 0});               // weight stored KxN / NxK
@@ -176,6 +176,17 @@ static std::string fmt(const char *f, ...) {
 
 static const int64_t LDS_LIMIT = 163840;   // bytes one workgroup may allocate on gfx950
 
+// Depth of the direct-to-LDS ring of bf16 GEMM stages 7: as many stages as
+// fit the LDS share of one workgroup when occ waves per SIMD are resident,
+// at most 12, and few enough that the loads a wave keeps in flight
+// (NSTAGE - 2 tiles) fit the 6-bit vector-memory counter.
+int gemm_ring_stages(int tm, int tn, int tk, int nb, int waves, int occ) {
+    const int64_t sb = (int64_t)(tm + nb * tn) * tk * 2;
+    const int64_t wgs = std::max<int64_t>(1, (occ * 4 + waves - 1) / waves);
+    const int64_t lpt = std::max<int64_t>(1, sb / 1024 / waves);
+    return (int)std::min<int64_t>(std::min<int64_t>(12, LDS_LIMIT / (wgs * sb)), 63 / lpt + 2);
+}
+
 // Rules for one bf16 GEMM stage of shape M x N x K (M < 0: ragged expert
 // groups), NB weight operands sharing the A tile.  Any M is legal: the last
 // M tile's missing rows are predicated off.
@@ -201,10 +212,13 @@ static std::string check_bf16_block(const rc_op_desc *d, const rc_schedule *s,
         return fmt("%s: tile_m %d: tile_m %d already covers M = %lld", tag, tm, tm / 2, (long long)M);
     if (N % tn) return fmt("%s: tile_n %d does not divide N = %lld", tag, tn, (long long)N);
     if (K % tk) return fmt("%s: tile_k %d does not divide K = %lld", tag, tk, (long long)K);
-    if ((int64_t)tm * tk % ((int64_t)vec * nt))
+    // register-staged loads: every thread moves whole vectors of each tile
+    // (the direct-to-LDS stages 4, 6 and 7 have their own wave-load rules)
+    const bool dma = st == 4 || st == 6 || st == 7;
+    if (!dma && (int64_t)tm * tk % ((int64_t)vec * nt))
         return fmt("%s: A tile %dx%d does not split into %d threads x %d-wide loads", tag, tm, tk,
                    nt, vec);
-    if ((int64_t)tn * tk % ((int64_t)vec * nt))
+    if (!dma && (int64_t)tn * tk % ((int64_t)vec * nt))
         return fmt("%s: B tile %dx%d does not split into %d threads x %d-wide loads", tag, tk, tn,
                    nt, vec);
     if (lay == 0 && tn % vec) return fmt("%s: vec %d does not divide tile_n %d", tag, vec, tn);
@@ -239,7 +253,33 @@ static std::string check_bf16_block(const rc_op_desc *d, const rc_schedule *s,
             return fmt("%s: %lld accumulator + %lld fragment registers per lane exceed 224", tag,
                        (long long)accr, (long long)frag);
     }
-    int64_t lds = (int64_t)(st == 4 || st == 6 ? 3 : st > 1 ? 2 : 1) * ((int64_t)tm * tk + (int64_t)NB * tn * tk) * 2;
+    if (st == 7) {
+        // deep direct-to-LDS ring of buffer loads (range-checked, so
+        // padded im2col taps and missing rows load zeros)
+        if (lay != 1) return fmt("%s: the direct-to-LDS ring needs weights stored N x K", tag);
+        if (vec != 8) return fmt("%s: the direct-to-LDS ring moves 16-byte vectors (vec 8)", tag);
+        if (((int64_t)tm * tk / 512) % (wm * wn) || tm * tk < 512 * wm * wn)
+            return fmt("%s: A tile is not a whole number of 1 KiB wave-loads per wave", tag);
+        if (((int64_t)tn * tk / 512) % (wm * wn) || tn * tk < 512 * wm * wn)
+            return fmt("%s: B tile is not a whole number of 1 KiB wave-loads per wave", tag);
+        // 32-bit buffer offsets, and an out-of-range offset (2^31) past every operand
+        if ((M > 0 ? M : 0) * K * 2 >= (1LL << 31) || N * K * 2 >= (1LL << 31))
+            return fmt("%s: operands of 2 GiB or more exceed the ring's 32-bit buffer offsets", tag);
+        const int ns = gemm_ring_stages(tm, tn, tk, NB, wm * wn, kv(d, s, names[11]));
+        if (ns < 3) return fmt("%s: the LDS holds %d ring stages of this tile (needs 3)", tag, ns);
+        const int64_t lpt = ((int64_t)tm * tk + (int64_t)NB * tn * tk) / 512 / (wm * wn);
+        if ((ns - 2) * lpt > 63)
+            return fmt("%s: %lld loads per wave in flight exceed the 6-bit vector-memory counter", tag,
+                       (long long)((ns - 2) * lpt));
+        const int64_t frag = (int64_t)(tm / wm / mf + NB * (tn / wn / mf)) * 4 * 2;
+        const int64_t accr = (int64_t)NB * tm * tn / nt;
+        if (accr + frag > 448)
+            return fmt("%s: %lld accumulator + %lld fragment registers per lane exceed 448", tag,
+                       (long long)accr, (long long)frag);
+    }
+    const int64_t stage_bytes = ((int64_t)tm * tk + (int64_t)NB * tn * tk) * 2;
+    int64_t lds = (int64_t)(st == 4 || st == 6 ? 3 : st > 1 ? 2 : 1) * stage_bytes;
+    if (st == 7) lds = (int64_t)gemm_ring_stages(tm, tn, tk, NB, wm * wn, kv(d, s, names[11])) * stage_bytes;
     if (lds > LDS_LIMIT)
         return fmt("%s: LDS %lld B exceeds %lld B", tag, (long long)lds, (long long)LDS_LIMIT);
     int64_t acc = (int64_t)NB * tm * tn / nt;
@@ -409,6 +449,9 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
             // LDS (16 x E x 4 B)
             if (E > 1024) return fmt("%lld experts exceed the routing kernel's 1024", (long long)E);
             if (D[0] * topk > INT32_MAX / 2) return "routed rows exceed the 32-bit row indices";
+            if ((kv(d, s, "up.stages") == 7 || kv(d, s, "down.stages") == 7) &&
+                std::max(D[0] * Hd, D[0] * topk * I) * 2 >= (1LL << 31))
+                return "activations of 2 GiB or more exceed the ring's 32-bit buffer offsets";
             std::string r = check_bf16_block(d, s, UP, -1, I, Hd, 2, "up");
             if (!r.empty()) return r;
             return check_bf16_block(d, s, DOWN, -1, Hd, I, 1, "down");

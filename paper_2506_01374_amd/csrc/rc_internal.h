@@ -28,6 +28,9 @@ bool desc_ok(const rc_op_desc *d);
 // Knob value by name (asserts the name exists for the kind).
 int32_t kv(const rc_op_desc *d, const rc_schedule *s, const char *name);
 
+// Depth of the direct-to-LDS ring of bf16 GEMM stages 7.
+int gemm_ring_stages(int tm, int tn, int tk, int nb, int waves, int occ);
+
 // Legality with a reason; "" when legal.
 std::string check_schedule(const rc_op_desc *d, const rc_schedule *s);
 

@@ -48,8 +48,12 @@ struct EwArgs {
     const void *G, *U, *bias;
     void *out;
 };
-struct MoePrepArgs {
+struct MoeHistArgs {
     const void *ids;
+    void *counts;
+};
+struct MoePrepArgs {
+    const void *ids, *counts;
     void *offsets, *perm, *pos, *tile_up, *tile_down;
 };
 struct MoeCombineArgs {
@@ -381,6 +385,7 @@ std::string gemm_defs(const GemmCfg &g, int nb, int amode, int epi, long gm, lon
     s += def("MF", g.mf) + def("STAGES", g.st) + def("VEC", g.vec) + def("UNROLL", g.un);
     s += def("LAYOUT", g.lay) + def("GRID", g.grid) + def("NB", nb) + def("AMODE", amode);
     s += def("EPI", epi) + def("GM", gm) + def("GN", gn) + def("GK", gk) + def("OCC", g.occ);
+    if (g.st == 7) s += def("NSTAGE", gemm_ring_stages(g.tm, g.tn, g.tk, nb, g.wm * g.wn, g.occ));
     return s;
 }
 
@@ -509,6 +514,8 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             size_t offPos = ws.add(R * 4, "pos");
             size_t offTu = ws.add((E + 1) * 4, "tile_up"), offTd = ws.add((E + 1) * 4, "tile_down");
             size_t offH = ws.add((size_t)R * I * 2, "hidden"), offY = ws.add((size_t)R * Hd * 2, "expert_out");
+            const long nblk = (R + 1023) / 1024;    // routing blocks of 1024 rows
+            size_t offCnt = ws.add((size_t)nblk * E * 4, "block_counts");
             size_t offG = 0, offU = 0;
             if (!fuse) {
                 offG = ws.add((size_t)R * I * 4, "gate.f32");
@@ -516,12 +523,22 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             }
             std::string moe = def("MOE_T", T) + def("MOE_TOPK", topk) + def("MOE_E", E) +
                               def("MOE_H", Hd) + def("MOE_TM_UP", up.tm) + def("MOE_TM_DOWN", dn.tm);
+            // routing: per-block expert histograms, then the stable scatter
+            Kern kh;
+            kh.src = Source{SRC_aux, "rc_moe_hist", moe};
+            kh.grid = dim3((unsigned)nblk, 1, 1);
+            kh.block = dim3(1024, 1, 1);
+            kh.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
+                put(b, MoeHistArgs{a->in[1], w + offCnt});
+            };
+            p.kerns.push_back(kh);
             Kern k0;
             k0.src = Source{SRC_aux, "rc_moe_prep", moe};
-            k0.grid = dim3(1, 1, 1);            // one workgroup: a stable counting sort
+            k0.grid = dim3((unsigned)nblk, 1, 1);
             k0.block = dim3(1024, 1, 1);
             k0.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
-                put(b, MoePrepArgs{a->in[1], w + offOff, w + offPerm, w + offPos, w + offTu, w + offTd});
+                put(b, MoePrepArgs{a->in[1], w + offCnt, w + offOff, w + offPerm, w + offPos, w + offTu,
+                                   w + offTd});
             };
             p.kerns.push_back(k0);
             std::string mdefs = def("TOPK", topk) + def("NEXP", E);
@@ -537,7 +554,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
                                     w + offTu});
             };
             p.kerns.push_back(k1);
-            p.dominant = 1;
+            p.dominant = 2;
             if (!fuse) {
                 Kern ke;
                 ke.src = Source{SRC_aux, "rc_swiglu_f32", def("EW_N", R * I) + def("EW_COLS", I)};
@@ -999,13 +1016,13 @@ rc_status rc_time(const rc_plan *p, const rc_args *a, void *ws, size_t ws_bytes,
     hipError_t se = hipStreamSynchronize(st);
     if (r == RC_OK && se != hipSuccess) r = hip_fail(se, "hipStreamSynchronize");
     if (r == RC_OK) {
-        std::vector<double> tot, per[4];
+        std::vector<double> tot, per[8];
         for (int i = 0; i < opt.repeat; ++i) {
             hipEvent_t *e = &ev[(size_t)i * (nk + 1)];
             float ms = 0.f;
             if (hipEventElapsedTime(&ms, e[0], e[nk]) != hipSuccess) r = fail(RC_ERR_HIP, "hipEventElapsedTime");
             tot.push_back(ms);
-            for (int k = 0; k < nk && k < 4; ++k) {
+            for (int k = 0; k < nk && k < 8; ++k) {
                 float km = 0.f;
                 if (hipEventElapsedTime(&km, e[k], e[k + 1]) != hipSuccess) r = fail(RC_ERR_HIP, "hipEventElapsedTime");
                 per[k].push_back(km);
@@ -1027,7 +1044,7 @@ rc_status rc_time(const rc_plan *p, const rc_args *a, void *ws, size_t ws_bytes,
         t.gbps = rc_op_bytes(&p->desc) / sec / 1e9;
         t.frac_flops = t.tflops * 1e12 / rc_peak_flops(&p->desc);
         t.frac_bytes = t.gbps * 1e9 / rc_peak_bytes_per_s();
-        for (int k = 0; k < nk && k < 4; ++k) t.kernel_ms[k] = quantile(per[k], 0.5);
+        for (int k = 0; k < nk && k < 8; ++k) t.kernel_ms[k] = quantile(per[k], 0.5);
         *out = t;
     }
     for (auto &e : ev) (void)hipEventDestroy(e);

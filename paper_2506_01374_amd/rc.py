@@ -67,7 +67,7 @@ class rc_timing(ctypes.Structure):
                 ("mean_ms", ctypes.c_double), ("q1_ms", ctypes.c_double),
                 ("q3_ms", ctypes.c_double), ("tflops", ctypes.c_double),
                 ("gbps", ctypes.c_double), ("frac_flops", ctypes.c_double),
-                ("frac_bytes", ctypes.c_double), ("kernel_ms", ctypes.c_double * 4)]
+                ("frac_bytes", ctypes.c_double), ("kernel_ms", ctypes.c_double * 8)]
 
 
 class rc_search_opts(ctypes.Structure):

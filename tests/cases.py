@@ -185,12 +185,21 @@ SCHEDULES = {
         _block("down.", 128, 256, 64, 2, 4, 32, 6, 8, 1, 1, 1, 2) + ",fuse=1",
         _block("up.", 128, 128, 32, 4, 2, 16, 6, 8, 1, 1, 0, 2) + "," +
         _block("down.", 256, 128, 32, 4, 2, 16, 6, 8, 1, 1, 0, 2) + ",fuse=0",
+        # deep direct-to-LDS ring (buffer loads, zero-filled missing rows)
+        _block("up.", 128, 128, 32, 2, 2, 16, 7, 8, 1, 1, 1) + "," +
+        _block("down.", 64, 128, 64, 2, 2, 16, 7, 8, 1, 1, 0, 2) + ",fuse=1",
+        _block("up.", 256, 128, 32, 4, 2, 16, 7, 8, 1, 1, 1, 2) + "," +
+        _block("down.", 128, 128, 64, 2, 2, 32, 7, 8, 1, 1, 1) + ",fuse=1",
+        _block("up.", 64, 64, 64, 2, 2, 32, 7, 8, 1, 1, 0) + "," +
+        _block("down.", 128, 256, 32, 2, 4, 16, 7, 8, 1, 1, 1, 2) + ",fuse=0",
     ],
     "mlp_odd": [
         _block("up.", 256, 64, 64, 4, 2, 16, 6, 8, 1, 1, 1, 2) + "," +
         _block("down.", 256, 64, 64, 4, 2, 16, 6, 8, 1, 1, 1, 2) + ",fuse=1",
         _block("up.", 256, 64, 64, 4, 2, 32, 6, 8, 1, 1, 0, 2) + "," +
         _block("down.", 128, 64, 64, 4, 2, 16, 6, 8, 1, 1, 0, 2) + ",fuse=1",
+        _block("up.", 128, 64, 64, 2, 2, 16, 7, 8, 1, 1, 1) + "," +
+        _block("down.", 64, 64, 32, 2, 2, 16, 7, 8, 1, 1, 0) + ",fuse=1",
     ],
     "moe": [
         "",
@@ -219,6 +228,11 @@ SCHEDULES = {
         _block("down.", 128, 256, 64, 2, 4, 16, 6, 8, 1, 1, 1, 2) + ",fuse=1",
         _block("up.", 128, 128, 32, 2, 4, 16, 6, 8, 1, 1, 0, 2) + "," +
         _block("down.", 128, 128, 32, 4, 2, 32, 6, 8, 1, 1, 0, 2) + ",fuse=0",
+        # deep direct-to-LDS ring over gathered (gate/up) and grouped (down) rows
+        _block("up.", 128, 128, 32, 2, 2, 16, 7, 8, 1, 1, 1) + "," +
+        _block("down.", 64, 128, 64, 2, 2, 16, 7, 8, 1, 1, 0, 2) + ",fuse=1",
+        _block("up.", 64, 128, 64, 2, 2, 32, 7, 8, 1, 1, 0) + "," +
+        _block("down.", 128, 256, 32, 2, 4, 16, 7, 8, 1, 1, 1, 2) + ",fuse=0",
     ],
     "conv": [
         "",
@@ -228,6 +242,10 @@ SCHEDULES = {
         _block("", 128, 64, 64, 2, 2, 32, 2, 8, 1, 1, 1) + ",fuse=1",
         _block("", 32, 64, 64, 1, 2, 16, 2, 2, 1, 0, 0) + ",fuse=1",
         _block("", 128, 64, 64, 2, 2, 16, 3, 8, 1, 1, 0, 2) + ",fuse=1",
+        # deep direct-to-LDS ring: padded taps and missing pixels load zeros
+        _block("", 64, 64, 64, 2, 2, 16, 7, 8, 1, 1, 1) + ",fuse=1",
+        _block("", 64, 64, 32, 2, 1, 32, 7, 8, 1, 1, 0, 2) + ",fuse=0",
+        _block("", 128, 64, 64, 2, 2, 16, 7, 8, 1, 1, 1, 2) + ",fuse=1",
     ],
 }
 
@@ -238,6 +256,8 @@ SCHEDULES["conv_k320"] = [
     _block("", 16, 320, 64, 1, 4, 16, 2, 4, 1, 0, 0) + ",fuse=1",
     _block("", 64, 320, 64, 2, 2, 32, 2, 8, 1, 1, 1) + ",fuse=1",
     _block("", 64, 160, 64, 2, 2, 16, 1, 8, 1, 1, 0, 2) + ",fuse=0",
+    _block("", 64, 160, 64, 2, 2, 16, 7, 8, 1, 1, 1) + ",fuse=1",
+    _block("", 64, 320, 32, 2, 2, 16, 7, 8, 1, 1, 0) + ",fuse=1",
 ]
 SCHEDULES["attn_causal_512"] = [
     "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=2,occ=2,chunk=8",
@@ -274,6 +294,8 @@ _ONE_ATTN = [
 ]
 _ONE_MLP = [
     "",
+    _block("up.", 16, 64, 32, 1, 1, 16, 7, 8, 1, 1, 1) + "," +
+    _block("down.", 16, 64, 32, 1, 1, 16, 7, 8, 1, 1, 1) + ",fuse=1",
     _block("up.", 16, 128, 64, 1, 2, 16, 4, 8, 1, 1, 1) + "," +
     _block("down.", 16, 128, 64, 1, 2, 16, 4, 8, 1, 1, 1) + ",fuse=1",
     _block("up.", 16, 64, 64, 1, 2, 16, 5, 8, 1, 1, 0) + "," +
@@ -293,6 +315,7 @@ SCHEDULES["mlp_one"] = _ONE_MLP
 SCHEDULES["moe_one"] = _ONE_MLP
 SCHEDULES["conv_one"] = [
     "",
+    _block("", 16, 64, 64, 1, 2, 16, 7, 8, 1, 1, 1) + ",fuse=1",
     _block("", 16, 64, 64, 1, 2, 16, 5, 8, 1, 1, 1) + ",fuse=1",
     _block("", 16, 64, 32, 1, 1, 16, 2, 8, 1, 0, 0) + ",fuse=0",
 ]
@@ -323,6 +346,15 @@ FULL_ALT = [
      _block("down.", 128, 128, 64, 2, 2, 16, 3, 8, 1, 1, 0) + ",fuse=1"),
     ("conv3x3_n2_64x64_c320_k320",
      _block("", 64, 64, 64, 4, 2, 16, 2, 8, 1, 1, 1) + ",fuse=1"),
+    # deep direct-to-LDS ring at full size
+    ("gated_mlp_t2048_h4096_i14336",
+     _block("up.", 256, 128, 32, 4, 2, 16, 7, 8, 1, 1, 1, 2) + "," +
+     _block("down.", 128, 128, 64, 2, 2, 16, 7, 8, 1, 1, 1) + ",fuse=1"),
+    ("moe_t4096_h2048_e64_i1408_top6",
+     _block("up.", 256, 128, 32, 4, 2, 16, 7, 8, 1, 1, 1, 2) + "," +
+     _block("down.", 128, 128, 64, 2, 2, 16, 7, 8, 1, 1, 1) + ",fuse=1"),
+    ("conv3x3_n2_64x64_c320_k320",
+     _block("", 64, 160, 64, 2, 2, 16, 7, 8, 1, 1, 1) + ",fuse=1"),
 ]
 
 
@@ -346,6 +378,8 @@ GEMM_1X1 = [
     _block("", 32, 64, 128, 1, 2, 16, 5, 8, 2, 1, 1) + ",fuse=0",
     _block("", 64, 32, 64, 2, 1, 16, 1, 4, 1, 0, 0) + ",fuse=1",
     _block("", 256, 128, 64, 4, 2, 16, 2, 8, 1, 1, 1, 2) + ",fuse=1",
+    _block("", 128, 128, 64, 2, 2, 16, 7, 8, 1, 1, 1) + ",fuse=1",
+    _block("", 64, 128, 32, 2, 2, 32, 7, 8, 1, 1, 0, 2) + ",fuse=1",
 ]
 GEMM_1X1_OP = (rc.RC_OP_CONV2D, (2, 16, 16, 256, 128, 1, 1, 0), rc.RC_FLAG_NO_ACT)
 CONV_FULL_ALT = _block("", 64, 64, 64, 4, 2, 16, 2, 8, 1, 1, 1) + ",fuse=1"

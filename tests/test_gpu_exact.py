@@ -255,8 +255,8 @@ def test_rc_time_flush_and_output(key):
     assert t.nkernels == plan.nkernels
     assert 0 < t.min_ms <= t.q1_ms <= t.median_ms <= t.q3_ms
     assert t.mean_ms >= t.min_ms
-    assert all(t.kernel_ms[i] > 0 for i in range(min(4, t.nkernels)))
-    assert sum(t.kernel_ms[:min(4, t.nkernels)]) <= t.q3_ms * 1.5 + 1e-3
+    assert all(t.kernel_ms[i] > 0 for i in range(min(8, t.nkernels)))
+    assert sum(t.kernel_ms[:min(8, t.nkernels)]) <= t.q3_ms * 1.5 + 1e-3
     sec = t.median_ms * 1e-3
     assert abs(t.tflops - op.flops() / sec / 1e12) <= 1e-9 * max(1.0, t.tflops)
     assert abs(t.frac_flops - op.flops() / sec / op.peak_flops()) <= 1e-9
