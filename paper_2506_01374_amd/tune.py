@@ -243,8 +243,8 @@ def _policy_args(name: str):
 
 def summarize_campaign(runs: List[dict], ref_reward: float, budget: int) -> Dict[str, dict]:
     """Per policy: mean best-so-far (as a fraction of the reference reward)
-    at the paper's sample counts, and samples to reach 90 % / 99 % of the
-    reference per seed."""
+    at the paper's sample counts, and samples to reach 50 / 75 / 90 / 99 %
+    of the reference per seed."""
     import statistics
     out: Dict[str, dict] = {}
     by: Dict[str, List[dict]] = {}
@@ -269,7 +269,8 @@ def summarize_campaign(runs: List[dict], ref_reward: float, budget: int) -> Dict
             return {"per_seed": got, "reached": len(hit), "of": len(got),
                     "median": statistics.median(hit) if hit else None}
         best = max(rs, key=lambda r: r["best_reward"])
-        out[name] = {"best_so_far_over_reference": at, "samples_to_90pct": reach(0.90),
+        out[name] = {"best_so_far_over_reference": at, "samples_to_50pct": reach(0.50),
+                     "samples_to_75pct": reach(0.75), "samples_to_90pct": reach(0.90),
                      "samples_to_99pct": reach(0.99),
                      "best_over_reference": best["best_reward"] / ref_reward,
                      "best_schedule": best["best"], "seeds": [r["seed"] for r in rs]}
@@ -629,8 +630,9 @@ def main(argv=None):
         print(json.dumps({k: rec[k] for k in ("workload", "reference_reward", "distinct_schedules",
                                                "invalid", "wall_s", "errors")}), flush=True)
         for pname, sm in rec["summary"].items():
-            print(pname, json.dumps({k: sm[k] for k in ("best_over_reference", "samples_to_90pct",
-                                                         "samples_to_99pct")}), flush=True)
+            print(pname, json.dumps({k: (sm[k] if k == "best_over_reference" else sm[k]["median"])
+                                     for k in ("best_over_reference", "samples_to_50pct", "samples_to_75pct",
+                                               "samples_to_90pct", "samples_to_99pct")}), flush=True)
         return
 
     tag = args.policy + (f"+{args.proposer}" if args.proposer else "") + ("+surrogate" if args.surrogate else "")
