@@ -60,8 +60,9 @@
 #define NTS (64 * NW)
 #define NT (NTS * SPLITS)
 #define NBUF (STAGES > 1 ? 2 : 1)      // register-staged paths
-// direct-to-LDS paths: ring slots per operand (two per split with two splits)
-#define RING (STAGES == 5 || SPLITS == 2 ? 4 : 3)
+// direct-to-LDS paths: ring slots per operand (two per split with several
+// splits)
+#define RING (STAGES == 5 ? 4 : SPLITS > 1 ? 2 * SPLITS : 3)
 #define KB (BN / MF)
 #define DB (AD / MF)
 #define NQT ((AS + BM - 1) / BM)
@@ -273,7 +274,7 @@ void rc_attention(AttnArgs args) {
     __shared__ __attribute__((aligned(16))) bf16_t ring[2 * RING][KT_ELEMS];
     bf16_t *const K0 = ring[0], *const K1 = ring[1], *const K2 = ring[2];
     bf16_t *const V0 = ring[RING], *const V1 = ring[RING + 1], *const V2 = ring[RING + 2];
-#if RING == 4
+#if RING >= 4
     bf16_t *const K3 = ring[3], *const V3 = ring[RING + 3];
 #endif
     bf16_t *const smem = ring[0];
@@ -345,17 +346,12 @@ void rc_attention(AttnArgs args) {
     // LDS byte addresses of the ring buffers and this wave's first 1 KiB
     typedef __attribute__((address_space(3))) bf16_t *lds_p;
     const unsigned wl0 = (unsigned)__builtin_amdgcn_readfirstlane(rg) * WL * 1024u;
-#if RING == 4
-    const unsigned KA[4] = {(unsigned)(size_t)(lds_p)K0 + wl0, (unsigned)(size_t)(lds_p)K1 + wl0,
-                            (unsigned)(size_t)(lds_p)K2 + wl0, (unsigned)(size_t)(lds_p)K3 + wl0};
-    const unsigned VA[4] = {(unsigned)(size_t)(lds_p)V0 + wl0, (unsigned)(size_t)(lds_p)V1 + wl0,
-                            (unsigned)(size_t)(lds_p)V2 + wl0, (unsigned)(size_t)(lds_p)V3 + wl0};
-#else
-    const unsigned KA[3] = {(unsigned)(size_t)(lds_p)K0 + wl0, (unsigned)(size_t)(lds_p)K1 + wl0,
-                            (unsigned)(size_t)(lds_p)K2 + wl0};
-    const unsigned VA[3] = {(unsigned)(size_t)(lds_p)V0 + wl0, (unsigned)(size_t)(lds_p)V1 + wl0,
-                            (unsigned)(size_t)(lds_p)V2 + wl0};
-#endif
+    unsigned KA[RING], VA[RING];
+#pragma unroll
+    for (int i = 0; i < RING; ++i) {
+        KA[i] = (unsigned)(size_t)(lds_p)ring[i] + wl0;
+        VA[i] = (unsigned)(size_t)(lds_p)ring[RING + i] + wl0;
+    }
     auto dma = [&](const bf16_t *gbase, unsigned off, unsigned lds_addr) {
         asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
                      :: "v"(off), "s"(gbase), "s"(lds_addr) : "memory", "m0");
@@ -705,16 +701,16 @@ void rc_attention(AttnArgs args) {
     // split sp visits key tiles sp, sp + SPLITS, ...; every wave runs the same
     // number of iterations so the workgroup barriers line up
     const int n_it = (n_kt + SPLITS - 1) / SPLITS;
-#if STAGES == 4 && SPLITS == 2
+#if STAGES == 4 && SPLITS > 1
     (void)compute;
 #define WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | ((((n) >> 4) & 3) << 14) | (7 << 4) | (15 << 8))
-    // Two splits share a ring of four slots: iteration i computes tile 2i
-    // (split 0) and tile 2i + 1 (split 1) from slots 2 (i % 2) + split,
-    // while each split loads its next tile into the other pair of slots.
-    // The pair was last read in iteration i - 1, before the last barrier.
+    // The splits share a ring of 2 x SPLITS slots: iteration i computes tile
+    // SPLITS i + split from slot SPLITS (i % 2) + split, while each split
+    // loads its next tile into the same slot of the other half of the ring.
+    // That half was last read in iteration i - 1, before the last barrier.
     auto body = [&](int it, int pair) {
-        const int kt = 2 * it + sp, nk = kt + 2;
-        if (nk < n_kt) gload_lds(nk, 2 - pair + sp);
+        const int kt = SPLITS * it + sp, nk = kt + SPLITS;
+        if (nk < n_kt) gload_lds(nk, SPLITS - pair + sp);
         if (kt < n_kt && !skipped(kt)) {
             accT sc[QB][KB];
             scores_at(ring[pair + sp], sc);
@@ -726,7 +722,7 @@ void rc_attention(AttnArgs args) {
     };
     for (int it = 0; it < n_it; it += 2) {
         body(it, 0);
-        if (it + 1 < n_it) body(it + 1, 2);
+        if (it + 1 < n_it) body(it + 1, SPLITS);
     }
 #undef WAIT_VM
 #elif STAGES == 4

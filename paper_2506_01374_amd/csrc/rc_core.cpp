@@ -399,9 +399,7 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
                 // direct-to-LDS ring: whole 1 KiB wave-loads, key-major V read
                 // by the 16x16 transposing load, one key split
                 if (mf != 16) return "direct-to-LDS attention uses the 16x16 MFMA shape";
-                if (sp > (st == 4 ? 2 : 1))
-                    return st == 4 ? "direct-to-LDS attention takes one or two key splits"
-                                   : "pipelined direct-to-LDS attention takes one key split";
+                if (st == 5 && sp > 1) return "pipelined direct-to-LDS attention takes one key split";
                 if (kv(d, s, "vec") != 8) return "direct-to-LDS loads move 16-byte vectors (vec 8)";
                 if ((bn * Dh / 512) % w || bn * Dh < 512 * w)
                     return fmt("K/V tile of %d x %lld is not a whole number of 1 KiB wave-loads per wave", bn, (long long)Dh);
@@ -411,7 +409,7 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
             // K tile + padded V^T tile per stage and split (three plain K/V
             // tiles for the direct-to-LDS ring)
             int64_t vts = bn + (mf == 16 ? 16 : 8);   // padded V^T row
-            int64_t lds = st >= 4 ? (st == 5 || sp == 2 ? 4 : 3) * 2 * (int64_t)bn * Dh * 2
+            int64_t lds = st >= 4 ? (st == 5 ? 4 : sp > 1 ? 2 * sp : 3) * 2 * (int64_t)bn * Dh * 2
                                   : (int64_t)sp * (st > 1 ? 2 : 1) * ((int64_t)bn * Dh + Dh * vts) * 2;
             if (lds > LDS_LIMIT) return fmt("LDS %lld B exceeds limit", (long long)lds);
             int64_t mf_acc = (mf == 16) ? 4 : 16;

@@ -249,7 +249,11 @@ class Op:
         return "hbm" if self.flops() / self.bytes() < ridge else "mfma"
 
     def knob_names(self) -> List[str]:
-        return [lib().rc_knob_name(self.ref, i).decode() for i in range(lib().rc_knob_count(self.ref))]
+        names = getattr(self, "_names", None)      # static per operator: read once
+        if names is None:
+            names = [lib().rc_knob_name(self.ref, i).decode() for i in range(lib().rc_knob_count(self.ref))]
+            self._names = names
+        return list(names)
 
     def knob_class(self, i: int) -> str:
         return lib().rc_knob_class(self.ref, i).decode()

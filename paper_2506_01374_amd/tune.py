@@ -418,6 +418,65 @@ class FeedbackProposer:
         return self.rng.choice(moves) if moves else ""
 
 
+CUS, LDS_BYTES = 256, 163840          # MI355X compute units; LDS one workgroup may use
+
+
+def _gemm_block_features(d: Dict[str, int], pre: str, M: int, N: int, K: int, nb: int) -> List[float]:
+    """Resource and shape features of one bf16 GEMM stage (a cheap analytic
+    description of what the knobs imply: the cost-model inputs of Sec. 3.2's
+    f-hat)."""
+    tm, tn, tk = d[pre + "tile_m"], d[pre + "tile_n"], d[pre + "tile_k"]
+    waves = d[pre + "waves_m"] * d[pre + "waves_n"]
+    wtm, wtn = tm / d[pre + "waves_m"], tn / d[pre + "waves_n"]
+    st, occ = d[pre + "stages"], d[pre + "occ"]
+    stage_bytes = (tm + nb * tn) * tk * 2
+    nbuf = {1: 1, 2: 2, 3: 2, 4: 3, 5: 2, 6: 3}.get(st, 0)
+    if st == 7:
+        wgs = max(1, -(-occ * 4 // waves))
+        nbuf = min(12, LDS_BYTES // (wgs * stage_bytes))
+    lds = nbuf * stage_bytes
+    acc = nb * tm * tn / (64 * waves)
+    per_cu = max(1, min(LDS_BYTES // max(lds, 1), max(1, int(512 // max(acc + 64, 1)) * 4 // waves), 32 // waves))
+    n_wg = -(-M // tm) * (N // tn)
+    slots = CUS * per_cu
+    rounds = n_wg / slots
+    tail = rounds / max(1, -(-n_wg // slots))
+    return [math.log2(tm), math.log2(tn), math.log2(tk), waves, wtm, wtn, acc, lds / 1024.0, per_cu,
+            rounds, tail, (wtm + nb * wtn) / (wtm * nb * wtn), (tm + nb * tn) / (tm * nb * tn),
+            K / tk, st, d[pre + "mfma"], d[pre + "vec"], occ]
+
+
+def schedule_features(op: rc.Op, sched: rc.Schedule) -> List[float]:
+    """Surrogate input: the raw knob values plus analytic features derived
+    from them and the operator's shape (tiles per compute unit, rounds of
+    workgroups and the last round's fill, accumulator registers, LDS bytes,
+    operand bytes per FLOP from LDS and from memory, dependent key tiles of
+    the longest attention query tile)."""
+    d = sched.as_dict()
+    f = [float(v) for v in d.values()]
+    D = op.dims
+    if op.kind == rc.RC_OP_GATED_MLP:
+        T, Hd, I = D
+        f += _gemm_block_features(d, "up.", T, I, Hd, 2) + _gemm_block_features(d, "down.", T, Hd, I, 1)
+    elif op.kind == rc.RC_OP_MOE:
+        T, Hd, E, I, k = D
+        rows = T * k + E * 64      # routed rows plus about half a tile of padding per expert
+        f += _gemm_block_features(d, "up.", rows, I, Hd, 2) + _gemm_block_features(d, "down.", rows, Hd, I, 1)
+    elif op.kind == rc.RC_OP_CONV2D:
+        N, H, W, C, K, R, S, pad = D
+        P, Q = H + 2 * pad - R + 1, W + 2 * pad - S + 1
+        f += _gemm_block_features(d, "", N * P * Q, K, R * S * C, 1)
+    elif op.kind == rc.RC_OP_ATTENTION:
+        B, H, S, Dh = D
+        bm, bn, w, sp, ch = d["block_m"], d["block_n"], d["waves"], d["splits"], d["chunk"]
+        nkt = -(-S // bn)
+        chain = (ch if ch > 0 else nkt) / sp          # dependent key tiles of the longest work item
+        nq = -(-S // bm)
+        items = B * H * nq * (1 if ch == 0 else -(-nkt // ch))
+        f += [bm / w, w * sp, chain, items / CUS, bm * bn / (64.0 * w), d["stages"] * 1.0]
+    return f
+
+
 class SurrogateEvaluator:
     """Rollout rewards from a learned surrogate (Sec. 3.2: the terminal
     program of a rollout is scored by a cheap learned model f-hat rather
@@ -435,10 +494,11 @@ class SurrogateEvaluator:
     measurement again at no cost."""
 
     def __init__(self, op: rc.Op, inner, seed: int, warm: int = 16, refit: int = 8,
-                 margin: float = 0.9, explore: float = 0.05):
+                 margin: float = 0.9, explore: float = 0.05, feature_set: str = "analytic"):
         import random
         self.op, self.inner, self.seed = op, inner, seed
         self.warm, self.refit, self.margin, self.explore = warm, refit, margin, explore
+        self.feature_set = feature_set          # "analytic" (schedule_features) or "raw" knob values
         self.rng = random.Random(seed)
         self.X: List[List[int]] = []
         self.y: List[float] = []
@@ -452,9 +512,10 @@ class SurrogateEvaluator:
         self.best_text: Optional[str] = None
         self.curve: List[float] = []
 
-    @staticmethod
-    def features(sched: rc.Schedule) -> List[int]:
-        return list(sched.as_dict().values())
+    def features(self, sched: rc.Schedule) -> List[float]:
+        if self.feature_set == "raw":
+            return [float(v) for v in sched.as_dict().values()]
+        return schedule_features(self.op, sched)
 
     def _fit(self):
         from sklearn.ensemble import ExtraTreesRegressor
@@ -496,9 +557,10 @@ class SurrogateEvaluator:
 
 
 def run_search(op, evaluator, policy: str, budget: int, seed: int, horizon=12, branching=2,
-               c=math.sqrt(2.0), proposer: Optional[str] = None, surrogate: bool = False):
+               c=math.sqrt(2.0), proposer: Optional[str] = None, surrogate: bool = False,
+               surrogate_features: str = "analytic"):
     prop = FeedbackProposer(op, seed) if proposer == "feedback" else None
-    sur = SurrogateEvaluator(op, evaluator, seed) if surrogate else None
+    sur = SurrogateEvaluator(op, evaluator, seed, feature_set=surrogate_features) if surrogate else None
 
     def ev(s):
         if sur is not None:
@@ -578,6 +640,8 @@ def main(argv=None):
                     help="expansion proposals from measured history (default: random legal)")
     ap.add_argument("--surrogate", action="store_true",
                     help="score rollouts with a learned surrogate; measure only promising ones")
+    ap.add_argument("--surrogate-features", default="analytic", choices=["analytic", "raw"],
+                    help="surrogate inputs: knob values plus analytic resource features, or knob values only")
     ap.add_argument("--repeat", type=int, default=10)
     ap.add_argument("--out", default="tune_out")
     ap.add_argument("--enumerate", action="store_true", help="list the whole legal space")
@@ -636,6 +700,8 @@ def main(argv=None):
         return
 
     tag = args.policy + (f"+{args.proposer}" if args.proposer else "") + ("+surrogate" if args.surrogate else "")
+    if args.surrogate and args.surrogate_features != "analytic":
+        tag += "-" + args.surrogate_features
     log = open(os.path.join(args.out, f"{args.workload}.{tag}.jsonl"), "a")
     if args.replay:
         evaluator = TableEvaluator(args.replay, op, args.column)
@@ -658,7 +724,7 @@ def main(argv=None):
     for seed in _parse_seeds(args.seeds):
         t0 = time.time()
         res = run_search(op, evaluator, args.policy, args.budget, seed, args.horizon, args.branching, args.c,
-                         args.proposer, args.surrogate)
+                         args.proposer, args.surrogate, args.surrogate_features)
         res.update(workload=args.workload, kind="search", wall_s=time.time() - t0)
         log.write(json.dumps(res) + "\n")
         log.flush()

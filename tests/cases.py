@@ -141,6 +141,10 @@ SCHEDULES = {
         "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=2,occ=4,splits=2",
         "block_m=32,block_n=32,waves=2,mfma=16,stages=4,vec=8,unroll=1,order=0,occ=2,splits=2",
         "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=1,occ=4,splits=2,chunk=4",
+        # four key splits sharing a ring of eight direct-to-LDS slots
+        "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=1,occ=4,splits=4",
+        "block_m=32,block_n=32,waves=2,mfma=16,stages=4,vec=8,unroll=2,order=0,occ=2,splits=4",
+        "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=2,occ=4,splits=4,chunk=4",
     ],
     "attn_full": [
         "",
@@ -152,6 +156,7 @@ SCHEDULES = {
         "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=0,chunk=4",
         "block_m=64,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=1,order=0",
         "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=0,occ=4,splits=2",
+        "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=0,occ=4,splits=4",
     ],
     "attn_d64": [
         "block_m=64,block_n=32,waves=2,mfma=32,stages=2,vec=8,unroll=1,order=0",
@@ -159,6 +164,7 @@ SCHEDULES = {
         "block_m=32,block_n=32,waves=2,mfma=16,stages=4,vec=8,unroll=1,order=0",
         "block_m=32,block_n=32,waves=2,mfma=16,stages=5,vec=8,unroll=1,order=0",
         "block_m=32,block_n=32,waves=2,mfma=16,stages=4,vec=8,unroll=1,order=0,splits=2",
+        "block_m=32,block_n=32,waves=2,mfma=16,stages=4,vec=8,unroll=1,order=0,splits=4",
     ],
     "mlp": [
         "",
@@ -291,6 +297,7 @@ _ONE_ATTN = [
     "block_m=16,block_n=32,waves=1,mfma=16,stages=1,vec=4,unroll=1,order=0",
     "block_m=16,block_n=32,waves=1,mfma=16,stages=3,vec=8,unroll=1,order=0",
     "block_m=16,block_n=32,waves=1,mfma=16,stages=4,vec=8,unroll=1,order=0,occ=1,splits=2",
+    "block_m=16,block_n=32,waves=1,mfma=16,stages=4,vec=8,unroll=1,order=0,occ=1,splits=4",
 ]
 _ONE_MLP = [
     "",
@@ -338,6 +345,8 @@ FULL_ALT = [
      "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=1,occ=4,splits=2"),
     ("attention_causal_b1_h32_s1024_d128",
      "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=2,occ=2,chunk=16"),
+    ("attention_causal_b1_h32_s1024_d128",
+     "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=1,occ=4,splits=4"),
     ("gated_mlp_t2048_h4096_i14336",
      _block("up.", 128, 128, 64, 2, 2, 16, 5, 8, 1, 1, 1) + "," +
      _block("down.", 128, 256, 64, 2, 4, 16, 4, 8, 1, 1, 1) + ",fuse=1"),
