@@ -277,13 +277,22 @@ def summarize_campaign(runs: List[dict], ref_reward: float, budget: int) -> Dict
     return out
 
 
+def default_horizon(op: rc.Op) -> int:
+    """Sequence length T: 12 transformations per GEMM block of knobs (the
+    gated MLP and the MoE carry two blocks, gate/up and down, so their
+    tuned schedules lie about twenty single-knob transformations from P0)."""
+    return 24 if op.kind in (rc.RC_OP_GATED_MLP, rc.RC_OP_MOE) else 12
+
+
 def run_campaign(op: rc.Op, name: str, policies: List[str], seeds: List[int], budget: int,
                  reference: str, jobs: int, out_path: str, cache_dir: Optional[str],
-                 repeat: int = 10, slow_ms: float = 50.0, log=None, time_fn=None, compile_fn=None) -> dict:
+                 repeat: int = 10, slow_ms: float = 50.0, log=None, time_fn=None, compile_fn=None,
+                 horizon: Optional[int] = None) -> dict:
     """Every (policy, seed) search in its own thread against one shared
     ParallelGpuEvaluator; the reference (tuned) schedule is measured the
     same way before and after."""
     import threading
+    T = horizon if horizon else default_horizon(op)
     ev = ParallelGpuEvaluator(op, jobs=jobs, repeat=repeat, slow_ms=slow_ms, cache_dir=cache_dir, log=log,
                               time_fn=time_fn, compile_fn=compile_fn)
     ref_sched = op.from_string(reference)
@@ -295,7 +304,7 @@ def run_campaign(op: rc.Op, name: str, policies: List[str], seeds: List[int], bu
     def one(pname, seed):
         try:
             a = _policy_args(pname)
-            r = run_search(op, ev, a["policy"], budget, seed, branching=a["branching"],
+            r = run_search(op, ev, a["policy"], budget, seed, horizon=T, branching=a["branching"],
                            proposer=a["proposer"], surrogate=a["surrogate"])
             r["policy_name"] = pname
             r["wall_s"] = time.time() - t0
@@ -315,7 +324,7 @@ def run_campaign(op: rc.Op, name: str, policies: List[str], seeds: List[int], bu
     ev.close()
     ref_reward = max(ref0.get("reward", 0.0), ref1.get("reward", 0.0))
     rec = {"workload": name, "dims": list(op.dims), "flags": op.flags, "budget": budget,
-           "seeds": seeds, "policies": policies,
+           "seeds": seeds, "policies": policies, "horizon": T,
            "measurement": (f"cold: a 512 MiB buffer overwritten before each timed launch; median of "
                            f"{repeat} launches (one launch when it exceeds {slow_ms:g} ms)"),
            "reward": "fraction of the binding roofline (bf16 MFMA peak or HBM bandwidth) at the median",
@@ -633,7 +642,8 @@ def main(argv=None):
     ap.add_argument("--policy", default="uct", choices=list(POLICIES) + ["list"])
     ap.add_argument("--budget", type=int, default=64)
     ap.add_argument("--seeds", default="0")
-    ap.add_argument("--horizon", type=int, default=12)
+    ap.add_argument("--horizon", type=int, default=0,
+                    help="sequence length T (default: 12 per GEMM block of knobs, 24 for the MLP and MoE)")
     ap.add_argument("--branching", type=int, default=2)
     ap.add_argument("--c", type=float, default=math.sqrt(2.0))
     ap.add_argument("--proposer", default=None, choices=["feedback"],
@@ -690,7 +700,7 @@ def main(argv=None):
         log = open(os.path.join(args.out, f"{args.workload}.campaign.jsonl"), "a")
         rec = run_campaign(op, args.workload, pols, _parse_seeds(args.seeds), args.budget,
                            tuned[args.workload], args.jobs, path, args.cache_dir, repeat=args.repeat,
-                           slow_ms=args.slow_ms, log=log)
+                           slow_ms=args.slow_ms, log=log, horizon=args.horizon)
         print(json.dumps({k: rec[k] for k in ("workload", "reference_reward", "distinct_schedules",
                                                "invalid", "wall_s", "errors")}), flush=True)
         for pname, sm in rec["summary"].items():
@@ -721,9 +731,10 @@ def main(argv=None):
         log.write(json.dumps({"kind": "list_best", "workload": args.workload, **(best or {})}) + "\n")
         return
 
+    horizon = args.horizon if args.horizon else default_horizon(op)
     for seed in _parse_seeds(args.seeds):
         t0 = time.time()
-        res = run_search(op, evaluator, args.policy, args.budget, seed, args.horizon, args.branching, args.c,
+        res = run_search(op, evaluator, args.policy, args.budget, seed, horizon, args.branching, args.c,
                          args.proposer, args.surrogate, args.surrogate_features)
         res.update(workload=args.workload, kind="search", wall_s=time.time() - t0)
         log.write(json.dumps(res) + "\n")
