@@ -274,9 +274,8 @@ def main():
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": achieved / HBM_PEAK_GBS}
     else:
-        # the dominant kernel's FLOPs: its share of the operator's contraction
-        share = {rc.RC_OP_GATED_MLP: 2.0 / 3.0, rc.RC_OP_MOE: 2.0 / 3.0}.get(op.kind, 1.0)
-        achieved = flops * share / (dom_ms * 1e-3) / 1e12
+        # the dominant kernel's own algorithmic FLOPs
+        achieved = plan.kernel_flops(dom) / (dom_ms * 1e-3) / 1e12
         peak = op.peak_flops() / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                 "frac": achieved / peak}

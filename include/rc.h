@@ -80,6 +80,10 @@ typedef enum rc_op_kind {
      * [Hd][I] (up.layout 0) or [I][Hd] (up.layout 1); in[3] = Wd stored
      * [I][Hd] (down.layout 0) or [Hd][I] (down.layout 1); out[0] = [T][Hd]. */
     RC_OP_GATED_MLP = 3,
+    /* (Schedules of the gated MLP have the knobs up.tail / down.tail: with
+     * 1, the column tiles of a last, partial round of workgroups run as a
+     * second launch with half-height tiles, so rc_plan_kernels may count
+     * up to two launches per GEMM.) */
     /* Routed mixture of gated-MLP experts (the MoE layer of Sec. 4.1):
      *   out[t] = bf16( sum_s w[t][s] * expert_{ids[t][s]}(X[t]) ),
      *   expert_e(x) = bf16( SiLU(x Wg[e]) * (x Wu[e]) ) Wd[e].
@@ -232,6 +236,11 @@ rc_status rc_plan_workspace(const rc_plan *p, size_t *bytes);
 /* Number of kernels one launch enqueues, and the index of the one doing
  * most of the FLOPs (the contraction). */
 rc_status rc_plan_kernels(const rc_plan *p, int32_t *nkernels, int32_t *dominant);
+
+/* Algorithmic FLOPs of kernel `kernel` of a launch (2 per multiply-add of
+ * the contraction it computes; 0 for routing, combine, reduction and
+ * elementwise kernels).  The kernels' FLOPs add up to rc_op_flops. */
+rc_status rc_plan_kernel_flops(const rc_plan *p, int32_t kernel, double *flops);
 
 /* Byte offset and size of a named part of the workspace, so that a caller
  * can read intermediate results after a launch (each part starts on a

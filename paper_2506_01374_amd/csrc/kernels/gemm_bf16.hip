@@ -31,6 +31,7 @@
 //   LAYOUT       weights stored 0: [K][N], 1: [N][K] (Layout)
 //   GRID         0: tile n fastest; 1: tile m fastest, with workgroups
 //                regrouped so each XCD owns a contiguous range of tiles
+//   NT_FIRST NT_COUNT  column tiles of this launch (default: all of GN)
 //   OCC          waves per SIMD the register allocation must leave room for
 //   NB           weight operands sharing the A tile (1, or 2 for gate/up)
 //   AMODE        A rows: 0 dense [GM][GK]; 1 MoE gather (row p of expert e
@@ -69,7 +70,15 @@
 // them; at least 1 keeps their unused arrays well formed)
 #define A_LOADS ((TM * TK) / (VEC * NT) > 0 ? (TM * TK) / (VEC * NT) : 1)
 #define B_LOADS ((TN * TK) / (VEC * NT) > 0 ? (TN * TK) / (VEC * NT) : 1)
-#define NTN (GN / TN)
+// this launch's column tiles: NT_COUNT tiles starting at tile NT_FIRST (a
+// GEMM may be split over two launches by column ranges)
+#ifndef NT_FIRST
+#define NT_FIRST 0
+#endif
+#ifndef NT_COUNT
+#define NT_COUNT (GN / TN)
+#endif
+#define NTN NT_COUNT
 
 typedef unsigned short bf16_t;
 
@@ -191,7 +200,7 @@ void rc_gemm_bf16(GemmBf16Args args) {
 #else
     int mt = bid / NTN, nt = bid % NTN;
 #endif
-    const int n0 = nt * TN;
+    const int n0 = (NT_FIRST + nt) * TN;
 
 #if AMODE == 1 || AMODE == 3
     // Ragged expert groups: find the expert owning M tile `mt`.

@@ -74,10 +74,19 @@ static std::vector<KnobDef> mlp_knobs() {
     add_gemm_block(v, UP, {16, 32, 64, 128, 256}, {32, 64, 128});
     add_gemm_block(v, DOWN, {16, 32, 64, 128, 256}, {32, 64, 128});
     v.push_back({"fuse", "ComputeLocation", {0, 1}, 0});
+    // 1: the column tiles of a last, partial round of workgroups run as a
+    // second launch with half-height tiles (twice as many, half the work
+    // each), so that round is as short as its share of the work
+    v.push_back({"up.tail", "Parallel", {0, 1}, 0});
+    v.push_back({"down.tail", "Parallel", {0, 1}, 0});
     return v;
 }
 
-static std::vector<KnobDef> moe_knobs() { return mlp_knobs(); }
+static std::vector<KnobDef> moe_knobs() {
+    std::vector<KnobDef> v = mlp_knobs();
+    v.resize(v.size() - 2);     // expert groups are ragged: no tail split
+    return v;
+}
 
 static std::vector<KnobDef> conv_knobs() {
     std::vector<KnobDef> v;
@@ -185,6 +194,26 @@ int gemm_ring_stages(int tm, int tn, int tk, int nb, int waves, int occ) {
     const int64_t wgs = std::max<int64_t>(1, (occ * 4 + waves - 1) / waves);
     const int64_t lpt = std::max<int64_t>(1, sb / 1024 / waves);
     return (int)std::min<int64_t>(std::min<int64_t>(12, LDS_LIMIT / (wgs * sb)), 63 / lpt + 2);
+}
+
+// Column split of a GEMM block whose workgroups end in a partial round:
+// the columns of whole rounds stay in the first launch, the rest go to a
+// second launch with half-height tiles.  Workgroups per CU are estimated
+// from the occupancy the schedule asks for and its LDS.  Returns false
+// when every round is full (nothing to split).
+bool gemm_tail_split(int tm, int tn, int tk, int nb, int waves, int occ, int st, int64_t M, int64_t N,
+                     int64_t *main_cols, int64_t *tail_cols) {
+    const int64_t stage_bytes = ((int64_t)tm * tk + (int64_t)nb * tn * tk) * 2;
+    int64_t nbuf = st == 4 || st == 6 ? 3 : st > 1 ? 2 : 1;
+    if (st == 7) nbuf = gemm_ring_stages(tm, tn, tk, nb, waves, occ);
+    const int64_t by_lds = std::max<int64_t>(1, LDS_LIMIT / (nbuf * stage_bytes));
+    const int64_t wgs = std::min<int64_t>(by_lds, std::max<int64_t>(1, (int64_t)occ * 4 / waves));
+    const int64_t slots = 256 * wgs, ntm = (M + tm - 1) / tm, cols = N / tn;
+    const int64_t full_cols = (ntm * cols / slots) * slots / ntm;   // whole rounds, whole columns
+    if (full_cols <= 0 || full_cols >= cols) return false;
+    *main_cols = full_cols;
+    *tail_cols = cols - full_cols;
+    return true;
 }
 
 // Rules for one bf16 GEMM stage of shape M x N x K (M < 0: ragged expert
@@ -437,7 +466,26 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
             int64_t T = D[0], Hd = D[1], I = D[2];
             std::string r = check_bf16_block(d, s, UP, T, I, Hd, 2, "up");
             if (!r.empty()) return r;
-            return check_bf16_block(d, s, DOWN, T, Hd, I, 1, "down");
+            r = check_bf16_block(d, s, DOWN, T, Hd, I, 1, "down");
+            if (!r.empty()) return r;
+            for (int b = 0; b < 2; ++b) {
+                const char *const *nm = b == 0 ? UP : DOWN;
+                const char *tag = b == 0 ? "up" : "down";
+                if (kv(d, s, b == 0 ? "up.tail" : "down.tail") != 1) continue;
+                const int64_t N = b == 0 ? I : Hd, K = b == 0 ? Hd : I;
+                const int nb = b == 0 ? 2 : 1;
+                int64_t mc = 0, tc = 0;
+                if (!gemm_tail_split(kv(d, s, nm[0]), kv(d, s, nm[1]), kv(d, s, nm[2]), nb,
+                                     kv(d, s, nm[3]) * kv(d, s, nm[4]), kv(d, s, nm[11]), kv(d, s, nm[6]), T, N,
+                                     &mc, &tc))
+                    return fmt("%s: tail split: no partial round of workgroups to split", tag);
+                // the tail launch runs the same schedule with half-height tiles
+                rc_schedule h = *s;
+                h.knob[knob_index(d->kind, nm[0])] = kv(d, s, nm[0]) / 2;
+                std::string why = check_bf16_block(d, &h, nm, T, N, K, nb, tag);
+                if (!why.empty()) return fmt("%s: tail split: the half-height tile is illegal (%s)", tag, why.c_str());
+            }
+            return "";
         }
         case RC_OP_MOE: {
             int64_t Hd = D[1], E = D[2], I = D[3], topk = D[4];

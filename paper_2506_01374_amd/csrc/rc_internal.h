@@ -31,6 +31,10 @@ int32_t kv(const rc_op_desc *d, const rc_schedule *s, const char *name);
 // Depth of the direct-to-LDS ring of bf16 GEMM stages 7.
 int gemm_ring_stages(int tm, int tn, int tk, int nb, int waves, int occ);
 
+// Column split of a GEMM block over two launches (the "tail" knob).
+bool gemm_tail_split(int tm, int tn, int tk, int nb, int waves, int occ, int st, int64_t M, int64_t N,
+                     int64_t *main_cols, int64_t *tail_cols);
+
 // Legality with a reason; "" when legal.
 std::string check_schedule(const rc_op_desc *d, const rc_schedule *s);
 

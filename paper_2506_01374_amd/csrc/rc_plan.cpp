@@ -353,6 +353,7 @@ std::string def(const char *name, long long v) {
 struct Kern {
     Source src;
     dim3 grid, block;
+    double flops = 0;   // algorithmic FLOPs of this launch (contractions only)
     // fills the argument block from the caller's buffers and the workspace
     std::function<void(const rc_args *, char *ws, ArgBlob &blob)> bind;
     hipFunction_t fn = nullptr;
@@ -447,6 +448,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             else
                 k.grid = dim3((unsigned)((D[1] + tn - 1) / tn), (unsigned)((D[0] + tm - 1) / tm), 1);
             k.block = dim3(nt, 1, 1);
+            k.flops = 2.0 * D[0] * D[1] * D[2];
             k.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
                 put(b, GemmF32Args{a->in[0], a->in[1], a->out[0], split ? w + offP : nullptr});
             };
@@ -454,6 +456,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             p.dominant = 0;
             if (split) {
                 Kern kr = k;
+                kr.flops = 0;
                 kr.src.entry = "rc_gemm_f32_splitk_reduce";
                 kr.grid = dim3((unsigned)((D[0] * D[1] / 4 + 63) / 64), 1, 1);
                 kr.block = dim3(256, 1, 1);
@@ -465,6 +468,15 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             long T = D[0], Hd = D[1], I = D[2];
             GemmCfg up = read_block(d, s, "up."), dn = read_block(d, s, "down.");
             int fuse = kv(d, s, "fuse");
+            // column split of a block over a main and a tail launch
+            int64_t up_main = I / up.tn, up_tail = 0, dn_main = Hd / dn.tn, dn_tail = 0;
+            if (kv(d, s, "up.tail") == 1)
+                gemm_tail_split(up.tm, up.tn, up.tk, 2, up.wm * up.wn, up.occ, up.st, T, I, &up_main, &up_tail);
+            if (kv(d, s, "down.tail") == 1)
+                gemm_tail_split(dn.tm, dn.tn, dn.tk, 1, dn.wm * dn.wn, dn.occ, dn.st, T, Hd, &dn_main, &dn_tail);
+            auto cols = [](int64_t first, int64_t count) {
+                return def("NT_FIRST", first) + def("NT_COUNT", count);
+            };
             size_t offH = ws.add((size_t)T * I * 2, "hidden");
             size_t offG = 0, offU = 0;
             if (!fuse) {
@@ -472,9 +484,11 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
                 offU = ws.add((size_t)T * I * 4, "up.f32");
             }
             Kern k1;
-            k1.src = Source{SRC_gemm_bf16, "rc_gemm_bf16", gemm_defs(up, 2, 0, fuse ? 2 : 3, T, I, Hd)};
-            k1.grid = dim3((unsigned)(((T + up.tm - 1) / up.tm) * (I / up.tn)), 1, 1);
+            k1.src = Source{SRC_gemm_bf16, "rc_gemm_bf16",
+                            gemm_defs(up, 2, 0, fuse ? 2 : 3, T, I, Hd) + cols(0, up_main)};
+            k1.grid = dim3((unsigned)(((T + up.tm - 1) / up.tm) * up_main), 1, 1);
             k1.block = dim3(64 * up.wm * up.wn, 1, 1);
+            k1.flops = 4.0 * T * Hd * up_main * up.tn;
             k1.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
                 if (fuse)
                     put(b, GemmBf16Args{a->in[0], a->in[1], a->in[2], w + offH, nullptr, nullptr,
@@ -484,6 +498,15 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
                                         nullptr, nullptr, nullptr});
             };
             p.kerns.push_back(k1);
+            if (up_tail > 0) {
+                GemmCfg h = up;
+                h.tm /= 2;
+                Kern kt = k1;
+                kt.src.defines = gemm_defs(h, 2, 0, fuse ? 2 : 3, T, I, Hd) + cols(up_main, up_tail);
+                kt.grid = dim3((unsigned)(((T + h.tm - 1) / h.tm) * up_tail), 1, 1);
+                kt.flops = 4.0 * T * Hd * up_tail * up.tn;
+                p.kerns.push_back(kt);
+            }
             if (!fuse) {
                 Kern ke;
                 ke.src = Source{SRC_aux, "rc_swiglu_f32", def("EW_N", T * I) + def("EW_COLS", I)};
@@ -495,14 +518,24 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
                 p.kerns.push_back(ke);
             }
             Kern k2;
-            k2.src = Source{SRC_gemm_bf16, "rc_gemm_bf16", gemm_defs(dn, 1, 0, 0, T, Hd, I)};
-            k2.grid = dim3((unsigned)(((T + dn.tm - 1) / dn.tm) * (Hd / dn.tn)), 1, 1);
+            k2.src = Source{SRC_gemm_bf16, "rc_gemm_bf16", gemm_defs(dn, 1, 0, 0, T, Hd, I) + cols(0, dn_main)};
+            k2.grid = dim3((unsigned)(((T + dn.tm - 1) / dn.tm) * dn_main), 1, 1);
             k2.block = dim3(64 * dn.wm * dn.wn, 1, 1);
+            k2.flops = 2.0 * T * I * dn_main * dn.tn;
             k2.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
                 put(b, GemmBf16Args{w + offH, a->in[3], nullptr, a->out[0], nullptr, nullptr,
                                     nullptr, nullptr, nullptr});
             };
             p.kerns.push_back(k2);
+            if (dn_tail > 0) {
+                GemmCfg h = dn;
+                h.tm /= 2;
+                Kern kt = k2;
+                kt.src.defines = gemm_defs(h, 1, 0, 0, T, Hd, I) + cols(dn_main, dn_tail);
+                kt.grid = dim3((unsigned)(((T + h.tm - 1) / h.tm) * dn_tail), 1, 1);
+                kt.flops = 2.0 * T * I * dn_tail * dn.tn;
+                p.kerns.push_back(kt);
+            }
             p.dominant = 0;
             break;
         }
@@ -548,6 +581,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             long ntm_up = (R + up.tm - 1) / up.tm + E;
             k1.grid = dim3((unsigned)(ntm_up * (I / up.tn)), 1, 1);
             k1.block = dim3(64 * up.wm * up.wn, 1, 1);
+            k1.flops = 4.0 * R * Hd * I;
             k1.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
                 put(b, GemmBf16Args{a->in[0], a->in[3], a->in[4], w + (fuse ? offH : offG),
                                     fuse ? nullptr : w + offU, nullptr, w + offPerm, w + offOff,
@@ -570,6 +604,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             long ntm_dn = (R + dn.tm - 1) / dn.tm + E;
             k2.grid = dim3((unsigned)(ntm_dn * (Hd / dn.tn)), 1, 1);
             k2.block = dim3(64 * dn.wm * dn.wn, 1, 1);
+            k2.flops = 2.0 * R * I * Hd;
             k2.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
                 put(b, GemmBf16Args{w + offH, a->in[5], nullptr, w + offY, nullptr, nullptr,
                                     w + offPerm, w + offOff, w + offTd});
@@ -599,6 +634,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
                             gemm_defs(g, 1, 2, fuse ? (act ? 1 : 4) : 3, M, K, R * S * C) + cv};
             k1.grid = dim3((unsigned)(((M + g.tm - 1) / g.tm) * (K / g.tn)), 1, 1);
             k1.block = dim3(64 * g.wm * g.wn, 1, 1);
+            k1.flops = 2.0 * M * K * R * S * C;
             k1.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
                 if (fuse)
                     put(b, GemmBf16Args{a->in[0], a->in[1], nullptr, a->out[0], nullptr, a->in[2],
@@ -657,12 +693,14 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
                                def("CAUSAL", causal ? 1 : 0) + sbuf};
             k.grid = dim3((unsigned)(B * Hh * items), 1, 1);
             k.block = dim3(64 * w * kv(d, s, "splits"), 1, 1);
+            k.flops = rc_op_flops(d);
             k.bind = [=](const rc_args *a, char *ws_base, ArgBlob &b) {
                 put(b, AttnArgs{a->in[0], a->in[1], a->in[2], a->out[0], chunk > 0 ? ws_base + offP : nullptr});
             };
             p.kerns.push_back(k);
             if (chunk > 0) {
                 Kern kc = k;
+                kc.flops = 0;
                 kc.src.entry = "rc_attention_combine";
                 kc.grid = dim3((unsigned)(B * Hh * nqt), 1, 1);
                 kc.block = dim3(64 * w, 1, 1);
@@ -864,6 +902,13 @@ rc_status rc_plan_kernels(const rc_plan *p, int32_t *nkernels, int32_t *dominant
     if (!p) return fail(RC_ERR_INVALID_ARGUMENT, "null plan");
     if (nkernels) *nkernels = (int32_t)p->kerns.size();
     if (dominant) *dominant = p->dominant;
+    return RC_OK;
+}
+
+rc_status rc_plan_kernel_flops(const rc_plan *p, int32_t kernel, double *flops) {
+    if (!p || !flops) return fail(RC_ERR_INVALID_ARGUMENT, "null argument");
+    if (kernel < 0 || kernel >= (int32_t)p->kerns.size()) return fail(RC_ERR_INVALID_ARGUMENT, "kernel index out of range");
+    *flops = p->kerns[kernel].flops;
     return RC_OK;
 }
 

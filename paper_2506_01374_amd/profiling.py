@@ -48,20 +48,22 @@ def kernel_stats(dirpath: str) -> List[Dict[str, float]]:
 
 
 def dispatch_stats(dirpath: str) -> List[Dict[str, float]]:
-    """Per (kernel name, grid size in threads) duration statistics from the
-    per-dispatch ``*_kernel_trace.csv`` (two launches of one kernel with
-    different schedules share a name but not a grid)."""
+    """Per (kernel name, grid size in threads, workgroup size) duration
+    statistics from the per-dispatch ``*_kernel_trace.csv`` (launches of one
+    kernel with different schedules share a name, not always a grid)."""
     groups: Dict[tuple, List[float]] = {}
     for path in _find(dirpath, "kernel_trace.csv"):
         with open(path) as f:
             for r in csv.DictReader(f):
                 g = int(r.get("Grid_Size_X", 0)) * int(r.get("Grid_Size_Y", 1)) * int(r.get("Grid_Size_Z", 1))
+                w = int(r.get("Workgroup_Size_X", 0)) * int(r.get("Workgroup_Size_Y", 1)) * \
+                    int(r.get("Workgroup_Size_Z", 1))
                 d = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
-                groups.setdefault((r.get("Kernel_Name", ""), g), []).append(d)
+                groups.setdefault((r.get("Kernel_Name", ""), g, w), []).append(d)
     out = []
-    for (name, g), ds in groups.items():
-        out.append({"name": name, "grid_threads": g, "calls": len(ds), "avg_ns": sum(ds) / len(ds),
-                    "min_ns": min(ds), "max_ns": max(ds)})
+    for (name, g, w), ds in groups.items():
+        out.append({"name": name, "grid_threads": g, "workgroup": w, "calls": len(ds),
+                    "avg_ns": sum(ds) / len(ds), "min_ns": min(ds), "max_ns": max(ds)})
     return sorted(out, key=lambda r: -r["avg_ns"] * r["calls"])
 
 
@@ -148,7 +150,7 @@ def main(argv=None):
                   f"min={r['min_ns'] / 1e3:9.3f} max={r['max_ns'] / 1e3:9.3f} ({r['pct']:.1f}%)")
     elif argv[:1] == ["dispatches"]:
         for r in dispatch_stats(argv[1]):
-            print(f"{r['name'][:50]:50s} grid={r['grid_threads']:9d} calls={r['calls']:6d} "
+            print(f"{r['name'][:50]:50s} grid={r['grid_threads']:9d} wg={r['workgroup']:5d} calls={r['calls']:6d} "
                   f"avg={r['avg_ns'] / 1e3:9.3f} us min={r['min_ns'] / 1e3:9.3f} max={r['max_ns'] / 1e3:9.3f}")
     elif argv[:1] == ["counter"]:
         print(counter_per_dispatch(argv[1], argv[2], argv[3], int(argv[4]) if len(argv) > 4 else 0))

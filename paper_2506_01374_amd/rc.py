@@ -133,6 +133,7 @@ _SIGS = [
     ("rc_plan_workspace", ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_size_t)]),
     ("rc_plan_kernels", ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32),
                                        ctypes.POINTER(ctypes.c_int32)]),
+    ("rc_plan_kernel_flops", ctypes.c_int, [ctypes.c_void_p, ctypes.c_int32, ctypes.POINTER(ctypes.c_double)]),
     ("rc_plan_buffer", ctypes.c_int, [ctypes.c_void_p, ctypes.c_char_p, ctypes.POINTER(ctypes.c_size_t),
                                       ctypes.POINTER(ctypes.c_size_t)]),
     ("rc_time_release", ctypes.c_int, []),
@@ -425,6 +426,12 @@ class Plan:
         if getattr(self, "h", None) and _lib is not None:
             _lib.rc_plan_destroy(self.h)
             self.h = None
+
+    def kernel_flops(self, i: int) -> float:
+        """Algorithmic FLOPs of kernel i of a launch."""
+        f = ctypes.c_double()
+        _check(lib().rc_plan_kernel_flops(self.h, i, ctypes.byref(f)), "rc_plan_kernel_flops")
+        return f.value
 
     def buffer(self, name: str):
         """(byte offset, bytes) of a named part of the workspace."""

@@ -50,6 +50,10 @@ SMALL = {
     "attn_one_causal": (rc.RC_OP_ATTENTION, (1, 2, 1, 128), rc.RC_FLAG_CAUSAL),
     "attn_one_full": (rc.RC_OP_ATTENTION, (1, 2, 1, 128), 0),
     "mlp_one": (rc.RC_OP_GATED_MLP, (1, 256, 512), 0),
+    # more workgroups than one round: the tail split of the gate/up GEMM
+    # (I = 2304) and of the down GEMM (Hd = 576) runs a second launch
+    "mlp_tail": (rc.RC_OP_GATED_MLP, (256, 256, 2304), 0),
+    "mlp_tail_down": (rc.RC_OP_GATED_MLP, (1024, 576, 256), 0),
     "moe_one": (rc.RC_OP_MOE, (1, 256, 8, 128, 2), 0),
     "conv_one": (rc.RC_OP_CONV2D, (1, 1, 1, 64, 64, 3, 3, 1), 0),
 }
@@ -255,6 +259,20 @@ SCHEDULES = {
     ],
 }
 
+SCHEDULES["mlp_tail"] = [
+    _block("up.", 64, 32, 64, 2, 2, 16, 2, 8, 1, 1, 1) + "," +
+    _block("down.", 64, 64, 64, 2, 2, 16, 2, 8, 1, 1, 0) + ",fuse=1,up.tail=1",
+    _block("up.", 64, 32, 64, 2, 2, 16, 7, 8, 1, 1, 1) + "," +
+    _block("down.", 64, 64, 64, 2, 2, 16, 3, 8, 1, 1, 0) + ",fuse=1,up.tail=1",
+    _block("up.", 64, 32, 32, 2, 2, 16, 5, 4, 1, 1, 0) + "," +
+    _block("down.", 32, 64, 64, 1, 2, 16, 2, 8, 1, 1, 0) + ",fuse=0,up.tail=1",
+]
+SCHEDULES["mlp_tail_down"] = [
+    _block("up.", 64, 64, 64, 2, 2, 16, 2, 8, 1, 1, 1) + "," +
+    _block("down.", 64, 32, 64, 2, 2, 16, 2, 8, 1, 1, 1) + ",fuse=1,down.tail=1",
+    _block("up.", 64, 64, 64, 2, 2, 16, 7, 8, 1, 1, 1) + "," +
+    _block("down.", 64, 32, 64, 2, 2, 16, 7, 8, 1, 1, 0) + ",fuse=1,down.tail=1",
+]
 SCHEDULES["conv_k320"] = [
     _block("", 64, 80, 64, 1, 1, 16, 2, 8, 1, 1, 0) + ",fuse=1",
     _block("", 32, 160, 64, 1, 2, 16, 5, 8, 1, 1, 1) + ",fuse=1",
@@ -355,6 +373,13 @@ FULL_ALT = [
      _block("down.", 128, 128, 64, 2, 2, 16, 3, 8, 1, 1, 0) + ",fuse=1"),
     ("conv3x3_n2_64x64_c320_k320",
      _block("", 64, 64, 64, 4, 2, 16, 2, 8, 1, 1, 1) + ",fuse=1"),
+    # the gate/up GEMM's last half round as a second, half-height launch
+    ("gated_mlp_t2048_h4096_i14336",
+     _block("up.", 256, 128, 64, 4, 4, 16, 2, 8, 1, 1, 1, 2) + "," +
+     _block("down.", 128, 128, 64, 2, 2, 16, 3, 8, 1, 1, 0) + ",fuse=1,up.tail=1"),
+    ("gated_mlp_t2048_h4096_i14336",
+     _block("up.", 256, 128, 32, 2, 4, 16, 7, 8, 1, 1, 1) + "," +
+     _block("down.", 128, 128, 64, 2, 2, 16, 3, 8, 1, 1, 0) + ",fuse=1,up.tail=1"),
     # deep direct-to-LDS ring at full size
     ("gated_mlp_t2048_h4096_i14336",
      _block("up.", 256, 128, 32, 4, 2, 16, 7, 8, 1, 1, 1, 2) + "," +
