@@ -91,7 +91,10 @@ typedef enum rc_op_kind {
      * [T][topk] int32 in [0, E); in[2] = w [T][topk] fp32; in[3] = Wg,
      * in[4] = Wu stored [E][Hd][I] (up.layout 0) or [E][I][Hd] (1);
      * in[5] = Wd stored [E][I][Hd] (down.layout 0) or [E][Hd][I] (1);
-     * out[0] = [T][Hd] bf16.  Routing (ids, w) is an input. */
+     * out[0] = [T][Hd] bf16.  Routing (ids, w) is an input.
+     * (Its schedules have the knobs up.skip / down.skip: with 1, an
+     * expert's last, partial M tile skips the MFMAs of its empty row blocks;
+     * the result is the same.) */
     RC_OP_MOE = 4,
     /* 2-D convolution, stride 1, zero padding, bias and SiLU (the
      * convolution layer of Sec. 4.1), as an implicit GEMM:

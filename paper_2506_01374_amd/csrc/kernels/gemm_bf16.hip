@@ -30,8 +30,15 @@
 //   UNROLL       unroll factor of the K-tile loop (Unroll)
 //   LAYOUT       weights stored 0: [K][N], 1: [N][K] (Layout)
 //   GRID         0: tile n fastest; 1: tile m fastest, with workgroups
-//                regrouped so each XCD owns a contiguous range of tiles
+//                regrouped so each XCD owns a contiguous range of tiles;
+//                2: tile n fastest, each XCD owning a contiguous range of
+//                the tiles that hold rows (for the MoE GEMMs the ones the
+//                routing filled), so the workgroups sharing an A tile, and
+//                an expert's weights, run on one XCD and its L2
 //   NT_FIRST NT_COUNT  column tiles of this launch (default: all of GN)
+//   ROWSKIP      MoE only: 1 - a tile past its expert's last row runs a
+//                second copy of the main loop that skips the fragment reads
+//                and MFMAs of its waves' empty row blocks (ComputeLocation)
 //   OCC          waves per SIMD the register allocation must leave room for
 //   NB           weight operands sharing the A tile (1, or 2 for gate/up)
 //   AMODE        A rows: 0 dense [GM][GK]; 1 MoE gather (row p of expert e
@@ -78,6 +85,10 @@
 #ifndef NT_COUNT
 #define NT_COUNT (GN / TN)
 #endif
+#ifndef ROWSKIP
+#define ROWSKIP 0
+#endif
+#define PART_TILES (ROWSKIP && (AMODE == 1 || AMODE == 3))
 #define NTN NT_COUNT
 
 typedef unsigned short bf16_t;
@@ -197,6 +208,22 @@ void rc_gemm_bf16(GemmBf16Args args) {
     if ((nblk & 7) == 0) bid = (bid & 7) * (nblk >> 3) + (bid >> 3);
     const int ntm_grid = nblk / NTN;
     int mt = bid % ntm_grid, nt = bid / ntm_grid;
+#elif GRID == 2
+    // Workgroups reach the 8 XCDs round-robin (workgroup b on XCD b % 8):
+    // XCD x takes work items [x * per, (x + 1) * per) of the live ones, in
+    // its own dispatch order; the rest of its workgroups exit at once.
+#if AMODE == 1 || AMODE == 3
+    const int live = args.tile_start[NEXP] * NTN;
+#else
+    const int live = nblk;
+#endif
+    if ((nblk & 7) == 0) {
+        const int per = (live + 7) >> 3, li = bid >> 3;
+        if (li >= per) return;
+        bid = (bid & 7) * per + li;
+    }
+    if (bid >= live) return;
+    int mt = bid / NTN, nt = bid % NTN;
 #else
     int mt = bid / NTN, nt = bid % NTN;
 #endif
@@ -229,6 +256,13 @@ void rc_gemm_bf16(GemmBf16Args args) {
 #if NB == 2
     const bf16_t *B1 = args.B1;
 #endif
+#endif
+
+#if PART_TILES
+    // MF-row blocks of this wave that hold routed rows; the products of the
+    // blocks past the group's last row would never be stored, so a partial
+    // tile skips their fragment reads and MFMAs
+    const int fm_live = __builtin_amdgcn_readfirstlane(min(FM, max(0, (rows_valid - wm * WTM + MF - 1) / MF)));
 #endif
 
     // ---- per-thread A row sources (fixed over the K loop) ---------------
@@ -357,7 +391,13 @@ void rc_gemm_bf16(GemmBf16Args args) {
     int foff[TK / KSTEP];
 #pragma unroll
     for (int ks = 0; ks < TK / KSTEP; ++ks) foff[ks] = swz(lane % MF, ks * (KSTEP / 8) + lane / MF);
-    auto load_frags = [&](const bf16_t *la, const bf16_t (*lb)[TN * TK], int ks, Frags &f) {
+    // `part` (IntC<0> or IntC<1>) selects the full tile or a partial MoE
+    // tile whose wave holds fm_live live row blocks.
+    auto load_frags = [&](const bf16_t *la, const bf16_t (*lb)[TN * TK], int ks, Frags &f, auto part) {
+#if PART_TILES
+        if constexpr (decltype(part)::value)
+            if (fm_live == 0) return;
+#endif
 #pragma unroll
         for (int i = 0; i < FM; ++i)
             f.a[i] = *(const bf16x8 *)(la + (wm * WTM + i * MF) * TK + foff[ks]);
@@ -367,30 +407,52 @@ void rc_gemm_bf16(GemmBf16Args args) {
             for (int j = 0; j < FN; ++j)
                 f.b[b][j] = *(const bf16x8 *)(lb[b] + (wn * WTN + j * MF) * TK + foff[ks]);
     };
-    auto mfmas = [&](const Frags &f) {
-#pragma unroll
-        for (int b = 0; b < NB; ++b)
+    auto mfmas = [&](const Frags &f, auto part) {
+        if constexpr (decltype(part)::value) {
+#if PART_TILES
 #pragma unroll
             for (int i = 0; i < FM; ++i)
+                if (i < fm_live) {
 #pragma unroll
-                for (int j = 0; j < FN; ++j) acc[b][i][j] = mfma(f.b[b][j], f.a[i], acc[b][i][j]);
+                    for (int b = 0; b < NB; ++b)
+#pragma unroll
+                        for (int j = 0; j < FN; ++j) acc[b][i][j] = mfma(f.b[b][j], f.a[i], acc[b][i][j]);
+                }
+#endif
+        } else {
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < FN; ++j) acc[b][i][j] = mfma(f.b[b][j], f.a[i], acc[b][i][j]);
+        }
+    };
+    // Runs a main loop `run(part)`: a second copy for partial MoE tiles.
+    auto run_tiles = [&](auto &&run) {
+#if PART_TILES
+        if (fm_live == FM) run(IntC<0>{});
+        else run(IntC<1>{});
+#else
+        run(IntC<0>{});
+#endif
     };
     // One K tile from LDS buffer s.  The fragments of k-step ks + 1 are read
     // while the MFMAs of k-step ks issue; `mid` (the LDS store of the next
     // tile into the other buffer) runs halfway through the MFMAs.
-    auto compute_at = [&](const bf16_t *la, const bf16_t (*lb)[TN * TK], auto &&mid) {
+    auto compute_at = [&](const bf16_t *la, const bf16_t (*lb)[TN * TK], auto &&mid, auto part) {
         constexpr int KS = TK / KSTEP;
         Frags f[2];
-        load_frags(la, lb, 0, f[0]);
+        load_frags(la, lb, 0, f[0], part);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-            if (ks + 1 < KS) load_frags(la, lb, ks + 1, f[(ks + 1) & 1]);
+            if (ks + 1 < KS) load_frags(la, lb, ks + 1, f[(ks + 1) & 1], part);
             if (ks == KS / 2) mid();
-            mfmas(f[ks & 1]);
+            mfmas(f[ks & 1], part);
         }
         if (KS == 1) mid();
     };
-    auto compute = [&](int s, auto &&mid) { compute_at(As[s], Bs[s], mid); };
+    auto compute = [&](int s, auto &&mid, auto part) { compute_at(As[s], Bs[s], mid, part); };
 
     auto nothing = [] {};
 #if STAGES == 4
@@ -462,9 +524,9 @@ void rc_gemm_bf16(GemmBf16Args args) {
     // tile kt sits in buffer kt % 3; buffer (kt + 2) % 3 held tile kt - 1,
     // finished before the last barrier, and receives tile kt + 2
     auto body = [&](int kt, bf16_t *cur_a, bf16_t (*cur_b)[TN * TK], bf16_t *fill_a,
-                    bf16_t (*fill_b)[TN * TK]) {
+                    bf16_t (*fill_b)[TN * TK], auto part) {
         if (kt + 2 < KTILES) gload_lds((kt + 2) * TK, fill_a, fill_b);
-        compute_at(cur_a, cur_b, nothing);
+        compute_at(cur_a, cur_b, nothing, part);
         if (kt + 2 < KTILES) {
             WAIT_VM(LPT);          // tile kt + 1 has landed; tile kt + 2 may be in flight
         } else {
@@ -477,11 +539,13 @@ void rc_gemm_bf16(GemmBf16Args args) {
         __builtin_amdgcn_s_waitcnt(0xC07F);      // lgkmcnt(0): this wave's LDS reads are done
         asm volatile("s_barrier" ::: "memory");
     };
-    for (int kt = 0; kt < KTILES; kt += 3) {
-        body(kt, As0, Bs0, As2, Bs2);
-        if (kt + 1 < KTILES) body(kt + 1, As1, Bs1, As0, Bs0);
-        if (kt + 2 < KTILES) body(kt + 2, As2, Bs2, As1, Bs1);
-    }
+    run_tiles([&](auto part) __attribute__((always_inline)) {
+        for (int kt = 0; kt < KTILES; kt += 3) {
+            body(kt, As0, Bs0, As2, Bs2, part);
+            if (kt + 1 < KTILES) body(kt + 1, As1, Bs1, As0, Bs0, part);
+            if (kt + 2 < KTILES) body(kt + 2, As2, Bs2, As1, Bs1, part);
+        }
+    });
 #undef WAIT_VM
 #elif STAGES == 7
     // Deep direct-to-LDS ring.  buffer_load_dwordx4 ... lds moves 64 lanes x
@@ -635,15 +699,17 @@ void rc_gemm_bf16(GemmBf16Args args) {
     auto stage_b = [&](const bf16_t *la) { return (const bf16_t (*)[TN * TK])(la + TM * TK); };
     // MFMAs of one k-step interleaved with the next k-step's fragment reads
     constexpr int NMF = NB * FM * FN, NRD = FM + NB * FN;
-    auto kstep = [&](const Frags &cur, const bf16_t *ln, int ksn, Frags &nxt) {
-        load_frags(ln, stage_b(ln), ksn, nxt);
-        mfmas(cur);
+    auto kstep = [&](const Frags &cur, const bf16_t *ln, int ksn, Frags &nxt, auto part) {
+        load_frags(ln, stage_b(ln), ksn, nxt, part);
+        mfmas(cur, part);
+        if constexpr (!decltype(part)::value) {
 #pragma unroll
-        for (int r = 0; r < NRD; ++r) {
-            __builtin_amdgcn_sched_group_barrier(0x008, NMF / NRD > 0 ? NMF / NRD : 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            for (int r = 0; r < NRD; ++r) {
+                __builtin_amdgcn_sched_group_barrier(0x008, NMF / NRD > 0 ? NMF / NRD : 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, NMF, 0);
         }
-        __builtin_amdgcn_sched_group_barrier(0x008, NMF, 0);
     };
     Frags f7[2];
 #pragma unroll
@@ -652,8 +718,7 @@ void rc_gemm_bf16(GemmBf16Args args) {
     wait_tiles(min(NSTAGE - 2, KTILES - 1));
     __builtin_amdgcn_s_waitcnt(0xC07F);
     asm volatile("s_barrier" ::: "memory");
-    load_frags(stage_a(0), stage_b(stage_a(0)), 0, f7[0]);
-    auto body7 = [&](int t, auto par) {
+    auto body7 = [&](int t, auto par, auto part) {
         constexpr int P = decltype(par)::value;
         if (t + 1 < KTILES) {
             // tile t + 1 has landed; every wave is done with tile t - 1's stage
@@ -668,18 +733,21 @@ void rc_gemm_bf16(GemmBf16Args args) {
         for (int ks = 0; ks < KS; ++ks) {
             const int ci = (P * KS + ks) & 1;          // a constant once unrolled
             if (ks + 1 < KS) {
-                if (ci == 0) kstep(f7[0], la, ks + 1, f7[1]);
-                else kstep(f7[1], la, ks + 1, f7[0]);
+                if (ci == 0) kstep(f7[0], la, ks + 1, f7[1], part);
+                else kstep(f7[1], la, ks + 1, f7[0], part);
             } else {
-                if (ci == 0) kstep(f7[0], ln, 0, f7[1]);
-                else kstep(f7[1], ln, 0, f7[0]);
+                if (ci == 0) kstep(f7[0], ln, 0, f7[1], part);
+                else kstep(f7[1], ln, 0, f7[0], part);
             }
         }
     };
-    for (int t = 0; t < KTILES; t += 2) {
-        body7(t, IntC<0>{});
-        if (t + 1 < KTILES) body7(t + 1, IntC<1>{});
-    }
+    run_tiles([&](auto part) __attribute__((always_inline)) {
+        load_frags(stage_a(0), stage_b(stage_a(0)), 0, f7[0], part);
+        for (int t = 0; t < KTILES; t += 2) {
+            body7(t, IntC<0>{}, part);
+            if (t + 1 < KTILES) body7(t + 1, IntC<1>{}, part);
+        }
+    });
 #undef WAIT_VM
 #elif STAGES == 6
     // Ping-pong.  Waves 0-3 (group 0) and 4-7 (group 1) hold one wave per
@@ -802,7 +870,7 @@ void rc_gemm_bf16(GemmBf16Args args) {
     auto compute_tile = [&]() {
         __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-        for (int ks = 0; ks < TK / KSTEP; ++ks) mfmas(fr[ks]);
+        for (int ks = 0; ks < TK / KSTEP; ++ks) mfmas(fr[ks], IntC<0>{});
         __builtin_amdgcn_s_setprio(0);
     };
     // Both groups run the same loop, "compute tile t; barrier; memory work
@@ -863,14 +931,16 @@ void rc_gemm_bf16(GemmBf16Args args) {
 #undef WAIT_LGKM0
 #undef SLOT_BARRIER
 #elif STAGES == 1
+    run_tiles([&](auto part) __attribute__((always_inline)) {
 #pragma unroll UNROLL
-    for (int kt = 0; kt < KTILES; ++kt) {
-        gload(kt * TK, 0);
-        swrite(0, 0);
-        __syncthreads();
-        compute(0, nothing);
-        __syncthreads();
-    }
+        for (int kt = 0; kt < KTILES; ++kt) {
+            gload(kt * TK, 0);
+            swrite(0, 0);
+            __syncthreads();
+            compute(0, nothing, part);
+            __syncthreads();
+        }
+    });
 #elif STAGES == 5
     // Tile t lives in register set t % 2 and LDS buffer t % 2.  Its loads are
     // issued at the end of iteration t - 3 (right after the set's previous
@@ -882,38 +952,42 @@ void rc_gemm_bf16(GemmBf16Args args) {
     if (KTILES > 1) gload(TK, 1);
     if (KTILES > 2) gload(2 * TK, 0);
     __syncthreads();
-    auto body = [&](int kt, auto par) {
+    auto body = [&](int kt, auto par, auto part) {
         constexpr int P = decltype(par)::value;
-        compute(P, nothing);
+        compute(P, nothing, part);
         if (kt + 1 < KTILES) swrite(1 - P, 1 - P);
         __syncthreads();
         if (kt + 3 < KTILES) gload((kt + 3) * TK, 1 - P);
     };
-    for (int kt = 0; kt < KTILES; kt += 2) {
-        body(kt, IntC<0>{});
-        if (kt + 1 < KTILES) body(kt + 1, IntC<1>{});
-    }
+    run_tiles([&](auto part) __attribute__((always_inline)) {
+        for (int kt = 0; kt < KTILES; kt += 2) {
+            body(kt, IntC<0>{}, part);
+            if (kt + 1 < KTILES) body(kt + 1, IntC<1>{}, part);
+        }
+    });
 #else
     gload(0, 0);
     swrite(0, 0);
     __syncthreads();
+    run_tiles([&](auto part) __attribute__((always_inline)) {
 #pragma unroll UNROLL
-    for (int kt = 0; kt < KTILES; ++kt) {
-        // buffer (kt + 1) & 1 was last read in iteration kt - 1, which ended
-        // with a barrier, so it may be overwritten during this tile's MFMAs
-        if (kt + 1 < KTILES) gload((kt + 1) * TK, 0);
-        const int nxt = (kt + 1) & 1;
-        const bool more = kt + 1 < KTILES;
+        for (int kt = 0; kt < KTILES; ++kt) {
+            // buffer (kt + 1) & 1 was last read in iteration kt - 1, which ended
+            // with a barrier, so it may be overwritten during this tile's MFMAs
+            if (kt + 1 < KTILES) gload((kt + 1) * TK, 0);
+            const int nxt = (kt + 1) & 1;
+            const bool more = kt + 1 < KTILES;
 #if STAGES == 3
-        compute(kt & 1, [&] {
-            if (more) swrite(nxt, 0);
-        });
+            compute(kt & 1, [&] {
+                if (more) swrite(nxt, 0);
+            }, part);
 #else
-        compute(kt & 1, nothing);
-        if (more) swrite(nxt, 0);
+            compute(kt & 1, nothing, part);
+            if (more) swrite(nxt, 0);
 #endif
-        __syncthreads();
-    }
+            __syncthreads();
+        }
+    });
 #endif
 
     // ---- epilogue --------------------------------------------------------

@@ -56,7 +56,9 @@ static void add_gemm_block(std::vector<KnobDef> &v, const char *const names[12],
     v.push_back({names[7], "Vectorize", {2, 4, 8}, 2});         // bf16 per global load
     v.push_back({names[8], "Unroll", {1, 2}, 1});
     v.push_back({names[9], "Layout", {0, 1}, 0});               // weight stored KxN / NxK
-    v.push_back({names[10], "Parallel", {0, 1}, 0});            // tile order: plain / XCD-grouped
+    // tile order: plain / XCD-grouped, m fastest / XCD-grouped over the
+    // tiles that hold rows, n fastest
+    v.push_back({names[10], "Parallel", {0, 1, 2}, 0});
     v.push_back({names[11], "Parallel", {1, 2}, 1});            // waves per SIMD to budget registers for
 }
 
@@ -85,6 +87,11 @@ static std::vector<KnobDef> mlp_knobs() {
 static std::vector<KnobDef> moe_knobs() {
     std::vector<KnobDef> v = mlp_knobs();
     v.resize(v.size() - 2);     // expert groups are ragged: no tail split
+    // 1: an expert's last, partial M tile runs a second copy of the GEMM's
+    // main loop that skips the fragment reads and MFMAs of its empty row
+    // blocks (full tiles keep the first copy unchanged)
+    v.push_back({"up.skip", "ComputeLocation", {0, 1}, 0});
+    v.push_back({"down.skip", "ComputeLocation", {0, 1}, 0});
     return v;
 }
 

@@ -372,12 +372,14 @@ struct WsLayout {
 
 struct GemmCfg {
     int tm, tn, tk, wm, wn, mf, st, vec, un, lay, grid, occ;
+    int skip;   // MoE only: partial tiles skip their empty row blocks
 };
 
 GemmCfg read_block(const rc_op_desc *d, const rc_schedule *s, const char *prefix) {
     auto k = [&](const char *n) { return kv(d, s, (std::string(prefix) + n).c_str()); };
     return GemmCfg{k("tile_m"), k("tile_n"), k("tile_k"), k("waves_m"), k("waves_n"), k("mfma"),
-                   k("stages"), k("vec"), k("unroll"), k("layout"), k("grid"), k("occ")};
+                   k("stages"), k("vec"), k("unroll"), k("layout"), k("grid"), k("occ"),
+                   std::max(0, k("skip"))};
 }
 
 std::string gemm_defs(const GemmCfg &g, int nb, int amode, int epi, long gm, long gn, long gk) {
@@ -386,6 +388,7 @@ std::string gemm_defs(const GemmCfg &g, int nb, int amode, int epi, long gm, lon
     s += def("MF", g.mf) + def("STAGES", g.st) + def("VEC", g.vec) + def("UNROLL", g.un);
     s += def("LAYOUT", g.lay) + def("GRID", g.grid) + def("NB", nb) + def("AMODE", amode);
     s += def("EPI", epi) + def("GM", gm) + def("GN", gn) + def("GK", gk) + def("OCC", g.occ);
+    if (g.skip) s += def("ROWSKIP", 1);
     if (g.st == 7) s += def("NSTAGE", gemm_ring_stages(g.tm, g.tn, g.tk, nb, g.wm * g.wn, g.occ));
     return s;
 }

@@ -202,6 +202,9 @@ SCHEDULES = {
         _block("down.", 128, 128, 64, 2, 2, 32, 7, 8, 1, 1, 1) + ",fuse=1",
         _block("up.", 64, 64, 64, 2, 2, 32, 7, 8, 1, 1, 0) + "," +
         _block("down.", 128, 256, 32, 2, 4, 16, 7, 8, 1, 1, 1, 2) + ",fuse=0",
+        # XCD-major tile order, n fastest
+        _block("up.", 128, 128, 32, 2, 2, 16, 7, 8, 1, 1, 2) + "," +
+        _block("down.", 128, 64, 64, 2, 2, 16, 3, 8, 1, 1, 2) + ",fuse=1",
     ],
     "mlp_odd": [
         _block("up.", 256, 64, 64, 4, 2, 16, 6, 8, 1, 1, 1, 2) + "," +
@@ -243,6 +246,23 @@ SCHEDULES = {
         _block("down.", 64, 128, 64, 2, 2, 16, 7, 8, 1, 1, 0, 2) + ",fuse=1",
         _block("up.", 64, 128, 64, 2, 2, 32, 7, 8, 1, 1, 0) + "," +
         _block("down.", 128, 256, 32, 2, 4, 16, 7, 8, 1, 1, 1, 2) + ",fuse=0",
+        # XCD-major order over the routed tiles (n fastest); partial tiles
+        # skip their empty row blocks on every staging path
+        _block("up.", 256, 128, 32, 2, 4, 16, 7, 8, 1, 1, 2, 2) + "," +
+        _block("down.", 128, 256, 64, 2, 4, 16, 4, 8, 1, 1, 2, 2) + ",fuse=1",
+        _block("up.", 128, 64, 64, 4, 1, 16, 3, 8, 1, 1, 2) + "," +
+        _block("down.", 128, 64, 32, 4, 1, 16, 1, 8, 1, 1, 2) + ",fuse=1",
+        _block("up.", 64, 128, 64, 2, 2, 16, 5, 8, 1, 1, 2) + "," +
+        _block("down.", 64, 128, 64, 4, 1, 16, 2, 8, 1, 1, 2) + ",fuse=0",
+        # partial tiles skipping their empty row blocks, on each staging path
+        _block("up.", 256, 128, 32, 2, 4, 16, 7, 8, 1, 1, 1, 2) + "," +
+        _block("down.", 128, 128, 64, 2, 2, 16, 4, 8, 1, 1, 1) + ",fuse=1,up.skip=1,down.skip=1",
+        _block("up.", 128, 64, 64, 4, 1, 16, 3, 8, 1, 1, 0) + "," +
+        _block("down.", 128, 64, 32, 4, 1, 32, 1, 8, 1, 1, 2) + ",fuse=1,up.skip=1,down.skip=1",
+        _block("up.", 128, 128, 64, 2, 2, 16, 5, 8, 1, 1, 2) + "," +
+        _block("down.", 128, 64, 64, 2, 1, 16, 2, 8, 2, 1, 0) + ",fuse=0,up.skip=1,down.skip=1",
+        _block("up.", 128, 128, 64, 4, 2, 16, 6, 8, 1, 1, 1, 2) + "," +
+        _block("down.", 192, 64, 64, 4, 1, 16, 7, 8, 1, 1, 0) + ",fuse=1,up.skip=1,down.skip=1",
     ],
     "conv": [
         "",
@@ -256,6 +276,7 @@ SCHEDULES = {
         _block("", 64, 64, 64, 2, 2, 16, 7, 8, 1, 1, 1) + ",fuse=1",
         _block("", 64, 64, 32, 2, 1, 32, 7, 8, 1, 1, 0, 2) + ",fuse=0",
         _block("", 128, 64, 64, 2, 2, 16, 7, 8, 1, 1, 1, 2) + ",fuse=1",
+        _block("", 64, 64, 64, 2, 2, 16, 7, 8, 1, 1, 2) + ",fuse=1",
     ],
 }
 
@@ -387,6 +408,9 @@ FULL_ALT = [
     ("moe_t4096_h2048_e64_i1408_top6",
      _block("up.", 256, 128, 32, 4, 2, 16, 7, 8, 1, 1, 1, 2) + "," +
      _block("down.", 128, 128, 64, 2, 2, 16, 7, 8, 1, 1, 1) + ",fuse=1"),
+    ("moe_t4096_h2048_e64_i1408_top6",
+     _block("up.", 256, 128, 32, 2, 4, 16, 7, 8, 1, 1, 2, 2) + "," +
+     _block("down.", 128, 256, 64, 2, 4, 16, 7, 8, 1, 1, 2, 2) + ",fuse=1,up.skip=1,down.skip=1"),
     ("conv3x3_n2_64x64_c320_k320",
      _block("", 64, 160, 64, 2, 2, 16, 7, 8, 1, 1, 1) + ",fuse=1"),
 ]
