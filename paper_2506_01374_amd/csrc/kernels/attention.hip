@@ -18,9 +18,9 @@
 //                softmax (software pipeline); 4: direct global-to-LDS loads
 //                into a ring of three K/V buffers, two tiles in flight
 //                while one is computed, V kept key-major and read with the
-//                transposing LDS load; 5: as 4 with a ring of four and the
-//                scores of the next tile computed ahead of this tile's
-//                softmax (ComputeLocation)
+//                transposing LDS load; 5: as 4 with a ring of four slots
+//                per key split and the scores of the split's next tile
+//                computed ahead of this tile's softmax (ComputeLocation)
 //   VEC          bf16 per global load of K (Vectorize)
 //   UNROLL       unroll factor of the key-tile loop (Unroll)
 //   ORDER        0: query tiles in order; 1: longest (last) query tiles
@@ -62,7 +62,7 @@
 #define NBUF (STAGES > 1 ? 2 : 1)      // register-staged paths
 // direct-to-LDS paths: ring slots per operand (two per split with several
 // splits)
-#define RING (STAGES == 5 ? 4 : SPLITS > 1 ? 2 * SPLITS : 3)
+#define RING (STAGES == 5 ? 4 * SPLITS : SPLITS > 1 ? 2 * SPLITS : 3)
 #define KB (BN / MF)
 #define DB (AD / MF)
 #define NQT ((AS + BM - 1) / BM)
@@ -346,12 +346,10 @@ void rc_attention(AttnArgs args) {
     // LDS byte addresses of the ring buffers and this wave's first 1 KiB
     typedef __attribute__((address_space(3))) bf16_t *lds_p;
     const unsigned wl0 = (unsigned)__builtin_amdgcn_readfirstlane(rg) * WL * 1024u;
-    unsigned KA[RING], VA[RING];
-#pragma unroll
-    for (int i = 0; i < RING; ++i) {
-        KA[i] = (unsigned)(size_t)(lds_p)ring[i] + wl0;
-        VA[i] = (unsigned)(size_t)(lds_p)ring[RING + i] + wl0;
-    }
+    const unsigned ka0 = (unsigned)(size_t)(lds_p)ring[0] + wl0;
+    // K and V slot b (the slots are consecutive KT_ELEMS blocks)
+    auto KA = [&](int b) { return ka0 + (unsigned)b * (KT_ELEMS * 2u); };
+    auto VA = [&](int b) { return ka0 + (unsigned)(RING + b) * (KT_ELEMS * 2u); };
     auto dma = [&](const bf16_t *gbase, unsigned off, unsigned lds_addr) {
         asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
                      :: "v"(off), "s"(gbase), "s"(lds_addr) : "memory", "m0");
@@ -366,21 +364,27 @@ void rc_attention(AttnArgs args) {
 #pragma unroll
             for (int j = 0; j < WL; ++j) {
                 const unsigned back = 2u * AD * (unsigned)max(kv_row[RAGGED_S ? j : 0] - (kvalid - 1), 0);
-                dma(Kg, k_src[j] - back, KA[b] + j * 1024u);
+                dma(Kg, k_src[j] - back, KA(b) + j * 1024u);
             }
 #pragma unroll
             for (int j = 0; j < WL; ++j) {
                 const unsigned back = 2u * AD * (unsigned)max(kv_row[RAGGED_S ? j : 0] - (kvalid - 1), 0);
-                dma(Vg, v_src[j] - back, VA[b] + j * 1024u);
+                dma(Vg, v_src[j] - back, VA(b) + j * 1024u);
             }
             return;
         }
 #pragma unroll
-        for (int j = 0; j < WL; ++j) dma(Kg, k_src[j], KA[b] + j * 1024u);
+        for (int j = 0; j < WL; ++j) dma(Kg, k_src[j], KA(b) + j * 1024u);
 #pragma unroll
-        for (int j = 0; j < WL; ++j) dma(Vg, v_src[j], VA[b] + j * 1024u);
+        for (int j = 0; j < WL; ++j) dma(Vg, v_src[j], VA(b) + j * 1024u);
     };
-#if SPLITS == 1
+#if STAGES == 5
+    // split sp's first three tiles (sp, sp + SPLITS, sp + 2 SPLITS) are in
+    // flight while Q is read, in the split's slots 4 sp .. 4 sp + 2
+#pragma unroll
+    for (int u = 0; u < 3; ++u)
+        if (SPLITS * u + sp < n_kt) gload_lds(SPLITS * u + sp, 4 * sp + u);
+#elif SPLITS == 1
     // the first RING - 1 key tiles are in flight while Q is read
 #pragma unroll
     for (int t = 0; t < RING - 1; ++t)
@@ -759,10 +763,10 @@ void rc_attention(AttnArgs args) {
     }
 #undef WAIT_VM
 #elif STAGES == 5
-    (void)n_it;
     (void)compute;
 #define WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | ((((n) >> 4) & 3) << 14) | (7 << 4) | (15 << 8))
-    // Software pipeline over a ring of four K/V tiles.  Iteration kt runs two
+    // Software pipeline over a ring of four K/V tiles per key split.
+    // Iteration kt (of a split's tiles) runs two
     // phases, each pairing matrix work with vector work that does not depend
     // on it, so the MFMAs execute while the VALU exponentiates:
     //   phase 1: S^T of tile kt + 1 (MFMA)  |  exponentials, row sums and
@@ -775,16 +779,23 @@ void rc_attention(AttnArgs args) {
     // Row sums are kept per lane and reduced across lane groups once, after
     // the loop: every lane of a query applies the same rescale factors.
     //
-    // Tile kt sits in ring slot kt % 4.  Iteration kt reads K of tile kt + 1
-    // and V of tile kt and fills slot (kt + 3) % 4, which held tile kt - 1
-    // (its K was read in iteration kt - 2, its V in kt - 1, both before the
-    // last barrier).
+    // Split sp takes the key tiles sp, sp + SPLITS, ...; its j-th tile
+    // (tile SPLITS j + sp) sits in ring slot 4 sp + j % 4.  Iteration j reads
+    // K of the split's tile j + 1 and V of its tile j and fills slot
+    // 4 sp + (j + 3) % 4, which held its tile j - 1 (whose K was read in
+    // iteration j - 2, its V in j - 1, both before the last barrier).  Every
+    // wave runs n_it iterations, so the barriers line up across splits.
+    auto gt = [&](int j) { return SPLITS * j + sp; };        // tile of the split's j-th
+    auto local_count = [&](int n) { return n > sp ? (n - sp - 1) / SPLITS + 1 : 0; };
+    const int n_loc = local_count(n_kt);
 #if CAUSAL
-    // last key tile (relative) holding a key visible to this wave's rows
-    const int nact = max(0, min(n_kt, (q0w + RPW - 1) / BN - kt0 + 1));
+    // the split's tiles below the last key tile that holds a key visible to
+    // this wave's rows
+    const int nact = local_count(max(0, min(n_kt, (q0w + RPW - 1) / BN - kt0 + 1)));
 #else
-    const int nact = n_kt;
+    const int nact = n_loc;
 #endif
+    bf16_t *const Ks = ring[4 * sp], *const Vs = ring[RING + 4 * sp];   // the split's slot 0
     constexpr int NKS = AD / KSTEP;            // k-steps of the score product
     constexpr int NPJ = BN / KSTEP;            // k-steps of the P V product
     constexpr int MF1 = KB * NKS * QB;         // phase-1 MFMAs
@@ -914,14 +925,15 @@ void rc_attention(AttnArgs args) {
     float mx[QB];
     if (nact > 0) {
         bf16x8 kf[KB][NKS];
-        read_k(K0, kf);
+        read_k(Ks, kf);
         score_mfmas(kf, sc_a);
-        if (needs_mask(0)) mask(0, sc_a);
+        if (needs_mask(gt(0))) mask(gt(0), sc_a);
         tile_max(sc_a, mx);
     }
     // Phase 1 as straight-line code (the scheduling groups act within one
-    // basic block); MASKED applies the causal mask to tile kt + 1's scores.
-    auto phase1 = [&](auto masked, int kt, accT (&cur)[QB][KB], accT (&nxt)[QB][KB], const bf16_t *kn,
+    // basic block); MASKED applies the causal mask to the successor tile's
+    // scores (tile ktn).
+    auto phase1 = [&](auto masked, int ktn, accT (&cur)[QB][KB], accT (&nxt)[QB][KB], const bf16_t *kn,
                       const bf16_t *vc, bf16x8 (&vf)[NPJ][DB], bf16x8 (&pf)[NPJ][QB]) {
         bf16x8 kf[KB][NKS];
         // distinct markers keep the compiler from hoisting the variants'
@@ -941,7 +953,7 @@ void rc_attention(AttnArgs args) {
             __builtin_amdgcn_sched_group_barrier(0x100, DS1_PER, 0);
         }
         if (decltype(masked)::value) {
-            mask(kt + 1, nxt);
+            mask(ktn, nxt);
             // keep the mask inside this variant (not merged into the common
             // block as selects that every tile would execute)
 #pragma unroll
@@ -950,15 +962,15 @@ void rc_attention(AttnArgs args) {
                 for (int kb = 0; kb < KB; ++kb) asm volatile("" : "+v"(nxt[qb][kb]));
         }
     };
-    auto body = [&](int kt, accT (&cur)[QB][KB], accT (&nxt)[QB][KB], const bf16_t *kn,
+    auto body = [&](int j, accT (&cur)[QB][KB], accT (&nxt)[QB][KB], const bf16_t *kn,
                     const bf16_t *vc, int fill) {
-        if (kt + 3 < n_kt) gload_lds(kt + 3, fill);
-        if (kt < nact) {
+        if (j + 3 < n_loc) gload_lds(gt(j + 3), 4 * sp + fill);
+        if (j < nact) {
             rescale(mx);
             bf16x8 vf[NPJ][DB], pf[NPJ][QB];
-            if (kt + 1 < nact) {
-                if (needs_mask(kt + 1)) phase1(IntC<1>{}, kt, cur, nxt, kn, vc, vf, pf);
-                else phase1(IntC<0>{}, kt, cur, nxt, kn, vc, vf, pf);
+            if (j + 1 < nact) {
+                if (needs_mask(gt(j + 1))) phase1(IntC<1>{}, gt(j + 1), cur, nxt, kn, vc, vf, pf);
+                else phase1(IntC<0>{}, gt(j + 1), cur, nxt, kn, vc, vf, pf);
             } else {
                 // the wave's last tile: no successor to overlap with
                 asm volatile("; last tile");
@@ -976,19 +988,20 @@ void rc_attention(AttnArgs args) {
                 __builtin_amdgcn_sched_group_barrier(0x002, 2, 1);
             }
         }
-        if (kt + 3 < n_kt) {
-            WAIT_VM(2 * WL);       // tiles up to kt + 2 have landed; kt + 3 may be in flight
+        if (j + 3 < n_loc) {
+            WAIT_VM(2 * WL);       // tiles up to j + 2 have landed; j + 3 may be in flight
         } else {
             WAIT_VM(0);
         }
         __builtin_amdgcn_s_waitcnt(0xC07F);      // lgkmcnt(0): this wave's LDS reads are done
         asm volatile("s_barrier" ::: "memory");
     };
-    for (int kt = 0; kt < n_kt; kt += 4) {
-        body(kt, sc_a, sc_b, K1, V0, 3);
-        if (kt + 1 < n_kt) body(kt + 1, sc_b, sc_a, K2, V1, 0);
-        if (kt + 2 < n_kt) body(kt + 2, sc_a, sc_b, K3, V2, 1);
-        if (kt + 3 < n_kt) body(kt + 3, sc_b, sc_a, K0, V3, 2);
+    // slot u of the split: K at Ks + u KT_ELEMS, V at Vs + u KT_ELEMS
+    for (int j = 0; j < n_it; j += 4) {
+        body(j, sc_a, sc_b, Ks + KT_ELEMS, Vs, 3);
+        if (j + 1 < n_it) body(j + 1, sc_b, sc_a, Ks + 2 * KT_ELEMS, Vs + KT_ELEMS, 0);
+        if (j + 2 < n_it) body(j + 2, sc_a, sc_b, Ks + 3 * KT_ELEMS, Vs + 2 * KT_ELEMS, 1);
+        if (j + 3 < n_it) body(j + 3, sc_b, sc_a, Ks, Vs + 3 * KT_ELEMS, 2);
     }
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) l[qb] = group_sum(l[qb]);

@@ -433,19 +433,19 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
             if (w * sp > 16) return fmt("waves x splits = %d exceeds 16 waves per workgroup", w * sp);
             if (st >= 4) {
                 // direct-to-LDS ring: whole 1 KiB wave-loads, key-major V read
-                // by the 16x16 transposing load, one key split
+                // by the 16x16 transposing load
                 if (mf != 16) return "direct-to-LDS attention uses the 16x16 MFMA shape";
-                if (st == 5 && sp > 1) return "pipelined direct-to-LDS attention takes one key split";
                 if (kv(d, s, "vec") != 8) return "direct-to-LDS loads move 16-byte vectors (vec 8)";
                 if ((bn * Dh / 512) % w || bn * Dh < 512 * w)
                     return fmt("K/V tile of %d x %lld is not a whole number of 1 KiB wave-loads per wave", bn, (long long)Dh);
                 if (2 * bn * Dh / 512 / w > 62)
                     return fmt("%lld loads per wave per K/V tile exceed the 6-bit vector-memory counter", (long long)(2 * bn * Dh / 512 / w));
             }
-            // K tile + padded V^T tile per stage and split (three plain K/V
-            // tiles for the direct-to-LDS ring)
+            // K tile + padded V^T tile per stage and split (for the
+            // direct-to-LDS ring: three K/V slots, two per split, or four per
+            // split with the pipelined stages 5)
             int64_t vts = bn + (mf == 16 ? 16 : 8);   // padded V^T row
-            int64_t lds = st >= 4 ? (st == 5 ? 4 : sp > 1 ? 2 * sp : 3) * 2 * (int64_t)bn * Dh * 2
+            int64_t lds = st >= 4 ? (st == 5 ? 4 * sp : sp > 1 ? 2 * sp : 3) * 2 * (int64_t)bn * Dh * 2
                                   : (int64_t)sp * (st > 1 ? 2 : 1) * ((int64_t)bn * Dh + Dh * vts) * 2;
             if (lds > LDS_LIMIT) return fmt("LDS %lld B exceeds limit", (long long)lds);
             int64_t mf_acc = (mf == 16) ? 4 : 16;

@@ -149,6 +149,10 @@ SCHEDULES = {
         "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=1,occ=4,splits=4",
         "block_m=32,block_n=32,waves=2,mfma=16,stages=4,vec=8,unroll=2,order=0,occ=2,splits=4",
         "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=2,occ=4,splits=4,chunk=4",
+        # the two-phase pipeline with key splits: four ring slots per split
+        "block_m=64,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=1,order=1,occ=2,splits=2",
+        "block_m=32,block_n=32,waves=2,mfma=16,stages=5,vec=8,unroll=1,order=0,occ=1,splits=2",
+        "block_m=64,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=1,order=2,occ=2,splits=2,chunk=4",
     ],
     "attn_full": [
         "",
@@ -161,6 +165,7 @@ SCHEDULES = {
         "block_m=64,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=1,order=0",
         "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=0,occ=4,splits=2",
         "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=0,occ=4,splits=4",
+        "block_m=64,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=1,order=0,occ=2,splits=2",
     ],
     "attn_d64": [
         "block_m=64,block_n=32,waves=2,mfma=32,stages=2,vec=8,unroll=1,order=0",
@@ -169,6 +174,8 @@ SCHEDULES = {
         "block_m=32,block_n=32,waves=2,mfma=16,stages=5,vec=8,unroll=1,order=0",
         "block_m=32,block_n=32,waves=2,mfma=16,stages=4,vec=8,unroll=1,order=0,splits=2",
         "block_m=32,block_n=32,waves=2,mfma=16,stages=4,vec=8,unroll=1,order=0,splits=4",
+        "block_m=32,block_n=32,waves=2,mfma=16,stages=5,vec=8,unroll=1,order=0,splits=2",
+        "block_m=32,block_n=32,waves=2,mfma=16,stages=5,vec=8,unroll=1,order=2,splits=4",
     ],
     "mlp": [
         "",
@@ -310,6 +317,7 @@ SCHEDULES["attn_causal_512"] = [
     "block_m=32,block_n=32,waves=2,mfma=16,stages=2,vec=8,unroll=1,order=1,chunk=8",
     "block_m=64,block_n=32,waves=2,mfma=32,stages=2,vec=8,unroll=1,order=0,splits=4,chunk=8",
     "block_m=64,block_n=64,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=1,occ=1,splits=2,chunk=4",
+    "block_m=64,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=1,order=2,occ=2,splits=2,chunk=8",
 ]
 SCHEDULES["gemm_skinny"].append(
     "tile_m=16,tile_n=64,tile_k=16,waves_m=1,waves_n=2,vec=4,stages=3,unroll=1,layout=0,splits=32")
@@ -386,6 +394,10 @@ FULL_ALT = [
      "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=2,occ=2,chunk=16"),
     ("attention_causal_b1_h32_s1024_d128",
      "block_m=64,block_n=32,waves=4,mfma=16,stages=4,vec=8,unroll=1,order=1,occ=4,splits=4"),
+    ("attention_causal_b1_h32_s1024_d128",
+     "block_m=64,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=1,order=1,occ=2,splits=2"),
+    ("attention_noncausal_b1_h24_s4096_d128",
+     "block_m=128,block_n=32,waves=4,mfma=16,stages=5,vec=8,unroll=1,order=1,occ=2,splits=2"),
     ("gated_mlp_t2048_h4096_i14336",
      _block("up.", 128, 128, 64, 2, 2, 16, 5, 8, 1, 1, 1) + "," +
      _block("down.", 128, 256, 64, 2, 4, 16, 4, 8, 1, 1, 1) + ",fuse=1"),
