@@ -505,6 +505,12 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
             if ((kv(d, s, "up.stages") == 7 || kv(d, s, "down.stages") == 7) &&
                 std::max(D[0] * Hd, D[0] * topk * I) * 2 >= (1LL << 31))
                 return "activations of 2 GiB or more exceed the ring's 32-bit buffer offsets";
+            // the ping-pong stage has no partial-tile copy of its loop: a skip
+            // there would only duplicate the schedule without it
+            if (kv(d, s, "up.skip") == 1 && kv(d, s, "up.stages") == 6)
+                return "up: the ping-pong stage (6) has no partial-tile loop to skip rows in";
+            if (kv(d, s, "down.skip") == 1 && kv(d, s, "down.stages") == 6)
+                return "down: the ping-pong stage (6) has no partial-tile loop to skip rows in";
             std::string r = check_bf16_block(d, s, UP, -1, I, Hd, 2, "up");
             if (!r.empty()) return r;
             return check_bf16_block(d, s, DOWN, -1, Hd, I, 1, "down");

@@ -269,7 +269,7 @@ SCHEDULES = {
         _block("up.", 128, 128, 64, 2, 2, 16, 5, 8, 1, 1, 2) + "," +
         _block("down.", 128, 64, 64, 2, 1, 16, 2, 8, 2, 1, 0) + ",fuse=0,up.skip=1,down.skip=1",
         _block("up.", 128, 128, 64, 4, 2, 16, 6, 8, 1, 1, 1, 2) + "," +
-        _block("down.", 192, 64, 64, 4, 1, 16, 7, 8, 1, 1, 0) + ",fuse=1,up.skip=1,down.skip=1",
+        _block("down.", 192, 64, 64, 4, 1, 16, 7, 8, 1, 1, 0) + ",fuse=1,up.skip=0,down.skip=1",
     ],
     "conv": [
         "",
