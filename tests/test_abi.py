@@ -3,6 +3,7 @@ the header declares; descriptors, knob tables, legality, transformations,
 parsing and the FLOP / byte model.  No GPU work is done here."""
 import ctypes
 import math
+import json
 import os
 import re
 import subprocess
@@ -111,6 +112,31 @@ def test_validate_rejects_with_reasons():
     s = g.default()
     s.raw.knob[0] = 48                      # not an allowed value
     assert "not an allowed value" in s.validate()
+
+
+def test_moe_row_skip_and_pipelined_attention_splits_legality():
+    # the MoE's partial-tile skip needs a staging path with a partial-tile
+    # copy of its loop (not the ping-pong stage); the tile order knob has a
+    # third value; the pipelined attention stage takes key splits while its
+    # four ring slots per split fit the LDS
+    moe = W.workload_op("moe_t4096_h2048_e64_i1408_top6")
+    tuned = json.load(open(os.path.join(ROOT, "paper_2506_01374_amd", "tuned.json")))
+    base = tuned["moe_t4096_h2048_e64_i1408_top6"]
+    assert moe.from_string(base + ",up.skip=1,down.skip=1,up.grid=2,down.grid=2").validate() == ""
+    names = moe.knob_names()
+    assert "up.skip" in names and "down.skip" in names
+    assert moe.knob_values(names.index("up.grid")) == [0, 1, 2]
+    pp = moe.from_string("up.tile_m=128,up.tile_n=128,up.tile_k=64,up.waves_m=4,up.waves_n=2,up.stages=6,"
+                         "up.vec=8,up.layout=1,up.occ=2,up.skip=1")
+    assert "ping-pong" in pp.validate()
+    assert "ping-pong" not in moe.from_string(str(pp).replace("up.skip=1", "up.skip=0")).validate()
+    mlp = W.workload_op("gated_mlp_t2048_h4096_i14336")
+    assert "up.skip" not in mlp.knob_names()
+    att = W.workload_op("attention_causal_b1_h32_s1024_d128")
+    two = att.schedule(block_m=64, block_n=32, waves=4, mfma=16, stages=5, vec=8, occ=2, order=1, splits=2)
+    assert two.validate() == ""
+    four = att.schedule(block_m=64, block_n=32, waves=4, mfma=16, stages=5, vec=8, occ=1, order=1, splits=4)
+    assert "LDS" in four.validate()
 
 
 def test_apply_enumerate_and_illegal_transform():
