@@ -379,9 +379,14 @@ typedef int32_t (*rc_eval_fn)(void *user, const rc_schedule *s, double *reward);
 
 /* Optional transformation proposer for expansion (Sec. 3.1): writes a
  * proposal text for the node `at` (whose ancestors' schedules are
- * parent/grandparent, NULL at the root).  Proposals are parsed with
- * rc_parse_transform; when none is valid the search samples a random legal
- * transformation instead. */
+ * parent/grandparent, NULL at the root).  The text holds alternatives
+ * separated by ';' or newlines, tried in order; each alternative is one
+ * transformation or a sequence of them joined by '+' (Sec. 3.1 proposes
+ * sequences), parsed step by step with rc_parse_transform: steps that do
+ * not parse are discarded, the others are applied in order (intermediate
+ * schedules need not be legal) and the result becomes the new child if it
+ * is legal and not yet in the tree.  When no alternative yields one, the
+ * search samples a random legal transformation instead (a fallback). */
 typedef int32_t (*rc_propose_fn)(void *user, const rc_schedule *at, const rc_schedule *parent,
                                  const rc_schedule *grandparent, char *buf, size_t len);
 

@@ -7,7 +7,8 @@
 //                 c sqrt(ln N_parent / N_i), unvisited children first, ties to
 //                 the earliest-inserted child;
 //   expansion     a node with fewer than B children (B = branching) gets a new
-//                 child from a proposed transformation; proposals are
+//                 child from a proposed transformation, or a proposed
+//                 sequence of them applied together; proposals are
 //                 validated and, when none is valid, a random legal
 //                 transformation is used (Sec. 3.1); a child whose program
 //                 already exists in the tree is not added, keeping the tree
@@ -162,6 +163,11 @@ int expand(rc_search *s, int at) {
         buf[0] = 0;
         s->propose(s->propose_user, &cur, par, gpar, buf, sizeof buf);
         buf[sizeof buf - 1] = 0;
+        // Alternatives are separated by ';' or newlines and tried in order;
+        // an alternative may chain transformations with '+' (a proposed
+        // sequence, Sec. 3.1): its steps are applied in order, steps that do
+        // not parse are discarded, intermediate schedules need not be legal,
+        // and the resulting schedule must be legal and new to the tree.
         std::string text(buf);
         size_t pos = 0;
         while (pos <= text.size()) {
@@ -169,12 +175,26 @@ int expand(rc_search *s, int at) {
             if (e == std::string::npos) e = text.size();
             std::string item = text.substr(pos, e - pos);
             pos = e + 1;
-            rc_transform t;
-            rc_schedule nx;
-            if (item.empty() || rc_parse_transform(&s->desc, item.c_str(), &t) != RC_OK) continue;
-            if (rc_apply(&s->desc, &cur, &t, &nx) != RC_OK) continue;
+            rc_schedule nx = cur;
+            rc_transform first{-1, 0};
+            size_t q = 0;
+            while (q <= item.size()) {
+                size_t f = item.find('+', q);
+                if (f == std::string::npos) f = item.size();
+                std::string step = item.substr(q, f - q);
+                q = f + 1;
+                rc_transform t;
+                if (step.find_first_not_of(" \t\r") == std::string::npos ||
+                    rc_parse_transform(&s->desc, step.c_str(), &t) != RC_OK)
+                    continue;
+                if (nx.knob[t.knob] == t.value) continue;
+                nx.knob[t.knob] = t.value;
+                if (first.knob < 0) first = t;
+            }
+            if (first.knob < 0) continue;
+            if (!check_schedule(&s->desc, &nx).empty()) continue;
             if (s->in_tree.count(rc_schedule_hash(&nx))) continue;
-            return add_child(s, at, t, nx);
+            return add_child(s, at, first, nx);
         }
         ++s->fallbacks;
     }

@@ -234,10 +234,11 @@ PAPER_AXES = (18, 36, 72, 150, 200)   # sample counts of the paper's best-vs-sam
 
 
 def _policy_args(name: str):
-    """'random', 'uct', 'uct+feedback', 'uct+feedback+surrogate' (B = 4 with
-    the surrogate, as in the replay study), ..."""
+    """'random', 'uct', 'uct+feedback', 'uct+sequence', 'uct+feedback+surrogate'
+    (B = 4 with the surrogate, as in the replay study), ..."""
     parts = name.split("+")
-    return {"policy": parts[0], "proposer": "feedback" if "feedback" in parts else None,
+    proposer = "sequence" if "sequence" in parts else "feedback" if "feedback" in parts else None
+    return {"policy": parts[0], "proposer": proposer,
             "surrogate": "surrogate" in parts, "branching": 4 if "surrogate" in parts else 2}
 
 
@@ -394,14 +395,17 @@ class FeedbackProposer:
     with the language model replaced by a plain rule): take the `top`
     best schedules measured so far, find each knob's most common value among
     them, and propose setting one knob (chosen at random among those where
-    the node disagrees with that consensus) to its consensus value.  Before
-    `warm` valid samples exist, or when the node already agrees everywhere,
-    it proposes nothing and the search expands with a random legal
-    transformation."""
+    the node disagrees with that consensus) to its consensus value.  With
+    `sequence`, the proposal is a sequence of such transformations applied
+    together (Sec. 3.1 proposes sequences): every disagreeing knob set to its
+    consensus value, then a random two or three of them, then each alone, as
+    alternatives tried in that order.  Before `warm` valid samples exist, or
+    when the node already agrees everywhere, it proposes nothing and the
+    search expands with a random legal transformation."""
 
-    def __init__(self, op: rc.Op, seed: int, top: int = 8, warm: int = 8):
+    def __init__(self, op: rc.Op, seed: int, top: int = 8, warm: int = 8, sequence: bool = False):
         import random
-        self.op, self.top, self.warm = op, top, warm
+        self.op, self.top, self.warm, self.sequence = op, top, warm, sequence
         self.rng = random.Random(seed)
         self.names = op.knob_names()
         self.classes = [op.knob_class(i) for i in range(len(self.names))]
@@ -424,7 +428,17 @@ class FeedbackProposer:
             value = max(counts, key=lambda v: (counts[v], -abs(v - cur[name])))
             if value != cur[name]:
                 moves.append(f"{self.classes[i]}({name}={value})")
-        return self.rng.choice(moves) if moves else ""
+        if not moves:
+            return ""
+        if not self.sequence:
+            return self.rng.choice(moves)
+        self.rng.shuffle(moves)
+        alts = []
+        if len(moves) > 1:
+            alts.append(" + ".join(moves))
+        if len(moves) > 3:
+            alts.append(" + ".join(moves[: self.rng.choice((2, 3))]))
+        return "\n".join(alts + moves)
 
 
 CUS, LDS_BYTES = 256, 163840          # MI355X compute units; LDS one workgroup may use
@@ -568,7 +582,7 @@ class SurrogateEvaluator:
 def run_search(op, evaluator, policy: str, budget: int, seed: int, horizon=12, branching=2,
                c=math.sqrt(2.0), proposer: Optional[str] = None, surrogate: bool = False,
                surrogate_features: str = "analytic"):
-    prop = FeedbackProposer(op, seed) if proposer == "feedback" else None
+    prop = FeedbackProposer(op, seed, sequence=proposer == "sequence") if proposer in ("feedback", "sequence") else None
     sur = SurrogateEvaluator(op, evaluator, seed, feature_set=surrogate_features) if surrogate else None
 
     def ev(s):
@@ -646,7 +660,7 @@ def main(argv=None):
                     help="sequence length T (default: 12 per GEMM block of knobs, 24 for the MLP and MoE)")
     ap.add_argument("--branching", type=int, default=2)
     ap.add_argument("--c", type=float, default=math.sqrt(2.0))
-    ap.add_argument("--proposer", default=None, choices=["feedback"],
+    ap.add_argument("--proposer", default=None, choices=["feedback", "sequence"],
                     help="expansion proposals from measured history (default: random legal)")
     ap.add_argument("--surrogate", action="store_true",
                     help="score rollouts with a learned surrogate; measure only promising ones")

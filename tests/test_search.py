@@ -75,6 +75,51 @@ def test_fallback_when_no_proposal_is_valid():
     assert r == 0.5
 
 
+def test_sequence_proposals_apply_their_steps_together():
+    # An alternative chaining transformations with '+' is applied as one
+    # expansion (Sec. 3.1 proposes sequences): unparsable steps are
+    # discarded, intermediate schedules need not be legal, an illegal result
+    # gives way to the next alternative.
+    op = tiny_op()
+    evals = []
+    prop = lambda at, par, gpar: "ComputeLocation(stages=2) + no such step + Layout(layout=1)"
+    s = rc.Search(op, lambda x: evals.append((x["stages"], x["layout"])) or 0.5, policy=rc.RC_POLICY_UCT,
+                  budget=1, horizon=1, branching=2, seed=0, propose=prop)
+    s.step()
+    assert evals == [(2, 1)] and s.fallbacks() == 0
+    g = rc.Op(rc.RC_OP_GEMM_F32, (128, 128, 128))
+    with pytest.raises(rc.RCError, match="multiple of 16"):
+        g.default().apply(g.parse("Parallel(waves_m=2)"))            # alone it is illegal
+    seen = []
+    prop = lambda at, par, gpar: ("Parallel(waves_m=2) + TileSize(tile_m=32)\n"       # illegal result
+                                  "Parallel(waves_m=2) + TileSize(tile_m=32) + TileSize(tile_k=16)")
+    s = rc.Search(g, lambda x: seen.append((x["tile_m"], x["waves_m"], x["tile_k"])) or 0.5,
+                  policy=rc.RC_POLICY_UCT, budget=1, horizon=1, branching=2, seed=0, propose=prop)
+    s.step()
+    assert seen == [(32, 2, 16)] and s.fallbacks() == 0
+
+
+def test_sequence_feedback_proposer_offers_the_consensus_jump_first():
+    from paper_2506_01374_amd.tune import FeedbackProposer, legal_space
+    op = rc.Op(rc.RC_OP_GEMM_F32, (128, 128, 128))
+    space = legal_space(op)
+    prop = FeedbackProposer(op, seed=0, top=4, warm=4, sequence=True)
+    good = [s for s in space if s["tile_m"] == 64 and s["tile_n"] == 64 and s["vec"] == 4][:4]
+    for s in good:
+        prop.record(s, 1.0)
+    at = op.default()
+    lines = prop(at, None, None).split("\n")
+    first = [t.strip() for t in lines[0].split("+")]
+    assert len(first) >= 3 and all(op.parse(t) for t in first)
+    assert any("tile_m=64" in t for t in first) and any("vec=4" in t for t in first)
+    singles = [l for l in lines if "+" not in l]
+    assert set(singles) == set(first)             # then every step alone
+    d = at.as_dict()
+    for t in first:                               # each step moves toward the consensus
+        name, value = t[t.index("(") + 1:-1].split("=")
+        assert d[name] != int(value)
+
+
 def synthetic_reward(s):
     # a smooth, single-peaked function of the knobs of the fp32 GEMM
     d = s.as_dict()
