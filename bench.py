@@ -104,21 +104,24 @@ def _output_bytes(op):
 
 def _search_summary(name, tuned_text):
     """Samples the search needed to reach the tuned schedule, from the
-    committed campaign record of this workload (results/), if any."""
-    path = os.path.join(ROOT, "results", f"{name}.campaign.json")
-    if not os.path.exists(path):
-        return None
-    try:
-        rec = json.load(open(path))
-    except (OSError, ValueError):
-        return None
-    summ = rec.get("summary")
-    if not summ:
-        return None
-    return {"source": os.path.relpath(path, ROOT), "reference_schedule": rec.get("reference_schedule"),
-            "reference_is_tuned": rec.get("reference_schedule") == tuned_text,
-            "measurement": rec.get("measurement"), "budget": rec.get("budget"),
-            "seeds": rec.get("seeds"), "policies": summ}
+    committed campaign records of this workload (results/), if any: one
+    entry per record (the policy comparison, the sequence-proposal
+    comparison, the longer-budget run), each against its own reference."""
+    import glob
+    out = []
+    for path in sorted(glob.glob(os.path.join(ROOT, "results", f"{name}.campaign*.json"))):
+        try:
+            rec = json.load(open(path))
+        except (OSError, ValueError):
+            continue
+        summ = rec.get("summary")
+        if not summ:
+            continue
+        out.append({"source": os.path.relpath(path, ROOT), "reference_schedule": rec.get("reference_schedule"),
+                    "reference_is_tuned": rec.get("reference_schedule") == tuned_text,
+                    "measurement": rec.get("measurement"), "budget": rec.get("budget"),
+                    "seeds": rec.get("seeds"), "policies": summ})
+    return out or None
 
 
 def _kernel_source(name):
