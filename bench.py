@@ -102,7 +102,7 @@ def _output_bytes(op):
     return float(np.prod(shape)) * (4 if dt == "float32" else 2)
 
 
-def _search_summary(name, tuned_text):
+def _search_summary(name, op, sched):
     """Samples the search needed to reach the tuned schedule, from the
     committed campaign records of this workload (results/), if any: one
     entry per record (the policy comparison, the sequence-proposal
@@ -117,8 +117,12 @@ def _search_summary(name, tuned_text):
         summ = rec.get("summary")
         if not summ:
             continue
+        try:       # records name the knobs of their day; unnamed knobs take their defaults
+            same = str(op.from_string(rec.get("reference_schedule") or "")) == str(sched)
+        except Exception:
+            same = False
         out.append({"source": os.path.relpath(path, ROOT), "reference_schedule": rec.get("reference_schedule"),
-                    "reference_is_tuned": rec.get("reference_schedule") == tuned_text,
+                    "reference_is_tuned": same,
                     "measurement": rec.get("measurement"), "budget": rec.get("budget"),
                     "seeds": rec.get("seeds"), "policies": summ})
     return out or None
@@ -130,7 +134,7 @@ def _kernel_source(name):
     return {rc.RC_OP_ATTENTION: "attention.hip", rc.RC_OP_GEMM_F32: "gemm_f32.hip"}.get(kind, "gemm_bf16.hip")
 
 
-def _load_traffic(name, plan_key):
+def _load_traffic(name, op, sched):
     """Counter-measured HBM bytes per launch, only if recorded for this exact
     schedule and this exact kernel source (else null: the kernel changed)."""
     import hashlib
@@ -141,7 +145,12 @@ def _load_traffic(name, plan_key):
         rec = json.load(open(path)).get(name)
     except (OSError, ValueError):
         return None
-    if not rec or rec.get("key") != plan_key:
+    if not rec:
+        return None
+    try:       # the record names the knobs of its day; unnamed knobs take their defaults
+        if str(op.from_string(rec.get("key") or "")) != str(sched):
+            return None
+    except Exception:
         return None
     src = os.path.join(ROOT, "paper_2506_01374_amd", "csrc", "kernels", _kernel_source(name))
     if hashlib.sha1(open(src, "rb").read()).hexdigest()[:16] != rec.get("kernel_source_sha1"):
@@ -282,7 +291,7 @@ def main():
         peak = op.peak_flops() / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                 "frac": achieved / peak}
-    roof["traffic"] = _load_traffic(name, str(sched))
+    roof["traffic"] = _load_traffic(name, op, sched)
     roof["kernel"] = ["rc_attention"] if op.kind == rc.RC_OP_ATTENTION else None
     roof["dominant_kernel_ms"] = dom_ms
     roof["kernel_ms"] = kern_ms
@@ -314,7 +323,7 @@ def main():
                    "input_copies": R, "input_bytes_per_copy": in_bytes,
                    "frac_of_mfma_peak": value * 1e12 / op.peak_flops()},
         "roofline": roof, "cpu_baseline": cpu,
-        "search": _search_summary(name, str(sched)),
+        "search": _search_summary(name, op, sched),
     }
     print(json.dumps(rec), flush=True)
 

@@ -4,6 +4,7 @@
 // Compile-time sizes (generated prologue):
 //   EW_N          elements of an unfused elementwise epilogue
 //   EW_COLS       columns of the bias + SiLU epilogue (bias length)
+//   EW_SPLITS     K-split partial sums added by rc_splitk_sum_bf16
 //   MOE_T MOE_TOPK MOE_E MOE_H   tokens, slots per token, experts, hidden
 //   MOE_TM_UP MOE_TM_DOWN        M tiles of the two expert GEMMs
 
@@ -61,6 +62,28 @@ extern "C" __global__ __launch_bounds__(256) void rc_bias_silu_f32(EwArgs a) {
     p[1] = (unsigned)f2bf(ew_act(g[2] + a.bias[n + 2])) | ((unsigned)f2bf(ew_act(g[3] + a.bias[n + 3])) << 16);
     *(u32x2 *)(a.out + i) = p;
 }
+
+#ifdef EW_SPLITS
+// out[i] = bf16(G[0][i] + ... + G[EW_SPLITS - 1][i]): the fp32 partial sums
+// of a GEMM whose K range was cut over EW_SPLITS workgroups, added in a
+// fixed order; eight elements per thread (EW_N is a multiple of 8).
+extern "C" __global__ __launch_bounds__(256) void rc_splitk_sum_bf16(EwArgs a) {
+    const long i = ((long)blockIdx.x * 256 + threadIdx.x) * 8;
+    if (i >= EW_N) return;
+    f32x4 s0 = *(const f32x4 *)(a.G + i), s1 = *(const f32x4 *)(a.G + i + 4);
+#pragma unroll
+    for (int z = 1; z < EW_SPLITS; ++z) {
+        s0 += *(const f32x4 *)(a.G + (long)z * EW_N + i);
+        s1 += *(const f32x4 *)(a.G + (long)z * EW_N + i + 4);
+    }
+    u32x4 p;
+    p[0] = (unsigned)f2bf(s0[0]) | ((unsigned)f2bf(s0[1]) << 16);
+    p[1] = (unsigned)f2bf(s0[2]) | ((unsigned)f2bf(s0[3]) << 16);
+    p[2] = (unsigned)f2bf(s1[0]) | ((unsigned)f2bf(s1[1]) << 16);
+    p[3] = (unsigned)f2bf(s1[2]) | ((unsigned)f2bf(s1[3]) << 16);
+    *(u32x4 *)(a.out + i) = p;
+}
+#endif
 #endif
 
 #ifdef MOE_T

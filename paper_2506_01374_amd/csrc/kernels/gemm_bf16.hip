@@ -36,6 +36,9 @@
 //                routing filled), so the workgroups sharing an A tile, and
 //                an expert's weights, run on one XCD and its L2
 //   NT_FIRST NT_COUNT  column tiles of this launch (default: all of GN)
+//   SPLITK       dense rows only: the K range is cut into SPLITK equal parts,
+//                one workgroup per (tile, part); part z stores its fp32
+//                partial sums at C + z GM GN (EPI 3) for a separate sum
 //   ROWSKIP      MoE only: 1 - a tile past its expert's last row runs a
 //                second copy of the main loop that skips the fragment reads
 //                and MFMAs of its waves' empty row blocks (ComputeLocation)
@@ -71,7 +74,13 @@
 #define FN (WTN / MF)
 #define CPR (TK / 8)
 #define RPL ((16 / CPR) > 0 ? (16 / CPR) : 1)
-#define KTILES (GK / TK)
+#ifndef SPLITK
+#define SPLITK 1
+#endif
+#if SPLITK > 1 && (AMODE != 0 || EPI != 3 || NB != 1)
+#error "a K split needs dense rows, one weight operand and fp32 partial stores"
+#endif
+#define KTILES (GK / TK / SPLITK)     // K tiles of one workgroup
 #define RAGGED_M ((AMODE == 0 || AMODE == 2) && (GM % TM) != 0)
 // register-staged vectors per thread (the direct-to-LDS stages do not use
 // them; at least 1 keeps their unused arrays well formed)
@@ -206,8 +215,6 @@ void rc_gemm_bf16(GemmBf16Args args) {
     const int nblk = gridDim.x;
 #if GRID == 1
     if ((nblk & 7) == 0) bid = (bid & 7) * (nblk >> 3) + (bid >> 3);
-    const int ntm_grid = nblk / NTN;
-    int mt = bid % ntm_grid, nt = bid / ntm_grid;
 #elif GRID == 2
     // Workgroups reach the 8 XCDs round-robin (workgroup b on XCD b % 8):
     // XCD x takes work items [x * per, (x + 1) * per) of the live ones, in
@@ -223,11 +230,29 @@ void rc_gemm_bf16(GemmBf16Args args) {
         bid = (bid & 7) * per + li;
     }
     if (bid >= live) return;
-    int mt = bid / NTN, nt = bid % NTN;
+#endif
+    // K split: the grid holds SPLITK copies of the tiles, copy z taking K
+    // range z; with the XCD regrouping above, an XCD's workgroups fall in
+    // one copy (one K range of the operands in its L2)
+#if SPLITK > 1
+    const int ntiles = nblk / SPLITK;
+    const int kz = bid / ntiles;
+    bid -= kz * ntiles;
 #else
+    const int ntiles = nblk;
+    constexpr int kz = 0;
+#endif
+#if GRID == 1
+    const int ntm_grid = ntiles / NTN;
+    int mt = bid % ntm_grid, nt = bid / ntm_grid;
+#else
+    (void)ntiles;
     int mt = bid / NTN, nt = bid % NTN;
 #endif
     const int n0 = (NT_FIRST + nt) * TN;
+    // first K column of this workgroup's range; the operand bases below
+    // start there, rows keep their full stride GK
+    const size_t KBASE = (size_t)kz * (GK / SPLITK);
 
 #if AMODE == 1 || AMODE == 3
     // Ragged expert groups: find the expert owning M tile `mt`.
@@ -246,13 +271,15 @@ void rc_gemm_bf16(GemmBf16Args args) {
     const int rows_valid = min(TM, args.offsets[e + 1] - row_base);
     const size_t wstride = (size_t)GK * GN;
     const bf16_t *B0 = args.B0 + (size_t)e * wstride;
+    const bf16_t *const Ab = args.A;
 #if NB == 2
     const bf16_t *B1 = args.B1 + (size_t)e * wstride;
 #endif
 #else
     const int row_base = mt * TM;
     const int rows_valid = RAGGED_M ? min(TM, GM - row_base) : TM;
-    const bf16_t *B0 = args.B0;
+    const bf16_t *const Ab = args.A + KBASE;
+    const bf16_t *B0 = args.B0 + (LAYOUT == 1 ? KBASE : KBASE * GN);
 #if NB == 2
     const bf16_t *B1 = args.B1;
 #endif
@@ -286,12 +313,12 @@ void rc_gemm_bf16(GemmBf16Args args) {
         aval[i] = !RAGGED_M || r < rows_valid;
 #endif
 #if AMODE == 0
-        arow[i] = args.A + (size_t)(aval[i] ? row_base + r : 0) * GK;
+        arow[i] = Ab + (size_t)(aval[i] ? row_base + r : 0) * GK;
 #elif AMODE == 1
         int tok = aval[i] ? args.perm[row_base + r] / TOPK : 0;
-        arow[i] = args.A + (size_t)tok * GK;
+        arow[i] = Ab + (size_t)tok * GK;
 #elif AMODE == 3
-        arow[i] = args.A + (size_t)(aval[i] ? row_base + r : 0) * GK;
+        arow[i] = Ab + (size_t)(aval[i] ? row_base + r : 0) * GK;
 #else
         const int m = row_base + r, c = (v % (TK / VEC)) * VEC;
         const int n = m / (CV_P * CV_Q), p = (m / CV_Q) % CV_P, q = m % CV_Q;
@@ -303,7 +330,7 @@ void rc_gemm_bf16(GemmBf16Args args) {
             if (ih >= 0 && ih < CV_H && iw >= 0 && iw < CV_W) mask |= 1u << tap;
         }
         a_mask[i] = aval[i] ? mask : 0u;      // rows past GM load nothing
-        arow[i] = args.A;
+        arow[i] = Ab;
 #endif
     }
 
@@ -333,7 +360,7 @@ void rc_gemm_bf16(GemmBf16Args args) {
             (void)c;
             const int tap = k0 / CV_C;
             const long long tap_off = ((long long)(tap / CV_S) * CV_W + tap % CV_S) * CV_C + (k0 - tap * CV_C);
-            ra[set][i] = ((a_mask[i] >> tap) & 1u) ? *(const vecT *)(args.A + (a_off[i] + tap_off)) : (vecT)0;
+            ra[set][i] = ((a_mask[i] >> tap) & 1u) ? *(const vecT *)(Ab + (a_off[i] + tap_off)) : (vecT)0;
 #else
             ra[set][i] = aval[i] ? *(const vecT *)(arow[i] + k0 + c) : (vecT)0;
 #endif
@@ -475,13 +502,13 @@ void rc_gemm_bf16(GemmBf16Args args) {
         const int row = c / CPR, lc = (c % CPR) ^ ((row / RPL) % CPR);
 #if AMODE == 0
         // rows past GM read the tile's first row; their products are never stored
-        a_src[j] = args.A + (size_t)(row_base + (RAGGED_M && row >= rows_valid ? 0 : row)) * GK + lc * 8;
+        a_src[j] = Ab + (size_t)(row_base + (RAGGED_M && row >= rows_valid ? 0 : row)) * GK + lc * 8;
 #elif AMODE == 1
         // rows past the group read a valid row; their products are never stored
         const int tok = args.perm[row_base + (row < rows_valid ? row : 0)] / TOPK;
-        a_src[j] = args.A + (size_t)tok * GK + lc * 8;
+        a_src[j] = Ab + (size_t)tok * GK + lc * 8;
 #else
-        a_src[j] = args.A + (size_t)(row_base + (row < rows_valid ? row : 0)) * GK + lc * 8;
+        a_src[j] = Ab + (size_t)(row_base + (row < rows_valid ? row : 0)) * GK + lc * 8;
 #endif
     }
 #pragma unroll
@@ -579,14 +606,14 @@ void rc_gemm_bf16(GemmBf16Args args) {
         return r;
     };
 #if AMODE == 1
-    const i32x4 rsA = rsrc(args.A, (unsigned long long)(GM / TOPK) * GK * 2);
+    const i32x4 rsA = rsrc(Ab, (unsigned long long)(GM / TOPK) * GK * 2);
 #elif AMODE == 2
-    const i32x4 rsA = rsrc(args.A, (unsigned long long)(GM / (CV_P * CV_Q)) * CV_H * CV_W * CV_C * 2);
+    const i32x4 rsA = rsrc(Ab, (unsigned long long)(GM / (CV_P * CV_Q)) * CV_H * CV_W * CV_C * 2);
 #else
-    const i32x4 rsA = rsrc(args.A, (unsigned long long)GM * GK * 2);
+    const i32x4 rsA = rsrc(Ab, ((unsigned long long)GM * GK - KBASE) * 2);
 #endif
     i32x4 rsB[NB];
-    rsB[0] = rsrc(B0, (unsigned long long)GN * GK * 2);
+    rsB[0] = rsrc(B0, ((unsigned long long)GN * GK - KBASE) * 2);
 #if NB == 2
     rsB[1] = rsrc(B1, (unsigned long long)GN * GK * 2);
 #endif
@@ -782,7 +809,7 @@ void rc_gemm_bf16(GemmBf16Args args) {
 #pragma unroll
     for (int x = 0; x < NX; ++x) voff[x] = (unsigned)(r_l * GK * 2 + ((lc0 ^ (4 * x)) << 4));
 #if AMODE != 0 || RAGGED_M
-    // gathered or ragged rows: one offset (from args.A) per load
+    // gathered or ragged rows: one offset (from the A base) per load
     unsigned a_off[A_WL];
 #pragma unroll
     for (int j = 0; j < A_WL; ++j) {
@@ -818,10 +845,10 @@ void rc_gemm_bf16(GemmBf16Args args) {
         for (int j = 0; j < A_WL; ++j) {
             const int W = lw * A_WL + j;
 #if AMODE == 0 && !RAGGED_M
-            const char *base = (const char *)(args.A + ((size_t)row_base + W * (64 / CPR)) * GK + k0);
+            const char *base = (const char *)(Ab + ((size_t)row_base + W * (64 / CPR)) * GK + k0);
             __builtin_amdgcn_global_load_lds((gbl_vp)(base + vo[A_WL % NX == 0 ? j % NX : W % NX]), (lds_vp)(la + W * 512), 16, 0, 0);
 #else
-            const char *base = (const char *)(args.A + k0);
+            const char *base = (const char *)(Ab + k0);
             __builtin_amdgcn_global_load_lds((gbl_vp)(base + ao[j]), (lds_vp)(la + W * 512), 16, 0, 0);
 #endif
         }
@@ -1010,7 +1037,7 @@ void rc_gemm_bf16(GemmBf16Args args) {
 #pragma unroll
                 for (int r = 0; r < 4; ++r) v[r] = acc[0][i][j][g * 4 + r];
 #if EPI == 3
-                *(f32x4 *)((float *)args.C + orow + n) = f32x4{v[0], v[1], v[2], v[3]};
+                *(f32x4 *)((float *)args.C + (size_t)kz * GM * GN + orow + n) = f32x4{v[0], v[1], v[2], v[3]};
 #if NB == 2
                 *(f32x4 *)((float *)args.C1 + orow + n) =
                     f32x4{acc[1][i][j][g * 4 + 0], acc[1][i][j][g * 4 + 1], acc[1][i][j][g * 4 + 2],

@@ -81,12 +81,15 @@ static std::vector<KnobDef> mlp_knobs() {
     // each), so that round is as short as its share of the work
     v.push_back({"up.tail", "Parallel", {0, 1}, 0});
     v.push_back({"down.tail", "Parallel", {0, 1}, 0});
+    // K range of the down projection cut over 1, 2 or 4 workgroups per
+    // output tile (fp32 partial sums, added by a separate kernel)
+    v.push_back({"down.split", "Parallel", {1, 2, 4}, 1});
     return v;
 }
 
 static std::vector<KnobDef> moe_knobs() {
     std::vector<KnobDef> v = mlp_knobs();
-    v.resize(v.size() - 2);     // expert groups are ragged: no tail split
+    v.resize(v.size() - 3);     // expert groups are ragged: no tail or K split
     // 1: an expert's last, partial M tile runs a second copy of the GEMM's
     // main loop that skips the fragment reads and MFMAs of its empty row
     // blocks (full tiles keep the first copy unchanged)
@@ -491,6 +494,15 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
                 h.knob[knob_index(d->kind, nm[0])] = kv(d, s, nm[0]) / 2;
                 std::string why = check_bf16_block(d, &h, nm, T, N, K, nb, tag);
                 if (!why.empty()) return fmt("%s: tail split: the half-height tile is illegal (%s)", tag, why.c_str());
+            }
+            const int sk = kv(d, s, "down.split");
+            if (sk > 1) {
+                const int tk = kv(d, s, "down.tile_k"), un = kv(d, s, "down.unroll");
+                if (kv(d, s, "down.tail") == 1) return "down: the tail split and the K split do not combine";
+                if (I % ((int64_t)sk * tk))
+                    return fmt("down: K = %lld is not a whole number of %d-wide K tiles per split of %d", (long long)I, tk, sk);
+                if ((I / tk / sk) % un)
+                    return fmt("down: unroll %d does not divide the %lld K tiles of a split", un, (long long)(I / tk / sk));
             }
             return "";
         }

@@ -520,16 +520,33 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
                 };
                 p.kerns.push_back(ke);
             }
+            // K split of the down projection: SPLITK copies of the tile grid
+            // store fp32 partial sums, a separate kernel adds them
+            const int sk = std::max(1, kv(d, s, "down.split"));
+            size_t offP = sk > 1 ? ws.add((size_t)sk * T * Hd * 4, "down.partials") : 0;
             Kern k2;
-            k2.src = Source{SRC_gemm_bf16, "rc_gemm_bf16", gemm_defs(dn, 1, 0, 0, T, Hd, I) + cols(0, dn_main)};
-            k2.grid = dim3((unsigned)(((T + dn.tm - 1) / dn.tm) * dn_main), 1, 1);
+            k2.src = Source{SRC_gemm_bf16, "rc_gemm_bf16",
+                            gemm_defs(dn, 1, 0, sk > 1 ? 3 : 0, T, Hd, I) + cols(0, dn_main) +
+                                (sk > 1 ? def("SPLITK", sk) : std::string())};
+            k2.grid = dim3((unsigned)(((T + dn.tm - 1) / dn.tm) * dn_main * sk), 1, 1);
             k2.block = dim3(64 * dn.wm * dn.wn, 1, 1);
             k2.flops = 2.0 * T * I * dn_main * dn.tn;
             k2.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
-                put(b, GemmBf16Args{w + offH, a->in[3], nullptr, a->out[0], nullptr, nullptr,
-                                    nullptr, nullptr, nullptr});
+                put(b, GemmBf16Args{w + offH, a->in[3], nullptr, sk > 1 ? w + offP : a->out[0], nullptr,
+                                    nullptr, nullptr, nullptr, nullptr});
             };
             p.kerns.push_back(k2);
+            if (sk > 1) {
+                Kern kr;
+                kr.src = Source{SRC_aux, "rc_splitk_sum_bf16",
+                                def("EW_N", T * Hd) + def("EW_COLS", Hd) + def("EW_SPLITS", sk)};
+                kr.grid = dim3((unsigned)((T * Hd / 8 + 255) / 256), 1, 1);
+                kr.block = dim3(256, 1, 1);
+                kr.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
+                    put(b, EwArgs{w + offP, nullptr, nullptr, a->out[0]});
+                };
+                p.kerns.push_back(kr);
+            }
             if (dn_tail > 0) {
                 GemmCfg h = dn;
                 h.tm /= 2;

@@ -460,7 +460,9 @@ def _gemm_block_features(d: Dict[str, int], pre: str, M: int, N: int, K: int, nb
     lds = nbuf * stage_bytes
     acc = nb * tm * tn / (64 * waves)
     per_cu = max(1, min(LDS_BYTES // max(lds, 1), max(1, int(512 // max(acc + 64, 1)) * 4 // waves), 32 // waves))
-    n_wg = -(-M // tm) * (N // tn)
+    split = max(1, d.get(pre + "split", 1))      # K range cut over this many workgroups per tile
+    K //= split
+    n_wg = -(-M // tm) * (N // tn) * split
     slots = CUS * per_cu
     rounds = n_wg / slots
     tail = rounds / max(1, -(-n_wg // slots))

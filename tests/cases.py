@@ -212,6 +212,20 @@ SCHEDULES = {
         # XCD-major tile order, n fastest
         _block("up.", 128, 128, 32, 2, 2, 16, 7, 8, 1, 1, 2) + "," +
         _block("down.", 128, 64, 64, 2, 2, 16, 3, 8, 1, 1, 2) + ",fuse=1",
+        # the down projection's K range cut over 2 or 4 workgroups per tile
+        # (every staging path; weights stored N x K and K x N)
+        _block("up.", 128, 128, 32, 2, 2, 16, 7, 8, 1, 1, 1) + "," +
+        _block("down.", 64, 64, 64, 2, 2, 16, 7, 8, 1, 1, 1) + ",fuse=1,down.split=2",
+        _block("up.", 64, 64, 64, 2, 2, 16, 2, 8, 1, 1, 0) + "," +
+        _block("down.", 128, 128, 32, 2, 2, 16, 4, 8, 1, 1, 0) + ",fuse=1,down.split=4",
+        _block("up.", 64, 64, 64, 2, 2, 16, 2, 8, 1, 1, 0) + "," +
+        _block("down.", 64, 128, 64, 2, 2, 32, 3, 8, 2, 1, 2) + ",fuse=0,down.split=2",
+        _block("up.", 64, 64, 64, 2, 2, 16, 2, 8, 1, 1, 0) + "," +
+        _block("down.", 128, 128, 64, 2, 4, 16, 6, 8, 1, 1, 1, 2) + ",fuse=1,down.split=2",
+        _block("up.", 64, 64, 64, 2, 2, 16, 2, 8, 1, 1, 0) + "," +
+        _block("down.", 64, 64, 32, 2, 2, 16, 5, 4, 1, 0, 0) + ",fuse=1,down.split=4",
+        _block("up.", 64, 64, 64, 2, 2, 16, 2, 8, 1, 1, 0) + "," +
+        _block("down.", 32, 64, 64, 1, 2, 16, 1, 8, 2, 0, 2) + ",fuse=1,down.split=2",
     ],
     "mlp_odd": [
         _block("up.", 256, 64, 64, 4, 2, 16, 6, 8, 1, 1, 1, 2) + "," +
@@ -220,6 +234,9 @@ SCHEDULES = {
         _block("down.", 128, 64, 64, 4, 2, 16, 6, 8, 1, 1, 0, 2) + ",fuse=1",
         _block("up.", 128, 64, 64, 2, 2, 16, 7, 8, 1, 1, 1) + "," +
         _block("down.", 64, 64, 32, 2, 2, 16, 7, 8, 1, 1, 0) + ",fuse=1",
+        # K split with an odd number of K tiles per split (320 = 2 x 5 x 32)
+        _block("up.", 128, 64, 64, 2, 2, 16, 7, 8, 1, 1, 1) + "," +
+        _block("down.", 64, 64, 32, 2, 2, 16, 7, 8, 1, 1, 1) + ",fuse=1,down.split=2",
     ],
     "moe": [
         "",
@@ -425,6 +442,13 @@ FULL_ALT = [
      _block("down.", 128, 256, 64, 2, 4, 16, 7, 8, 1, 1, 2, 2) + ",fuse=1,up.skip=1,down.skip=1"),
     ("conv3x3_n2_64x64_c320_k320",
      _block("", 64, 160, 64, 2, 2, 16, 7, 8, 1, 1, 1) + ",fuse=1"),
+    # the down projection on 256 x 256 tiles with its K range cut in two
+    ("gated_mlp_t2048_h4096_i14336",
+     _block("up.", 256, 128, 32, 2, 4, 16, 7, 8, 1, 1, 1) + "," +
+     _block("down.", 256, 256, 32, 2, 4, 16, 7, 8, 1, 1, 1) + ",fuse=1,up.tail=1,down.split=2"),
+    ("gated_mlp_t2048_h4096_i14336",
+     _block("up.", 256, 128, 32, 2, 4, 16, 7, 8, 1, 1, 1) + "," +
+     _block("down.", 128, 256, 64, 2, 4, 16, 4, 8, 1, 1, 2) + ",fuse=1,up.tail=1,down.split=4"),
 ]
 
 

@@ -43,6 +43,7 @@ def test_traffic_records_are_keyed_by_the_tuned_schedules():
     records = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))
     for name, text in tuned.items():
         op = W.workload_op(name)
-        assert records[name]["key"] == str(op.from_string(text)), name
+        # (a knob added later takes its default in an older key)
+        assert str(op.from_string(records[name]["key"])) == str(op.from_string(text)), name
         assert records[name]["bytes_per_launch"] > 0
-        assert bench._load_traffic(name, str(op.default())) is None
+        assert bench._load_traffic(name, op, op.default()) is None
