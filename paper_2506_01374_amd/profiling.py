@@ -48,9 +48,11 @@ def kernel_stats(dirpath: str) -> List[Dict[str, float]]:
 
 
 def dispatch_stats(dirpath: str) -> List[Dict[str, float]]:
-    """Per (kernel name, grid size in threads, workgroup size) duration
-    statistics from the per-dispatch ``*_kernel_trace.csv`` (launches of one
-    kernel with different schedules share a name, not always a grid)."""
+    """Per (kernel name, code object, grid size in threads, workgroup size)
+    duration statistics from the per-dispatch ``*_kernel_trace.csv``
+    (launches of one kernel with different schedules share a name, not
+    always a grid; each schedule is its own code object, with its own kernel
+    id, for the duration of a run)."""
     groups: Dict[tuple, List[float]] = {}
     for path in _find(dirpath, "kernel_trace.csv"):
         with open(path) as f:
@@ -59,10 +61,10 @@ def dispatch_stats(dirpath: str) -> List[Dict[str, float]]:
                 w = int(r.get("Workgroup_Size_X", 0)) * int(r.get("Workgroup_Size_Y", 1)) * \
                     int(r.get("Workgroup_Size_Z", 1))
                 d = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
-                groups.setdefault((r.get("Kernel_Name", ""), g, w), []).append(d)
+                groups.setdefault((r.get("Kernel_Name", ""), r.get("Kernel_Id", ""), g, w), []).append(d)
     out = []
-    for (name, g, w), ds in groups.items():
-        out.append({"name": name, "grid_threads": g, "workgroup": w, "calls": len(ds),
+    for (name, kid, g, w), ds in groups.items():
+        out.append({"name": name, "kernel_id": kid, "grid_threads": g, "workgroup": w, "calls": len(ds),
                     "avg_ns": sum(ds) / len(ds), "min_ns": min(ds), "max_ns": max(ds)})
     return sorted(out, key=lambda r: -r["avg_ns"] * r["calls"])
 
