@@ -4,7 +4,10 @@
 // Compile-time sizes (generated prologue):
 //   EW_N          elements of an unfused elementwise epilogue
 //   EW_COLS       columns of the bias + SiLU epilogue (bias length)
-//   EW_SPLITS     K-split partial sums added by rc_splitk_sum_bf16
+//   EW_SPLITS     K-split partial sums added by rc_splitk_sum_bf16 /
+//                 rc_splitk_swiglu_bf16 (EW_N = rows x EW_COLS each, stored
+//                 compact; the result goes to column EW_C0 + c of an output
+//                 whose rows are EW_LD elements apart)
 //   MOE_T MOE_TOPK MOE_E MOE_H   tokens, slots per token, experts, hidden
 //   MOE_TM_UP MOE_TM_DOWN        M tiles of the two expert GEMMs
 
@@ -64,24 +67,56 @@ extern "C" __global__ __launch_bounds__(256) void rc_bias_silu_f32(EwArgs a) {
 }
 
 #ifdef EW_SPLITS
-// out[i] = bf16(G[0][i] + ... + G[EW_SPLITS - 1][i]): the fp32 partial sums
-// of a GEMM whose K range was cut over EW_SPLITS workgroups, added in a
-// fixed order; eight elements per thread (EW_N is a multiple of 8).
+#ifndef EW_LD
+#define EW_LD EW_COLS
+#endif
+#ifndef EW_C0
+#define EW_C0 0
+#endif
+// Sums of the EW_SPLITS partial arrays at P[i] (8 consecutive elements of one
+// row: EW_COLS is a multiple of 8), added in a fixed order.
+__device__ __forceinline__ void splitk_sum8(const float *P, long i, f32x4 &s0, f32x4 &s1) {
+    s0 = *(const f32x4 *)(P + i);
+    s1 = *(const f32x4 *)(P + i + 4);
+#pragma unroll
+    for (int z = 1; z < EW_SPLITS; ++z) {
+        s0 += *(const f32x4 *)(P + (long)z * EW_N + i);
+        s1 += *(const f32x4 *)(P + (long)z * EW_N + i + 4);
+    }
+}
+__device__ __forceinline__ long splitk_out(long i) {
+    return (i / EW_COLS) * (long)EW_LD + EW_C0 + i % EW_COLS;
+}
+
+// out = bf16(G[0] + ... + G[EW_SPLITS - 1]): a GEMM whose K range was cut
+// over EW_SPLITS workgroups; eight elements per thread.
 extern "C" __global__ __launch_bounds__(256) void rc_splitk_sum_bf16(EwArgs a) {
     const long i = ((long)blockIdx.x * 256 + threadIdx.x) * 8;
     if (i >= EW_N) return;
-    f32x4 s0 = *(const f32x4 *)(a.G + i), s1 = *(const f32x4 *)(a.G + i + 4);
-#pragma unroll
-    for (int z = 1; z < EW_SPLITS; ++z) {
-        s0 += *(const f32x4 *)(a.G + (long)z * EW_N + i);
-        s1 += *(const f32x4 *)(a.G + (long)z * EW_N + i + 4);
-    }
+    f32x4 s0, s1;
+    splitk_sum8(a.G, i, s0, s1);
     u32x4 p;
     p[0] = (unsigned)f2bf(s0[0]) | ((unsigned)f2bf(s0[1]) << 16);
     p[1] = (unsigned)f2bf(s0[2]) | ((unsigned)f2bf(s0[3]) << 16);
     p[2] = (unsigned)f2bf(s1[0]) | ((unsigned)f2bf(s1[1]) << 16);
     p[3] = (unsigned)f2bf(s1[2]) | ((unsigned)f2bf(s1[3]) << 16);
-    *(u32x4 *)(a.out + i) = p;
+    *(u32x4 *)(a.out + splitk_out(i)) = p;
+}
+
+// out = bf16(SiLU(sum of the G partials) * (sum of the U partials)): the
+// gate and up products of a K-split gate/up GEMM; eight elements per thread.
+extern "C" __global__ __launch_bounds__(256) void rc_splitk_swiglu_bf16(EwArgs a) {
+    const long i = ((long)blockIdx.x * 256 + threadIdx.x) * 8;
+    if (i >= EW_N) return;
+    f32x4 g0, g1, u0, u1;
+    splitk_sum8(a.G, i, g0, g1);
+    splitk_sum8(a.U, i, u0, u1);
+    u32x4 p;
+    p[0] = (unsigned)f2bf(silu(g0[0]) * u0[0]) | ((unsigned)f2bf(silu(g0[1]) * u0[1]) << 16);
+    p[1] = (unsigned)f2bf(silu(g0[2]) * u0[2]) | ((unsigned)f2bf(silu(g0[3]) * u0[3]) << 16);
+    p[2] = (unsigned)f2bf(silu(g1[0]) * u1[0]) | ((unsigned)f2bf(silu(g1[1]) * u1[1]) << 16);
+    p[3] = (unsigned)f2bf(silu(g1[2]) * u1[2]) | ((unsigned)f2bf(silu(g1[3]) * u1[3]) << 16);
+    *(u32x4 *)(a.out + splitk_out(i)) = p;
 }
 #endif
 #endif

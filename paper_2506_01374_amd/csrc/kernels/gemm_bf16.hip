@@ -38,7 +38,9 @@
 //   NT_FIRST NT_COUNT  column tiles of this launch (default: all of GN)
 //   SPLITK       dense rows only: the K range is cut into SPLITK equal parts,
 //                one workgroup per (tile, part); part z stores its fp32
-//                partial sums at C + z GM GN (EPI 3) for a separate sum
+//                partial sums (EPI 3; with NB 2 the second operand's to C1)
+//                as a compact [SPLITK][GM][launch columns] array, for a
+//                separate summing kernel
 //   ROWSKIP      MoE only: 1 - a tile past its expert's last row runs a
 //                second copy of the main loop that skips the fragment reads
 //                and MFMAs of its waves' empty row blocks (ComputeLocation)
@@ -77,8 +79,16 @@
 #ifndef SPLITK
 #define SPLITK 1
 #endif
-#if SPLITK > 1 && (AMODE != 0 || EPI != 3 || NB != 1)
-#error "a K split needs dense rows, one weight operand and fp32 partial stores"
+#if SPLITK > 1 && (AMODE != 0 || EPI != 3)
+#error "a K split needs dense rows and fp32 partial stores"
+#endif
+// fp32 stores (EPI 3): row stride and first column of the stored block
+#if SPLITK > 1
+#define OUT_LD (NTN * TN)
+#define OUT_C0 (NT_FIRST * TN)
+#else
+#define OUT_LD GN
+#define OUT_C0 0
 #endif
 #define KTILES (GK / TK / SPLITK)     // K tiles of one workgroup
 #define RAGGED_M ((AMODE == 0 || AMODE == 2) && (GM % TM) != 0)
@@ -281,7 +291,7 @@ void rc_gemm_bf16(GemmBf16Args args) {
     const bf16_t *const Ab = args.A + KBASE;
     const bf16_t *B0 = args.B0 + (LAYOUT == 1 ? KBASE : KBASE * GN);
 #if NB == 2
-    const bf16_t *B1 = args.B1;
+    const bf16_t *B1 = args.B1 + (LAYOUT == 1 ? KBASE : KBASE * GN);
 #endif
 #endif
 
@@ -615,7 +625,7 @@ void rc_gemm_bf16(GemmBf16Args args) {
     i32x4 rsB[NB];
     rsB[0] = rsrc(B0, ((unsigned long long)GN * GK - KBASE) * 2);
 #if NB == 2
-    rsB[1] = rsrc(B1, (unsigned long long)GN * GK * 2);
+    rsB[1] = rsrc(B1, ((unsigned long long)GN * GK - KBASE) * 2);
 #endif
     // per-lane byte offsets of each wave-load at k0 = 0
     unsigned a_off7[A_WL];
@@ -1037,9 +1047,10 @@ void rc_gemm_bf16(GemmBf16Args args) {
 #pragma unroll
                 for (int r = 0; r < 4; ++r) v[r] = acc[0][i][j][g * 4 + r];
 #if EPI == 3
-                *(f32x4 *)((float *)args.C + (size_t)kz * GM * GN + orow + n) = f32x4{v[0], v[1], v[2], v[3]};
+                const size_t po = (size_t)kz * GM * OUT_LD + (size_t)(row_base + mloc) * OUT_LD + (n - OUT_C0);
+                *(f32x4 *)((float *)args.C + po) = f32x4{v[0], v[1], v[2], v[3]};
 #if NB == 2
-                *(f32x4 *)((float *)args.C1 + orow + n) =
+                *(f32x4 *)((float *)args.C1 + po) =
                     f32x4{acc[1][i][j][g * 4 + 0], acc[1][i][j][g * 4 + 1], acc[1][i][j][g * 4 + 2],
                           acc[1][i][j][g * 4 + 3]};
 #endif

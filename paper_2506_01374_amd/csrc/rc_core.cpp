@@ -76,11 +76,13 @@ static std::vector<KnobDef> mlp_knobs() {
     add_gemm_block(v, UP, {16, 32, 64, 128, 256}, {32, 64, 128});
     add_gemm_block(v, DOWN, {16, 32, 64, 128, 256}, {32, 64, 128});
     v.push_back({"fuse", "ComputeLocation", {0, 1}, 0});
-    // 1: the column tiles of a last, partial round of workgroups run as a
-    // second launch with half-height tiles (twice as many, half the work
-    // each), so that round is as short as its share of the work
-    v.push_back({"up.tail", "Parallel", {0, 1}, 0});
-    v.push_back({"down.tail", "Parallel", {0, 1}, 0});
+    // the column tiles of a last, partial round of workgroups run as a
+    // second launch, so that round is as short as its share of the work:
+    // 1 - with half-height tiles (twice as many, half the work each);
+    // 2 - with full tiles whose K range is cut in two (fp32 partial sums,
+    // added, with the epilogue, by a separate kernel)
+    v.push_back({"up.tail", "Parallel", {0, 1, 2}, 0});
+    v.push_back({"down.tail", "Parallel", {0, 1, 2}, 0});
     // K range of the down projection cut over 1, 2 or 4 workgroups per
     // output tile (fp32 partial sums, added by a separate kernel)
     v.push_back({"down.split", "Parallel", {1, 2, 4}, 1});
@@ -481,7 +483,8 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
             for (int b = 0; b < 2; ++b) {
                 const char *const *nm = b == 0 ? UP : DOWN;
                 const char *tag = b == 0 ? "up" : "down";
-                if (kv(d, s, b == 0 ? "up.tail" : "down.tail") != 1) continue;
+                const int tmode = kv(d, s, b == 0 ? "up.tail" : "down.tail");
+                if (tmode == 0) continue;
                 const int64_t N = b == 0 ? I : Hd, K = b == 0 ? Hd : I;
                 const int nb = b == 0 ? 2 : 1;
                 int64_t mc = 0, tc = 0;
@@ -489,6 +492,18 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
                                      kv(d, s, nm[3]) * kv(d, s, nm[4]), kv(d, s, nm[11]), kv(d, s, nm[6]), T, N,
                                      &mc, &tc))
                     return fmt("%s: tail split: no partial round of workgroups to split", tag);
+                if (tmode == 2) {
+                    // full tiles, K range cut in two; the gate/up epilogue
+                    // moves into the summing kernel
+                    const int tk = kv(d, s, nm[2]), un = kv(d, s, nm[8]);
+                    if (b == 0 && kv(d, s, "fuse") != 1)
+                        return "up: a K-split tail needs the fused SwiGLU epilogue (fuse 1)";
+                    if (K % (2LL * tk))
+                        return fmt("%s: K-split tail: K = %lld is not a whole number of %d-wide K tiles per half", tag, (long long)K, tk);
+                    if ((K / tk / 2) % un)
+                        return fmt("%s: K-split tail: unroll %d does not divide the %lld K tiles of a half", tag, un, (long long)(K / tk / 2));
+                    continue;
+                }
                 // the tail launch runs the same schedule with half-height tiles
                 rc_schedule h = *s;
                 h.knob[knob_index(d->kind, nm[0])] = kv(d, s, nm[0]) / 2;
@@ -498,7 +513,7 @@ std::string check_schedule(const rc_op_desc *d, const rc_schedule *s) {
             const int sk = kv(d, s, "down.split");
             if (sk > 1) {
                 const int tk = kv(d, s, "down.tile_k"), un = kv(d, s, "down.unroll");
-                if (kv(d, s, "down.tail") == 1) return "down: the tail split and the K split do not combine";
+                if (kv(d, s, "down.tail") != 0) return "down: the tail split and the K split do not combine";
                 if (I % ((int64_t)sk * tk))
                     return fmt("down: K = %lld is not a whole number of %d-wide K tiles per split of %d", (long long)I, tk, sk);
                 if ((I / tk / sk) % un)

@@ -473,9 +473,10 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
             int fuse = kv(d, s, "fuse");
             // column split of a block over a main and a tail launch
             int64_t up_main = I / up.tn, up_tail = 0, dn_main = Hd / dn.tn, dn_tail = 0;
-            if (kv(d, s, "up.tail") == 1)
+            const int up_tmode = kv(d, s, "up.tail"), dn_tmode = kv(d, s, "down.tail");
+            if (up_tmode >= 1)
                 gemm_tail_split(up.tm, up.tn, up.tk, 2, up.wm * up.wn, up.occ, up.st, T, I, &up_main, &up_tail);
-            if (kv(d, s, "down.tail") == 1)
+            if (dn_tmode >= 1)
                 gemm_tail_split(dn.tm, dn.tn, dn.tk, 1, dn.wm * dn.wn, dn.occ, dn.st, T, Hd, &dn_main, &dn_tail);
             auto cols = [](int64_t first, int64_t count) {
                 return def("NT_FIRST", first) + def("NT_COUNT", count);
@@ -501,7 +502,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
                                         nullptr, nullptr, nullptr});
             };
             p.kerns.push_back(k1);
-            if (up_tail > 0) {
+            if (up_tail > 0 && up_tmode == 1) {
                 GemmCfg h = up;
                 h.tm /= 2;
                 Kern kt = k1;
@@ -509,6 +510,32 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
                 kt.grid = dim3((unsigned)(((T + h.tm - 1) / h.tm) * up_tail), 1, 1);
                 kt.flops = 4.0 * T * Hd * up_tail * up.tn;
                 p.kerns.push_back(kt);
+            }
+            if (up_tail > 0 && up_tmode == 2) {
+                // full tiles, K range cut in two: fp32 gate and up partial
+                // sums of the tail columns, then SiLU(g) * u into the hidden
+                const long wc = up_tail * up.tn;
+                size_t offTG = ws.add((size_t)2 * T * wc * 4, "up.tail.gate"),
+                       offTU = ws.add((size_t)2 * T * wc * 4, "up.tail.up");
+                Kern kt = k1;
+                kt.src.defines = gemm_defs(up, 2, 0, 3, T, I, Hd) + cols(up_main, up_tail) + def("SPLITK", 2);
+                kt.grid = dim3((unsigned)(((T + up.tm - 1) / up.tm) * up_tail * 2), 1, 1);
+                kt.flops = 4.0 * T * Hd * up_tail * up.tn;
+                kt.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
+                    put(b, GemmBf16Args{a->in[0], a->in[1], a->in[2], w + offTG, w + offTU, nullptr,
+                                        nullptr, nullptr, nullptr});
+                };
+                p.kerns.push_back(kt);
+                Kern ks;
+                ks.src = Source{SRC_aux, "rc_splitk_swiglu_bf16",
+                                def("EW_N", T * wc) + def("EW_COLS", wc) + def("EW_LD", I) +
+                                    def("EW_C0", up_main * up.tn) + def("EW_SPLITS", 2)};
+                ks.grid = dim3((unsigned)((T * wc / 8 + 255) / 256), 1, 1);
+                ks.block = dim3(256, 1, 1);
+                ks.bind = [=](const rc_args *, char *w, ArgBlob &b) {
+                    put(b, EwArgs{w + offTG, w + offTU, nullptr, w + offH});
+                };
+                p.kerns.push_back(ks);
             }
             if (!fuse) {
                 Kern ke;
@@ -547,7 +574,7 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
                 };
                 p.kerns.push_back(kr);
             }
-            if (dn_tail > 0) {
+            if (dn_tail > 0 && dn_tmode == 1) {
                 GemmCfg h = dn;
                 h.tm /= 2;
                 Kern kt = k2;
@@ -555,6 +582,29 @@ rc_status describe(const rc_op_desc *d, const rc_schedule *s, rc_plan &p) {
                 kt.grid = dim3((unsigned)(((T + h.tm - 1) / h.tm) * dn_tail), 1, 1);
                 kt.flops = 2.0 * T * I * dn_tail * dn.tn;
                 p.kerns.push_back(kt);
+            }
+            if (dn_tail > 0 && dn_tmode == 2) {
+                const long wc = dn_tail * dn.tn;
+                size_t offTP = ws.add((size_t)2 * T * wc * 4, "down.tail.partials");
+                Kern kt = k2;
+                kt.src.defines = gemm_defs(dn, 1, 0, 3, T, Hd, I) + cols(dn_main, dn_tail) + def("SPLITK", 2);
+                kt.grid = dim3((unsigned)(((T + dn.tm - 1) / dn.tm) * dn_tail * 2), 1, 1);
+                kt.flops = 2.0 * T * I * dn_tail * dn.tn;
+                kt.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
+                    put(b, GemmBf16Args{w + offH, a->in[3], nullptr, w + offTP, nullptr, nullptr,
+                                        nullptr, nullptr, nullptr});
+                };
+                p.kerns.push_back(kt);
+                Kern ks;
+                ks.src = Source{SRC_aux, "rc_splitk_sum_bf16",
+                                def("EW_N", T * wc) + def("EW_COLS", wc) + def("EW_LD", Hd) +
+                                    def("EW_C0", dn_main * dn.tn) + def("EW_SPLITS", 2)};
+                ks.grid = dim3((unsigned)((T * wc / 8 + 255) / 256), 1, 1);
+                ks.block = dim3(256, 1, 1);
+                ks.bind = [=](const rc_args *a, char *w, ArgBlob &b) {
+                    put(b, EwArgs{w + offTP, nullptr, nullptr, a->out[0]});
+                };
+                p.kerns.push_back(ks);
             }
             p.dominant = 0;
             break;

@@ -312,11 +312,23 @@ SCHEDULES["mlp_tail"] = [
     _block("up.", 64, 32, 32, 2, 2, 16, 5, 4, 1, 1, 0) + "," +
     _block("down.", 32, 64, 64, 1, 2, 16, 2, 8, 1, 1, 0) + ",fuse=0,up.tail=1",
 ]
+# the tail columns as full tiles with their K range cut in two (partial
+# sums, then SwiGLU or the plain sum in a separate kernel)
+SCHEDULES["mlp_tail"] += [
+    _block("up.", 64, 32, 64, 2, 2, 16, 2, 8, 1, 1, 1) + "," +
+    _block("down.", 64, 64, 64, 2, 2, 16, 2, 8, 1, 1, 0) + ",fuse=1,up.tail=2",
+    _block("up.", 64, 32, 64, 2, 2, 16, 7, 8, 1, 1, 1) + "," +
+    _block("down.", 64, 64, 64, 2, 2, 16, 3, 8, 1, 1, 0) + ",fuse=1,up.tail=2",
+]
 SCHEDULES["mlp_tail_down"] = [
     _block("up.", 64, 64, 64, 2, 2, 16, 2, 8, 1, 1, 1) + "," +
     _block("down.", 64, 32, 64, 2, 2, 16, 2, 8, 1, 1, 1) + ",fuse=1,down.tail=1",
     _block("up.", 64, 64, 64, 2, 2, 16, 7, 8, 1, 1, 1) + "," +
     _block("down.", 64, 32, 64, 2, 2, 16, 7, 8, 1, 1, 0) + ",fuse=1,down.tail=1",
+    _block("up.", 64, 64, 64, 2, 2, 16, 2, 8, 1, 1, 1) + "," +
+    _block("down.", 64, 32, 64, 2, 2, 16, 2, 8, 1, 1, 1) + ",fuse=1,down.tail=2",
+    _block("up.", 64, 64, 64, 2, 2, 16, 7, 8, 1, 1, 1) + "," +
+    _block("down.", 64, 32, 64, 2, 2, 16, 7, 8, 1, 1, 0) + ",fuse=1,down.tail=2",
 ]
 SCHEDULES["conv_k320"] = [
     _block("", 64, 80, 64, 1, 1, 16, 2, 8, 1, 1, 0) + ",fuse=1",
@@ -449,6 +461,10 @@ FULL_ALT = [
     ("gated_mlp_t2048_h4096_i14336",
      _block("up.", 256, 128, 32, 2, 4, 16, 7, 8, 1, 1, 1) + "," +
      _block("down.", 128, 256, 64, 2, 4, 16, 4, 8, 1, 1, 2) + ",fuse=1,up.tail=1,down.split=4"),
+    # the gate/up tail as full tiles with their K range cut in two
+    ("gated_mlp_t2048_h4096_i14336",
+     _block("up.", 256, 128, 32, 2, 4, 16, 7, 8, 1, 1, 1) + "," +
+     _block("down.", 256, 256, 32, 2, 4, 16, 7, 8, 1, 1, 1) + ",fuse=1,up.tail=2,down.split=2"),
 ]
 
 
