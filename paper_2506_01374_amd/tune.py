@@ -237,7 +237,7 @@ def _policy_args(name: str):
     """'random', 'uct', 'uct+feedback', 'uct+sequence', 'uct+feedback+surrogate'
     (B = 4 with the surrogate, as in the replay study), ..."""
     parts = name.split("+")
-    proposer = "sequence" if "sequence" in parts else "feedback" if "feedback" in parts else None
+    proposer = next((p for p in ("model", "sequence", "feedback") if p in parts), None)
     return {"policy": parts[0], "proposer": proposer,
             "surrogate": "surrogate" in parts, "branching": 4 if "surrogate" in parts else 2}
 
@@ -411,7 +411,7 @@ class FeedbackProposer:
         self.classes = [op.knob_class(i) for i in range(len(self.names))]
         self.seen: List[tuple] = []          # (reward, {knob: value})
 
-    def record(self, sched: rc.Schedule, reward: Optional[float]):
+    def record(self, sched: rc.Schedule, reward: Optional[float], measured: bool = True):
         if reward is not None:
             self.seen.append((reward, sched.as_dict()))
 
@@ -439,6 +439,114 @@ class FeedbackProposer:
         if len(moves) > 3:
             alts.append(" + ".join(moves[: self.rng.choice((2, 3))]))
         return "\n".join(alts + moves)
+
+
+class ModelProposer:
+    """Expansion proposals guided by a learned model of the measured rewards
+    (Sec. 3.1's proposal step, with the language model's judgement of which
+    program to try next replaced by the regression model of Sec. 3.2's
+    f-hat).  A pool of candidates is drawn around the best measured
+    schedules: each of the `top` best, changed in one to four randomly
+    chosen knobs, kept if legal and not measured yet.  The model (the
+    search's surrogate when it has one, else an ensemble of randomised
+    regression trees fitted here on the measurements) scores the pool; each
+    expansion is offered the `offer` best-scoring candidates, best first,
+    each as the sequence of transformations that turns the expanded node
+    into it (the search keeps the first that is legal and not in its tree);
+    a candidate offered first is not offered again.  The pool is redrawn
+    and rescored whenever the model is refitted.  Before `warm`
+    measurements it proposes nothing (random expansion)."""
+
+    def __init__(self, op: rc.Op, seed: int, surrogate=None, top: int = 8, warm: int = 16,
+                 refit: int = 8, per_elite: int = 48, offer: int = 4):
+        import random
+        self.op, self.sur = op, surrogate
+        self.top, self.warm, self.refit, self.per_elite, self.offer = top, warm, refit, per_elite, offer
+        self.rng = random.Random(seed)
+        self.seed = seed
+        self.names = op.knob_names()
+        self.classes = [op.knob_class(i) for i in range(len(self.names))]
+        self.values = [op.knob_values(i) for i in range(len(self.names))]
+        self.measured: Dict[str, float] = {}      # schedule text -> measured reward (0 if invalid)
+        self.X: List[List[float]] = []
+        self.y: List[float] = []
+        self.model = None
+        self.model_at = -1                         # measurements behind the ranked pool
+        self.ranked: List[Dict[str, int]] = []
+        self.used: set = set()                     # candidates already offered first
+
+    def record(self, sched: rc.Schedule, reward: Optional[float], measured: bool = True):
+        if not measured:
+            return
+        text = str(sched)
+        if text in self.measured:
+            return
+        self.measured[text] = reward if reward is not None else 0.0
+        if self.sur is None:
+            self.X.append(schedule_features(self.op, sched))
+            self.y.append(reward if reward is not None else 0.0)
+
+    def _predictor(self):
+        """(model, number of measurements it was fitted on), or (None, 0)."""
+        if self.sur is not None:
+            return self.sur.model, self.sur.fitted_at
+        n = len(self.y)
+        if n >= self.warm and (self.model is None or n - self.model_at >= self.refit):
+            from sklearn.ensemble import ExtraTreesRegressor
+            import numpy as np
+            m = ExtraTreesRegressor(n_estimators=48, min_samples_leaf=2, random_state=self.seed)
+            m.fit(np.array(self.X, dtype=np.float64), np.array(self.y, dtype=np.float64))
+            self.model, self.model_at = m, n
+        return self.model, self.model_at
+
+    def _rank(self, model):
+        import numpy as np
+        elites = sorted(((r, t) for t, r in self.measured.items() if r > 0), reverse=True)[: self.top]
+        pool: Dict[str, rc.Schedule] = {}
+        for _, text in elites:
+            base = self.op.from_string(text).as_dict()
+            for _ in range(self.per_elite):
+                d = dict(base)
+                for _ in range(self.rng.randint(1, 4)):
+                    i = self.rng.randrange(len(self.names))
+                    d[self.names[i]] = self.rng.choice(self.values[i])
+                s = self.op.schedule(**d)
+                t = str(s)
+                if t in pool or t in self.measured or s.validate():
+                    continue
+                pool[t] = s
+        if not pool:
+            self.ranked = []
+            return
+        scheds = list(pool.values())
+        feats = self.sur.features if self.sur is not None else (lambda s: schedule_features(self.op, s))
+        pred = model.predict(np.array([feats(s) for s in scheds], dtype=np.float64))
+        order = sorted(range(len(scheds)), key=lambda k: -pred[k])
+        self.ranked = [scheds[k].as_dict() for k in order]
+
+    def __call__(self, at: rc.Schedule, parent, grandparent) -> str:
+        if len(self.measured) < self.warm:
+            return ""
+        model, fitted = self._predictor()
+        if model is None:
+            return ""
+        if fitted != self.model_at or not self.ranked:
+            self.model_at = fitted
+            self._rank(model)
+        cur = at.as_dict()
+        alts = []
+        for d in self.ranked:
+            text = str(self.op.schedule(**d))
+            if text in self.measured or text in self.used:
+                continue
+            moves = [f"{self.classes[i]}({n}={d[n]})" for i, n in enumerate(self.names) if d[n] != cur[n]]
+            if moves:
+                if not alts:
+                    self.used.add(text)
+                alts.append(" + ".join(moves))
+            if len(alts) == self.offer:
+                break
+        return "\n".join(alts)
 
 
 CUS, LDS_BYTES = 256, 163840          # MI355X compute units; LDS one workgroup may use
@@ -584,17 +692,25 @@ class SurrogateEvaluator:
 def run_search(op, evaluator, policy: str, budget: int, seed: int, horizon=12, branching=2,
                c=math.sqrt(2.0), proposer: Optional[str] = None, surrogate: bool = False,
                surrogate_features: str = "analytic"):
-    prop = FeedbackProposer(op, seed, sequence=proposer == "sequence") if proposer in ("feedback", "sequence") else None
     sur = SurrogateEvaluator(op, evaluator, seed, feature_set=surrogate_features) if surrogate else None
+    if proposer in ("feedback", "sequence"):
+        prop = FeedbackProposer(op, seed, sequence=proposer == "sequence")
+    elif proposer == "model":
+        prop = ModelProposer(op, seed, surrogate=sur)
+    else:
+        prop = None
 
     def ev(s):
         if sur is not None:
+            before = len(sur.y)                  # measurements, valid or not
             reward = sur(s)
+            measured = len(sur.y) != before
         else:
             r = evaluator.measure(s)
             reward = r["reward"] if r.get("valid") else None
+            measured = True
         if prop is not None:
-            prop.record(s, reward)
+            prop.record(s, reward, measured=measured)
         return reward
 
     # with a surrogate only measurements count, so the driver's own budget
@@ -662,7 +778,7 @@ def main(argv=None):
                     help="sequence length T (default: 12 per GEMM block of knobs, 24 for the MLP and MoE)")
     ap.add_argument("--branching", type=int, default=2)
     ap.add_argument("--c", type=float, default=math.sqrt(2.0))
-    ap.add_argument("--proposer", default=None, choices=["feedback", "sequence"],
+    ap.add_argument("--proposer", default=None, choices=["feedback", "sequence", "model"],
                     help="expansion proposals from measured history (default: random legal)")
     ap.add_argument("--surrogate", action="store_true",
                     help="score rollouts with a learned surrogate; measure only promising ones")

@@ -2,6 +2,7 @@
 the report metrics against Table 1."""
 import csv
 import math
+import random
 import os
 
 import pytest
@@ -118,6 +119,45 @@ def test_sequence_feedback_proposer_offers_the_consensus_jump_first():
     for t in first:                               # each step moves toward the consensus
         name, value = t[t.index("(") + 1:-1].split("=")
         assert d[name] != int(value)
+
+
+def test_model_proposer_offers_the_best_predicted_unmeasured_schedules():
+    from paper_2506_01374_amd.tune import ModelProposer, legal_space
+    op = rc.Op(rc.RC_OP_GEMM_F32, (128, 128, 128))
+    space = legal_space(op)
+    prop = ModelProposer(op, seed=0, top=4, warm=16, offer=3)
+    at = op.default()
+    assert prop(at, None, None) == ""             # nothing before the warm-up
+    rng = random.Random(1)
+    for s in rng.sample(space, 60):
+        prop.record(s, synthetic_reward(s))
+    lines = prop(at, None, None).split("\n")
+    assert 1 <= len(lines) <= 3
+    d0 = at.as_dict()
+    targets = []
+    for line in lines:
+        steps = [t.strip() for t in line.split("+")]
+        sched = at.copy()
+        for t in steps:
+            name, value = t[t.index("(") + 1:-1].split("=")
+            assert d0[name] != int(value)         # every step changes the node
+            sched = sched.apply(op.parse(t))
+        assert sched.validate() == "" and str(sched) not in prop.measured
+        targets.append(sched)
+    # the candidates come from around the best measured schedules and are
+    # ranked by the model: the first scores at least the median measured reward
+    import numpy as np
+    from paper_2506_01374_amd.tune import schedule_features
+    pred = prop.model.predict(np.array([schedule_features(op, s) for s in targets]))
+    assert list(pred) == sorted(pred, reverse=True)
+    assert pred[0] >= np.median(prop.y)
+    # the candidate offered first is not offered first again
+    again = prop(at, None, None).split("\n")[0]
+    assert again != lines[0]
+    # measurements behind a surrogate's predictions are not recorded
+    n = len(prop.measured)
+    prop.record(space[0], 0.5, measured=False)
+    assert len(prop.measured) == n
 
 
 def synthetic_reward(s):
