@@ -472,7 +472,7 @@ class ModelProposer:
         self.y: List[float] = []
         self.model = None
         self.model_at = -1                         # measurements behind the ranked pool
-        self.ranked: List[Dict[str, int]] = []
+        self.ranked: List[tuple] = []             # (schedule text, knob values), best predicted first
         self.used: set = set()                     # candidates already offered first
 
     def record(self, sched: rc.Schedule, reward: Optional[float], measured: bool = True):
@@ -522,7 +522,7 @@ class ModelProposer:
         feats = self.sur.features if self.sur is not None else (lambda s: schedule_features(self.op, s))
         pred = model.predict(np.array([feats(s) for s in scheds], dtype=np.float64))
         order = sorted(range(len(scheds)), key=lambda k: -pred[k])
-        self.ranked = [scheds[k].as_dict() for k in order]
+        self.ranked = [(str(scheds[k]), scheds[k].as_dict()) for k in order]
 
     def __call__(self, at: rc.Schedule, parent, grandparent) -> str:
         if len(self.measured) < self.warm:
@@ -535,8 +535,7 @@ class ModelProposer:
             self._rank(model)
         cur = at.as_dict()
         alts = []
-        for d in self.ranked:
-            text = str(self.op.schedule(**d))
+        for text, d in self.ranked:
             if text in self.measured or text in self.used:
                 continue
             moves = [f"{self.classes[i]}({n}={d[n]})" for i, n in enumerate(self.names) if d[n] != cur[n]]
