@@ -121,10 +121,16 @@ def _search_summary(name, op, sched):
             same = str(op.from_string(rec.get("reference_schedule") or "")) == str(sched)
         except Exception:
             same = False
-        out.append({"source": os.path.relpath(path, ROOT), "reference_schedule": rec.get("reference_schedule"),
-                    "reference_is_tuned": same,
-                    "measurement": rec.get("measurement"), "budget": rec.get("budget"),
-                    "seeds": rec.get("seeds"), "policies": summ})
+        pols = {}
+        for name, p in summ.items():       # the record's summary, without per-seed detail
+            curve = p.get("best_so_far_over_reference", {})
+            pols[name] = {"best_so_far_over_reference": {n: round(v["mean"], 4) for n, v in curve.items()},
+                          "best_over_reference": round(p.get("best_over_reference", 0.0), 4)}
+            for key in ("samples_to_50pct", "samples_to_75pct", "samples_to_90pct", "samples_to_99pct"):
+                if key in p:
+                    pols[name][key] = {k: p[key].get(k) for k in ("reached", "of", "median")}
+        out.append({"source": os.path.relpath(path, ROOT), "reference_is_tuned": same,
+                    "budget": rec.get("budget"), "seeds": len(rec.get("seeds") or []), "policies": pols})
     return out or None
 
 
