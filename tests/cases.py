@@ -287,6 +287,10 @@ SCHEDULES = {
         _block("down.", 128, 64, 64, 2, 1, 16, 2, 8, 2, 1, 0) + ",fuse=0,up.skip=1,down.skip=1",
         _block("up.", 128, 128, 64, 4, 2, 16, 6, 8, 1, 1, 1, 2) + "," +
         _block("down.", 192, 64, 64, 4, 1, 16, 7, 8, 1, 1, 0) + ",fuse=1,up.skip=0,down.skip=1",
+        # 256 x 256 down tiles on the ring, XCD-major, partial tiles skipping
+        # their empty row blocks (groups of ~64 rows: mostly empty tiles)
+        _block("up.", 64, 64, 32, 2, 2, 16, 7, 8, 1, 1, 2, 2) + "," +
+        _block("down.", 256, 256, 32, 2, 4, 16, 7, 8, 1, 1, 2) + ",fuse=1,up.skip=1,down.skip=1",
     ],
     "conv": [
         "",
@@ -452,6 +456,11 @@ FULL_ALT = [
     ("moe_t4096_h2048_e64_i1408_top6",
      _block("up.", 256, 128, 32, 2, 4, 16, 7, 8, 1, 1, 2, 2) + "," +
      _block("down.", 128, 256, 64, 2, 4, 16, 7, 8, 1, 1, 2, 2) + ",fuse=1,up.skip=1,down.skip=1"),
+    # both expert GEMMs on the ring in the XCD-major order, 256 x 256 down
+    # tiles whose partial last tile per expert skips its empty row blocks
+    ("moe_t4096_h2048_e64_i1408_top6",
+     _block("up.", 256, 128, 32, 2, 4, 16, 7, 8, 1, 1, 2, 2) + "," +
+     _block("down.", 256, 256, 32, 2, 4, 16, 7, 8, 1, 1, 2) + ",fuse=1,up.skip=1,down.skip=1"),
     ("conv3x3_n2_64x64_c320_k320",
      _block("", 64, 160, 64, 2, 2, 16, 7, 8, 1, 1, 1) + ",fuse=1"),
     # the down projection on 256 x 256 tiles with its K range cut in two
