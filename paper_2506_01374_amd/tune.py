@@ -152,11 +152,11 @@ class ParallelGpuEvaluator:
 
     def __init__(self, op: rc.Op, jobs: int = 8, repeat: int = 10, warmup: int = 2,
                  slow_ms: float = 50.0, cache_dir: Optional[str] = None, log=None,
-                 time_fn=None, compile_fn=None):
+                 time_fn=None, compile_fn=None, flush: bool = True):
         import threading
         from concurrent.futures import ProcessPoolExecutor
         import multiprocessing as mp
-        self.op, self.slow_ms, self.cache_dir = op, slow_ms, cache_dir
+        self.op, self.slow_ms, self.cache_dir, self.flush = op, slow_ms, cache_dir, flush
         # time_fn / compile_fn replace the GPU timing and the worker-process
         # compilation (CPU tests of the bookkeeping)
         self.inner = None if time_fn else GpuEvaluator(op, repeat=repeat, warmup=warmup, log=None)
@@ -178,11 +178,11 @@ class ParallelGpuEvaluator:
             plan = rc.Plan(self.op, sched)
             ws = plan.workspace()
             ins = inner._inputs(sched)
-            t = plan.time(ins, inner.out, ws, warmup=0, repeat=1, flush=True)
+            t = plan.time(ins, inner.out, ws, warmup=0, repeat=1, flush=self.flush)
             if t.median_ms > self.slow_ms:
                 rec.update(coarse=True)
             else:
-                t = plan.time(ins, inner.out, ws, warmup=inner.warmup, repeat=inner.repeat, flush=True)
+                t = plan.time(ins, inner.out, ws, warmup=inner.warmup, repeat=inner.repeat, flush=self.flush)
             rec.update(valid=True, ms=t.median_ms, q1_ms=t.q1_ms, q3_ms=t.q3_ms, tflops=t.tflops,
                        gbps=t.gbps, reward=reward_of(self.op, t.median_ms),
                        kernel_ms=list(t.kernel_ms)[: t.nkernels])
@@ -288,14 +288,16 @@ def default_horizon(op: rc.Op) -> int:
 def run_campaign(op: rc.Op, name: str, policies: List[str], seeds: List[int], budget: int,
                  reference: str, jobs: int, out_path: str, cache_dir: Optional[str],
                  repeat: int = 10, slow_ms: float = 50.0, log=None, time_fn=None, compile_fn=None,
-                 horizon: Optional[int] = None) -> dict:
+                 horizon: Optional[int] = None, flush: bool = True) -> dict:
     """Every (policy, seed) search in its own thread against one shared
     ParallelGpuEvaluator; the reference (tuned) schedule is measured the
-    same way before and after."""
+    same way before and after.  flush=False times warm: back-to-back
+    launches on the same inputs, which a workload that fits the last-level
+    cache then reads from it (no buffer is overwritten between launches)."""
     import threading
     T = horizon if horizon else default_horizon(op)
     ev = ParallelGpuEvaluator(op, jobs=jobs, repeat=repeat, slow_ms=slow_ms, cache_dir=cache_dir, log=log,
-                              time_fn=time_fn, compile_fn=compile_fn)
+                              time_fn=time_fn, compile_fn=compile_fn, flush=flush)
     ref_sched = op.from_string(reference)
     ref0 = ev._time_fn(ref_sched)
     runs: List[dict] = []
@@ -326,8 +328,9 @@ def run_campaign(op: rc.Op, name: str, policies: List[str], seeds: List[int], bu
     ref_reward = max(ref0.get("reward", 0.0), ref1.get("reward", 0.0))
     rec = {"workload": name, "dims": list(op.dims), "flags": op.flags, "budget": budget,
            "seeds": seeds, "policies": policies, "horizon": T,
-           "measurement": (f"cold: a 512 MiB buffer overwritten before each timed launch; median of "
-                           f"{repeat} launches (one launch when it exceeds {slow_ms:g} ms)"),
+           "measurement": ((f"cold: a 512 MiB buffer overwritten before each timed launch; median of "
+                            if flush else "warm: back-to-back launches on the same inputs; median of ")
+                           + f"{repeat} launches (one launch when it exceeds {slow_ms:g} ms)"),
            "reward": "fraction of the binding roofline (bf16 MFMA peak or HBM bandwidth) at the median",
            "reference_schedule": reference,
            "reference_reward": ref_reward, "reference_us": [ref0.get("ms", 0) * 1e3, ref1.get("ms", 0) * 1e3],
@@ -794,9 +797,11 @@ def main(argv=None):
     ap.add_argument("--threads", type=int, default=os.cpu_count() or 8)
     ap.add_argument("--cache-dir", default=os.path.join(HERE, "jit_cache"))
     ap.add_argument("--campaign", default=None, metavar="POLICIES",
-                    help="comma-separated policies (random, uct, uct+feedback, uct+feedback+surrogate) "
-                         "searched concurrently over --seeds with parallel compilation; writes "
-                         "<out>/<workload>.campaign.json")
+                    help="comma-separated policies (random, uct, uct+feedback, uct+sequence, uct+model, "
+                         "each optionally +surrogate) searched concurrently over --seeds with parallel "
+                         "compilation; writes <out>/<workload>.campaign.json")
+    ap.add_argument("--warm", action="store_true",
+                    help="campaign timing without the cache flush (back-to-back launches on the same inputs)")
     ap.add_argument("--jobs", type=int, default=12, help="compile worker processes (--campaign)")
     ap.add_argument("--slow-ms", type=float, default=50.0,
                     help="a schedule slower than this on its first launch is timed once (--campaign)")
@@ -831,7 +836,7 @@ def main(argv=None):
         log = open(os.path.join(args.out, f"{args.workload}.campaign.jsonl"), "a")
         rec = run_campaign(op, args.workload, pols, _parse_seeds(args.seeds), args.budget,
                            tuned[args.workload], args.jobs, path, args.cache_dir, repeat=args.repeat,
-                           slow_ms=args.slow_ms, log=log, horizon=args.horizon)
+                           slow_ms=args.slow_ms, log=log, horizon=args.horizon, flush=not args.warm)
         print(json.dumps({k: rec[k] for k in ("workload", "reference_reward", "distinct_schedules",
                                                "invalid", "wall_s", "errors")}), flush=True)
         for pname, sm in rec["summary"].items():

@@ -522,3 +522,46 @@ def test_campaign_threads_share_measurements_and_summarise(tmp_path):
             k = next((i + 1 for i, v in enumerate(r["curve"]) if v >= 0.9 * saved["reference_reward"]), None)
             assert k == sm["samples_to_90pct"]["per_seed"][sm["seeds"].index(r["seed"])]
             assert all(b >= a for a, b in zip(r["curve"], r["curve"][1:]))
+    assert saved["measurement"].startswith("cold")
+    warm = tune.run_campaign(op, "gemm_f32_128", ["random"], [0], 8, ref, 1, str(tmp_path / "w.json"), None,
+                             time_fn=fake_time, compile_fn=lambda job: 0, flush=False)
+    assert warm["measurement"].startswith("warm")
+
+
+def test_campaign_timing_passes_the_flush_choice_to_the_timer():
+    # the evaluator's own timer asks for the cache flush only in cold mode
+    from paper_2506_01374_amd import tune
+    op = rc.Op(rc.RC_OP_GEMM_F32, (128, 128, 128))
+    seen = []
+
+    class FakePlan:
+        def __init__(self, op, sched):
+            pass
+
+        def workspace(self):
+            return None
+
+        def time(self, ins, out, ws, warmup, repeat, flush):
+            seen.append(flush)
+
+            class T:
+                median_ms, q1_ms, q3_ms, tflops, gbps, nkernels, kernel_ms = 1.0, 1.0, 1.0, 1.0, 1.0, 0, []
+            return T()
+
+    class FakeInner:
+        warmup, repeat, out = 1, 2, None
+
+        def _inputs(self, sched):
+            return []
+
+    for flush in (True, False):
+        ev = tune.ParallelGpuEvaluator(op, time_fn=lambda s: {}, compile_fn=lambda job: 0, flush=flush)
+        ev.inner = FakeInner()
+        orig = tune.rc.Plan
+        tune.rc.Plan = FakePlan
+        try:
+            ev._time(op.default())
+        finally:
+            tune.rc.Plan = orig
+        assert seen and all(f is flush for f in seen)
+        seen.clear()
