@@ -474,7 +474,8 @@ class ModelProposer:
         self.X: List[List[float]] = []
         self.y: List[float] = []
         self.model = None
-        self.model_at = -1                         # measurements behind the ranked pool
+        self.fit_at = -1                           # measurements behind this proposer's own model
+        self.rank_at = -1                          # measurements behind the model that ranked the pool
         self.ranked: List[tuple] = []             # (schedule text, knob values), best predicted first
         self.used: set = set()                     # candidates already offered first
 
@@ -494,13 +495,13 @@ class ModelProposer:
         if self.sur is not None:
             return self.sur.model, self.sur.fitted_at
         n = len(self.y)
-        if n >= self.warm and (self.model is None or n - self.model_at >= self.refit):
+        if n >= self.warm and (self.model is None or n - self.fit_at >= self.refit):
             from sklearn.ensemble import ExtraTreesRegressor
             import numpy as np
             m = ExtraTreesRegressor(n_estimators=48, min_samples_leaf=2, random_state=self.seed)
             m.fit(np.array(self.X, dtype=np.float64), np.array(self.y, dtype=np.float64))
-            self.model, self.model_at = m, n
-        return self.model, self.model_at
+            self.model, self.fit_at = m, n
+        return self.model, self.fit_at
 
     def _rank(self, model):
         import numpy as np
@@ -533,8 +534,8 @@ class ModelProposer:
         model, fitted = self._predictor()
         if model is None:
             return ""
-        if fitted != self.model_at or not self.ranked:
-            self.model_at = fitted
+        if fitted != self.rank_at or not self.ranked:
+            self.rank_at = fitted
             self._rank(model)
         cur = at.as_dict()
         alts = []

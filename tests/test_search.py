@@ -158,6 +158,12 @@ def test_model_proposer_offers_the_best_predicted_unmeasured_schedules():
     n = len(prop.measured)
     prop.record(space[0], 0.5, measured=False)
     assert len(prop.measured) == n
+    # a refit (every 8 new measurements) redraws and reranks the pool
+    first_model = prop.model
+    for s in rng.sample(space, 40):
+        prop.record(s, synthetic_reward(s))
+    prop(at, None, None)
+    assert prop.model is not first_model and prop.rank_at == len(prop.y)
 
 
 def synthetic_reward(s):
