@@ -139,6 +139,49 @@ def test_moe_row_skip_and_pipelined_attention_splits_legality():
     assert "LDS" in four.validate()
 
 
+def test_k_split_and_k_split_tail_legality_and_plans():
+    # the MLP down projection's K split and the K-split tails: whole K tiles
+    # per split, no tail split with a K split, the fused epilogue for a
+    # K-split gate/up tail; the plans add the summing kernels and the
+    # partial-sum workspace
+    mlp = W.workload_op("gated_mlp_t2048_h4096_i14336")
+    tuned = json.load(open(os.path.join(ROOT, "paper_2506_01374_amd", "tuned.json")))
+    base = mlp.from_string(tuned["gated_mlp_t2048_h4096_i14336"]).as_dict()
+    names = mlp.knob_names()
+    assert mlp.knob_values(names.index("down.split")) == [1, 2, 4]
+    assert mlp.knob_values(names.index("up.tail")) == [0, 1, 2]
+    assert "down.split" not in W.workload_op("moe_t4096_h2048_e64_i1408_top6").knob_names()
+
+    def sched(**kw):
+        d = dict(base)
+        d.update(kw)
+        return mlp.schedule(**d)
+
+    assert sched(**{"down.split": 2}).validate() == ""
+    # a down GEMM whose tail split is legal on its own (1024 x 576 x 256)
+    import cases
+    tail_op = cases.small_op("mlp_tail_down")
+    for text in cases.SCHEDULES["mlp_tail_down"][:1]:
+        alone = tail_op.from_string(text)
+        assert alone.validate() == ""
+        for t in (1, 2):
+            both = tail_op.schedule(**{**alone.as_dict(), "down.tail": t, "down.split": 2})
+            assert "do not combine" in both.validate()
+    # 14336 = 448 K tiles of 32: two or four whole halves/quarters; with 128-wide
+    # K tiles 112 of them, 28 per quarter, an unroll of 2 divides them all
+    assert sched(**{"down.split": 4}).validate() == ""
+    odd = W.op_for(rc.RC_OP_GATED_MLP, (256, 256, 320))
+    odd_s = odd.schedule(**{**odd.default().as_dict(), "down.tile_k": 32, "down.split": 4})
+    assert "whole number" in odd_s.validate()          # 320 = 10 K tiles of 32, not 4 x whole
+    assert "fused SwiGLU" in sched(**{"up.tail": 2, "fuse": 0}).validate()
+    assert sched(**{"up.tail": 2}).validate() == ""
+    plan_names = [k["name"] for k in rc.describe(mlp, sched(**{"up.tail": 2}))]
+    assert plan_names == ["rc_gemm_bf16", "rc_gemm_bf16", "rc_splitk_swiglu_bf16", "rc_gemm_bf16",
+                          "rc_splitk_sum_bf16"]
+    grids = [k["grid"] for k in rc.describe(mlp, sched())]
+    assert grids[2] == 2 * (2048 // 256) * (4096 // 256)     # two copies of the 128 down tiles
+
+
 def test_apply_enumerate_and_illegal_transform():
     g = W.workload_op("gemm_f32_128")
     p0 = g.default()
