@@ -82,8 +82,12 @@ typedef enum rc_op_kind {
     RC_OP_GATED_MLP = 3,
     /* (Schedules of the gated MLP have the knobs up.tail / down.tail: with
      * 1, the column tiles of a last, partial round of workgroups run as a
-     * second launch with half-height tiles, so rc_plan_kernels may count
-     * up to two launches per GEMM.) */
+     * second launch with half-height tiles; with 2, as full tiles whose K
+     * range is cut in two, followed by a kernel that adds the two fp32
+     * partial sums (and, for the gate/up GEMM, applies SiLU(g) * u).  The
+     * knob down.split (1, 2, 4) cuts the down projection's K range over
+     * that many workgroups per output tile, followed by a summing kernel.
+     * rc_plan_kernels counts every launch.) */
     /* Routed mixture of gated-MLP experts (the MoE layer of Sec. 4.1):
      *   out[t] = bf16( sum_s w[t][s] * expert_{ids[t][s]}(X[t]) ),
      *   expert_e(x) = bf16( SiLU(x Wg[e]) * (x Wu[e]) ) Wd[e].
@@ -258,7 +262,9 @@ rc_status rc_plan_kernel_flops(const rc_plan *p, int32_t kernel, double *flops);
  *     rows); "expert_out" bf16 [T * topk][Hd] (permuted rows);
  *     "block_counts" int32 [ceil(T * topk / 1024)][E] (routed rows per
  *     block of 1024 consecutive rows and expert);
- *   RC_OP_GATED_MLP: "hidden" bf16 [T][I];
+ *   RC_OP_GATED_MLP: "hidden" bf16 [T][I]; with K splits "down.partials"
+ *     fp32 [down.split][T][Hd], "up.tail.gate" / "up.tail.up" fp32
+ *     [2][T][tail columns], "down.tail.partials" fp32 [2][T][tail columns];
  *   unfused epilogues: "gate.f32", "up.f32" or "pre.f32" (fp32 [rows][cols]);
  *   RC_OP_ATTENTION with chunk > 0: "partials"; RC_OP_GEMM_F32 streaming
  *   stage with splits > 1: "splitk.partials".
