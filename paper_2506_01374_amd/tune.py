@@ -238,6 +238,8 @@ def _policy_args(name: str):
     (B = 4 with the surrogate, as in the replay study), ..."""
     parts = name.split("+")
     proposer = next((p for p in ("model", "sequence", "feedback") if p in parts), None)
+    if proposer == "model" and "repair" in parts:
+        proposer = "model_repair"
     return {"policy": parts[0], "proposer": proposer,
             "surrogate": "surrogate" in parts, "branching": 4 if "surrogate" in parts else 2}
 
@@ -458,12 +460,43 @@ class ModelProposer:
     into it (the search keeps the first that is legal and not in its tree);
     a candidate offered first is not offered again.  The pool is redrawn
     and rescored whenever the model is refitted.  Before `warm`
-    measurements it proposes nothing (random expansion)."""
+    measurements it proposes nothing (random expansion).  With `repair`,
+    an illegal candidate is not dropped: up to `repair` times, the knob
+    that the legality check's reason names is set to the value it asks
+    for, or redrawn (`REPAIR_RULES`), until the candidate is legal, so the
+    pool also holds the coupled multi-knob moves that legality forces (a
+    staging path with the vector width and layout it needs, a tile with a
+    matching wave split, a ring that fits the LDS)."""
+
+    # reason text -> knobs of the block the reason names (its prefix before
+    # ':'), each with the value the reason asks for or None (redraw)
+    REPAIR_RULES = [
+        ("(vec 8)", [("vec", 8)]),
+        ("weights stored N x K", [("layout", 1)]),
+        ("two waves per SIMD (occ 2)", [("occ", 2)]),
+        ("fused SwiGLU", [("fuse", 1)]),
+        ("tail split", [("tail", 0)]),
+        ("do not combine", [("split", 1)]),
+        ("K-split tail", [("tail", 1)]),
+        ("tile_m/waves_m", [("waves_m", None)]),
+        ("tile_n/waves_n", [("waves_n", None)]),
+        ("needs 8 waves", [("waves_m", None), ("waves_n", None)]),
+        ("wave-loads", [("waves_m", None), ("waves_n", None), ("tile_k", None)]),
+        ("ring stages", [("tile_k", None), ("occ", None), ("tile_n", None)]),
+        ("LDS", [("tile_k", None), ("occ", None), ("stages", None)]),
+        ("registers", [("waves_m", None), ("waves_n", None), ("occ", None)]),
+        ("accumulators", [("waves_m", None), ("waves_n", None), ("occ", None)]),
+        ("vector-memory counter", [("tile_k", None), ("waves_m", None)]),
+        ("unroll", [("unroll", 1)]),
+        ("threads x", [("vec", None), ("waves_n", None)]),
+        ("does not divide", [("tile_k", None), ("tile_n", None)]),
+        ("padded im2col", [("stages", None)]),
+    ]
 
     def __init__(self, op: rc.Op, seed: int, surrogate=None, top: int = 8, warm: int = 16,
-                 refit: int = 8, per_elite: int = 48, offer: int = 4):
+                 refit: int = 8, per_elite: int = 48, offer: int = 4, repair: int = 0):
         import random
-        self.op, self.sur = op, surrogate
+        self.op, self.sur, self.repair = op, surrogate, repair
         self.top, self.warm, self.refit, self.per_elite, self.offer = top, warm, refit, per_elite, offer
         self.rng = random.Random(seed)
         self.seed = seed
@@ -503,6 +536,22 @@ class ModelProposer:
             self.model, self.fit_at = m, n
         return self.model, self.fit_at
 
+    def _repair_step(self, d: Dict[str, int], why: str) -> None:
+        """Change the knob(s) the legality reason `why` points at."""
+        block = why.split(":", 1)[0] if ":" in why else ""
+        prefix = block + "." if block in ("up", "down") else ""
+        for key, fixes in self.REPAIR_RULES:
+            if key in why:
+                name, value = fixes[self.rng.randrange(len(fixes))]
+                for full in (prefix + name, name):
+                    if full in d:
+                        i = self.names.index(full)
+                        d[full] = value if value is not None and value in self.values[i] else \
+                            self.rng.choice(self.values[i])
+                        return
+        i = self.rng.randrange(len(self.names))     # no rule: redraw any knob
+        d[self.names[i]] = self.rng.choice(self.values[i])
+
     def _rank(self, model):
         import numpy as np
         elites = sorted(((r, t) for t, r in self.measured.items() if r > 0), reverse=True)[: self.top]
@@ -511,10 +560,18 @@ class ModelProposer:
             base = self.op.from_string(text).as_dict()
             for _ in range(self.per_elite):
                 d = dict(base)
+                changed = set()
                 for _ in range(self.rng.randint(1, 4)):
                     i = self.rng.randrange(len(self.names))
                     d[self.names[i]] = self.rng.choice(self.values[i])
+                    changed.add(i)
                 s = self.op.schedule(**d)
+                for _ in range(self.repair):
+                    why = s.validate()
+                    if not why:
+                        break
+                    self._repair_step(d, why)
+                    s = self.op.schedule(**d)
                 t = str(s)
                 if t in pool or t in self.measured or s.validate():
                     continue
@@ -700,6 +757,8 @@ def run_search(op, evaluator, policy: str, budget: int, seed: int, horizon=12, b
         prop = FeedbackProposer(op, seed, sequence=proposer == "sequence")
     elif proposer == "model":
         prop = ModelProposer(op, seed, surrogate=sur)
+    elif proposer == "model_repair":
+        prop = ModelProposer(op, seed, surrogate=sur, repair=6)
     else:
         prop = None
 
@@ -781,7 +840,7 @@ def main(argv=None):
                     help="sequence length T (default: 12 per GEMM block of knobs, 24 for the MLP and MoE)")
     ap.add_argument("--branching", type=int, default=2)
     ap.add_argument("--c", type=float, default=math.sqrt(2.0))
-    ap.add_argument("--proposer", default=None, choices=["feedback", "sequence", "model"],
+    ap.add_argument("--proposer", default=None, choices=["feedback", "sequence", "model", "model_repair"],
                     help="expansion proposals from measured history (default: random legal)")
     ap.add_argument("--surrogate", action="store_true",
                     help="score rollouts with a learned surrogate; measure only promising ones")

@@ -166,6 +166,28 @@ def test_model_proposer_offers_the_best_predicted_unmeasured_schedules():
     assert prop.model is not first_model and prop.rank_at == len(prop.y)
 
 
+def test_model_proposer_repairs_candidates_by_the_legality_reason():
+    # a candidate put on the direct-to-LDS ring with a narrow vector and
+    # K x N weights is illegal for two stated reasons; the repair sets the
+    # values those reasons ask for and the candidate becomes legal
+    from paper_2506_01374_amd.tune import ModelProposer
+    from paper_2506_01374_amd import workloads as W
+    op = W.workload_op("gated_mlp_t2048_h4096_i14336")
+    d = op.default().as_dict()
+    d.update({"up.tile_m": 128, "up.tile_n": 128, "up.tile_k": 32, "up.waves_m": 2, "up.waves_n": 2,
+              "up.stages": 7, "up.vec": 2, "up.layout": 0})
+    why = op.schedule(**d).validate()
+    assert why.startswith("up:") and ("N x K" in why or "vec 8" in why)
+    prop = ModelProposer(op, seed=0, repair=6)
+    for _ in range(6):
+        why = op.schedule(**d).validate()
+        if not why:
+            break
+        prop._repair_step(d, why)
+    assert op.schedule(**d).validate() == ""
+    assert d["up.vec"] == 8 and d["up.layout"] == 1 and d["up.stages"] == 7
+
+
 def synthetic_reward(s):
     # a smooth, single-peaked function of the knobs of the fp32 GEMM
     d = s.as_dict()
