@@ -238,7 +238,9 @@ def _policy_args(name: str):
     (B = 4 with the surrogate, as in the replay study), ..."""
     parts = name.split("+")
     proposer = next((p for p in ("model", "sequence", "feedback") if p in parts), None)
-    if proposer == "model" and "repair" in parts:
+    if proposer == "model" and "structural" in parts:
+        proposer = "model_structural"
+    elif proposer == "model" and "repair" in parts:
         proposer = "model_repair"
     return {"policy": parts[0], "proposer": proposer,
             "surrogate": "surrogate" in parts, "branching": 4 if "surrogate" in parts else 2}
@@ -466,7 +468,9 @@ class ModelProposer:
     for, or redrawn (`REPAIR_RULES`), until the candidate is legal, so the
     pool also holds the coupled multi-knob moves that legality forces (a
     staging path with the vector width and layout it needs, a tile with a
-    matching wave split, a ring that fits the LDS)."""
+    matching wave split, a ring that fits the LDS).  With `structural`,
+    each elite also yields the `STRUCTURAL` moves of every GEMM block
+    (repaired the same way) besides its random mutations."""
 
     # reason text -> knobs of the block the reason names (its prefix before
     # ':'), each with the value the reason asks for or None (redraw)
@@ -493,10 +497,17 @@ class ModelProposer:
         ("padded im2col", [("stages", None)]),
     ]
 
+    # structural moves tried on every elite with `structural`: staging on the
+    # direct-to-LDS ring, the tail and K splits, the MoE row skip, the tile
+    # orders (each completed by the repair)
+    STRUCTURAL = [({"stages": 7, "vec": 8, "layout": 1},), ({"tail": 1},), ({"tail": 2},),
+                  ({"split": 2},), ({"split": 4},), ({"skip": 1},), ({"grid": 1},), ({"grid": 2},)]
+
     def __init__(self, op: rc.Op, seed: int, surrogate=None, top: int = 8, warm: int = 16,
-                 refit: int = 8, per_elite: int = 48, offer: int = 4, repair: int = 0):
+                 refit: int = 8, per_elite: int = 48, offer: int = 4, repair: int = 0,
+                 structural: bool = False):
         import random
-        self.op, self.sur, self.repair = op, surrogate, repair
+        self.op, self.sur, self.repair, self.structural = op, surrogate, repair, structural
         self.top, self.warm, self.refit, self.per_elite, self.offer = top, warm, refit, per_elite, offer
         self.rng = random.Random(seed)
         self.seed = seed
@@ -556,15 +567,24 @@ class ModelProposer:
         import numpy as np
         elites = sorted(((r, t) for t, r in self.measured.items() if r > 0), reverse=True)[: self.top]
         pool: Dict[str, rc.Schedule] = {}
+        blocks = sorted({n.split(".")[0] + "." for n in self.names if n.startswith(("up.", "down."))}) or [""]
         for _, text in elites:
             base = self.op.from_string(text).as_dict()
-            for _ in range(self.per_elite):
+            moves = []
+            if self.structural:
+                for (move,) in self.STRUCTURAL:
+                    for b in blocks:
+                        m = {b + k: v for k, v in move.items() if b + k in base}
+                        if m and any(base[k] != v for k, v in m.items()):
+                            moves.append(m)
+            for j in range(self.per_elite + len(moves)):
                 d = dict(base)
-                changed = set()
-                for _ in range(self.rng.randint(1, 4)):
-                    i = self.rng.randrange(len(self.names))
-                    d[self.names[i]] = self.rng.choice(self.values[i])
-                    changed.add(i)
+                if j < len(moves):
+                    d.update(moves[j])
+                else:
+                    for _ in range(self.rng.randint(1, 4)):
+                        i = self.rng.randrange(len(self.names))
+                        d[self.names[i]] = self.rng.choice(self.values[i])
                 s = self.op.schedule(**d)
                 for _ in range(self.repair):
                     why = s.validate()
@@ -759,6 +779,8 @@ def run_search(op, evaluator, policy: str, budget: int, seed: int, horizon=12, b
         prop = ModelProposer(op, seed, surrogate=sur)
     elif proposer == "model_repair":
         prop = ModelProposer(op, seed, surrogate=sur, repair=6)
+    elif proposer == "model_structural":
+        prop = ModelProposer(op, seed, surrogate=sur, repair=6, structural=True)
     else:
         prop = None
 
@@ -840,7 +862,7 @@ def main(argv=None):
                     help="sequence length T (default: 12 per GEMM block of knobs, 24 for the MLP and MoE)")
     ap.add_argument("--branching", type=int, default=2)
     ap.add_argument("--c", type=float, default=math.sqrt(2.0))
-    ap.add_argument("--proposer", default=None, choices=["feedback", "sequence", "model", "model_repair"],
+    ap.add_argument("--proposer", default=None, choices=["feedback", "sequence", "model", "model_repair", "model_structural"],
                     help="expansion proposals from measured history (default: random legal)")
     ap.add_argument("--surrogate", action="store_true",
                     help="score rollouts with a learned surrogate; measure only promising ones")

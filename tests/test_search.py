@@ -188,6 +188,31 @@ def test_model_proposer_repairs_candidates_by_the_legality_reason():
     assert d["up.vec"] == 8 and d["up.layout"] == 1 and d["up.stages"] == 7
 
 
+def test_model_proposer_structural_moves_reach_the_ring_from_a_register_staged_elite():
+    from paper_2506_01374_amd.tune import ModelProposer
+    from paper_2506_01374_amd import workloads as W
+    import numpy as np
+
+    class Zero:
+        def predict(self, X):
+            return np.zeros(len(X))
+
+    op = W.workload_op("gated_mlp_t2048_h4096_i14336")
+    d = op.default().as_dict()
+    d.update({"up.tile_m": 128, "up.tile_n": 128, "up.tile_k": 32, "up.waves_m": 2, "up.waves_n": 2,
+              "up.stages": 2, "up.vec": 2, "up.layout": 0})
+    elite = op.schedule(**d)
+    assert elite.validate() == ""
+    for structural, expect in ((False, False), (True, True)):
+        prop = ModelProposer(op, seed=0, repair=6, structural=structural, per_elite=0)
+        prop.measured[str(elite)] = 0.5
+        prop._rank(Zero())
+        ring = [t for t, k in prop.ranked if k["up.stages"] == 7]
+        assert bool(ring) == expect
+        for t, k in prop.ranked:
+            assert op.from_string(t).validate() == ""
+
+
 def synthetic_reward(s):
     # a smooth, single-peaked function of the knobs of the fp32 GEMM
     d = s.as_dict()
