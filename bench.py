@@ -134,6 +134,25 @@ def _search_summary(name, op, sched):
     return out or None
 
 
+def _search_headline(records):
+    """The policy with the best mean best-so-far after 200 samples among the
+    campaign records taken against the present tuned schedule: its mean,
+    and how many runs reached 90 % and 99 % of the tuned schedule (median
+    samples to get there)."""
+    best = None
+    for rec in records or []:
+        if not rec["reference_is_tuned"]:
+            continue
+        for name, p in rec["policies"].items():
+            at = p["best_so_far_over_reference"].get("200")
+            if at is not None and (best is None or at > best["mean_best_over_tuned_at_200"]):
+                best = {"source": rec["source"], "policy": name, "mean_best_over_tuned_at_200": at,
+                        "best_run_over_tuned": p["best_over_reference"],
+                        "samples_to_90pct": p.get("samples_to_90pct"),
+                        "samples_to_99pct": p.get("samples_to_99pct")}
+    return best
+
+
 def _kernel_source(name):
     from paper_2506_01374_amd import rc, workloads as W
     kind = W.workload_op(name).kind
@@ -317,6 +336,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         cpu = _oracle_baseline(name, op, host, args.cpu_budget)
+    search = _search_summary(name, op, sched)
 
     rec = {
         "metric": METRIC, "value": value, "unit": "TFLOP/s", "n_gpus": 1, "steps": K,
@@ -329,7 +349,8 @@ def main():
                    "input_copies": R, "input_bytes_per_copy": in_bytes,
                    "frac_of_mfma_peak": value * 1e12 / op.peak_flops()},
         "roofline": roof, "cpu_baseline": cpu,
-        "search": _search_summary(name, op, sched),
+        "search": search,
+        "search_headline": _search_headline(search),
     }
     print(json.dumps(rec), flush=True)
 
