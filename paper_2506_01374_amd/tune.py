@@ -152,11 +152,15 @@ class ParallelGpuEvaluator:
 
     def __init__(self, op: rc.Op, jobs: int = 8, repeat: int = 10, warmup: int = 2,
                  slow_ms: float = 50.0, cache_dir: Optional[str] = None, log=None,
-                 time_fn=None, compile_fn=None, flush: bool = True):
+                 time_fn=None, compile_fn=None, flush: bool = True, rotate: int = 0):
         import threading
         from concurrent.futures import ProcessPoolExecutor
         import multiprocessing as mp
         self.op, self.slow_ms, self.cache_dir, self.flush = op, slow_ms, cache_dir, flush
+        # rotate > 0: the benchmark's condition - back-to-back steps cycling
+        # through `rotate` copies of the inputs, no flush
+        self.rotate = rotate
+        self._copies: Dict[str, list] = {}
         # time_fn / compile_fn replace the GPU timing and the worker-process
         # compilation (CPU tests of the bookkeeping)
         self.inner = None if time_fn else GpuEvaluator(op, repeat=repeat, warmup=warmup, log=None)
@@ -171,9 +175,51 @@ class ParallelGpuEvaluator:
         self.log = log
         self.order: List[str] = []     # distinct schedules in measurement order
 
+    def _rotated(self, sched: rc.Schedule):
+        """`rotate` device copies of the schedule's stored inputs."""
+        inner = self.inner
+        key = ",".join(f"{k}={v}" for k, v in sched.as_dict().items() if k.endswith("layout"))
+        if key not in self._copies:
+            first = inner._inputs(sched)
+            self._copies[key] = [first] + [[t.clone() for t in first] for _ in range(self.rotate - 1)]
+        return self._copies[key]
+
+    def _time_rotated(self, plan, sched, ws, steps: int, warm: bool = True) -> float:
+        """Milliseconds per step over `steps` back-to-back launches that cycle
+        through the input copies (HIP events around the launches), after one
+        warm-up pass over the copies when `warm`."""
+        torch = self.inner.torch
+        copies = self._rotated(sched)
+        preps = [plan.prepare(c, self.inner.out, ws) for c in copies]
+        for i in range(len(preps) if warm else 0):
+            preps[i].launch()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for i in range(steps):
+            preps[i % len(preps)].launch()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
     def _time(self, sched: rc.Schedule) -> dict:
         inner = self.inner
         rec = {"schedule": str(sched)}
+        if self.rotate > 0:
+            try:
+                plan = rc.Plan(self.op, sched)
+                ws = plan.workspace()
+                ms = self._time_rotated(plan, sched, ws, 1, warm=False)
+                if ms > self.slow_ms:
+                    rec.update(coarse=True)
+                else:
+                    ms = self._time_rotated(plan, sched, ws, max(inner.repeat, int(20.0 / max(ms, 1e-3))))
+                rec.update(valid=True, ms=ms, q1_ms=ms, q3_ms=ms, tflops=self.op.flops() / ms / 1e9,
+                           gbps=self.op.bytes() / ms / 1e6, reward=reward_of(self.op, ms))
+                del plan, ws
+            except rc.RCError as e:
+                rec.update(valid=False, error=str(e)[:300])
+            return rec
         try:
             plan = rc.Plan(self.op, sched)
             ws = plan.workspace()
@@ -292,16 +338,18 @@ def default_horizon(op: rc.Op) -> int:
 def run_campaign(op: rc.Op, name: str, policies: List[str], seeds: List[int], budget: int,
                  reference: str, jobs: int, out_path: str, cache_dir: Optional[str],
                  repeat: int = 10, slow_ms: float = 50.0, log=None, time_fn=None, compile_fn=None,
-                 horizon: Optional[int] = None, flush: bool = True) -> dict:
+                 horizon: Optional[int] = None, flush: bool = True, rotate: int = 0) -> dict:
     """Every (policy, seed) search in its own thread against one shared
     ParallelGpuEvaluator; the reference (tuned) schedule is measured the
     same way before and after.  flush=False times warm: back-to-back
     launches on the same inputs, which a workload that fits the last-level
-    cache then reads from it (no buffer is overwritten between launches)."""
+    cache then reads from it (no buffer is overwritten between launches).
+    rotate > 0 times the benchmark's way: back-to-back steps cycling through
+    that many copies of the inputs."""
     import threading
     T = horizon if horizon else default_horizon(op)
     ev = ParallelGpuEvaluator(op, jobs=jobs, repeat=repeat, slow_ms=slow_ms, cache_dir=cache_dir, log=log,
-                              time_fn=time_fn, compile_fn=compile_fn, flush=flush)
+                              time_fn=time_fn, compile_fn=compile_fn, flush=flush, rotate=rotate)
     ref_sched = op.from_string(reference)
     ref0 = ev._time_fn(ref_sched)
     runs: List[dict] = []
@@ -332,7 +380,9 @@ def run_campaign(op: rc.Op, name: str, policies: List[str], seeds: List[int], bu
     ref_reward = max(ref0.get("reward", 0.0), ref1.get("reward", 0.0))
     rec = {"workload": name, "dims": list(op.dims), "flags": op.flags, "budget": budget,
            "seeds": seeds, "policies": policies, "horizon": T,
-           "measurement": ((f"cold: a 512 MiB buffer overwritten before each timed launch; median of "
+           "measurement": (f"benchmark: back-to-back steps cycling through {rotate} input copies, "
+                           f"mean over at least {repeat} steps and 20 ms" if rotate > 0 else
+                           (f"cold: a 512 MiB buffer overwritten before each timed launch; median of "
                             if flush else "warm: back-to-back launches on the same inputs; median of ")
                            + f"{repeat} launches (one launch when it exceeds {slow_ms:g} ms)"),
            "reward": "fraction of the binding roofline (bf16 MFMA peak or HBM bandwidth) at the median",
@@ -882,6 +932,8 @@ def main(argv=None):
                     help="comma-separated policies (random, uct, uct+feedback, uct+sequence, uct+model, "
                          "each optionally +surrogate) searched concurrently over --seeds with parallel "
                          "compilation; writes <out>/<workload>.campaign.json")
+    ap.add_argument("--bench-timing", type=int, default=0, metavar="R",
+                    help="campaign timing as the benchmark's: back-to-back steps through R input copies")
     ap.add_argument("--warm", action="store_true",
                     help="campaign timing without the cache flush (back-to-back launches on the same inputs)")
     ap.add_argument("--jobs", type=int, default=12, help="compile worker processes (--campaign)")
@@ -918,7 +970,8 @@ def main(argv=None):
         log = open(os.path.join(args.out, f"{args.workload}.campaign.jsonl"), "a")
         rec = run_campaign(op, args.workload, pols, _parse_seeds(args.seeds), args.budget,
                            tuned[args.workload], args.jobs, path, args.cache_dir, repeat=args.repeat,
-                           slow_ms=args.slow_ms, log=log, horizon=args.horizon, flush=not args.warm)
+                           slow_ms=args.slow_ms, log=log, horizon=args.horizon, flush=not args.warm,
+                           rotate=args.bench_timing)
         print(json.dumps({k: rec[k] for k in ("workload", "reference_reward", "distinct_schedules",
                                                "invalid", "wall_s", "errors")}), flush=True)
         for pname, sm in rec["summary"].items():

@@ -581,6 +581,75 @@ def test_campaign_threads_share_measurements_and_summarise(tmp_path):
     assert warm["measurement"].startswith("warm")
 
 
+def test_campaign_benchmark_timing_cycles_the_input_copies():
+    # rotate > 0: steps launched back to back through that many input
+    # copies, no flush; the record says so
+    from paper_2506_01374_amd import tune
+    op = rc.Op(rc.RC_OP_GEMM_F32, (128, 128, 128))
+    launched = []
+
+    class FakeEvent:
+        def __init__(self, enable_timing=True):
+            pass
+
+        def record(self):
+            pass
+
+        def elapsed_time(self, other):
+            return 2.0 * max(1, len(launched))
+
+    class FakeTorch:
+        class cuda:
+            Event = FakeEvent
+
+            @staticmethod
+            def synchronize():
+                pass
+
+    class FakePrepared:
+        def __init__(self, copy):
+            self.copy = copy
+
+        def launch(self):
+            launched.append(self.copy)
+
+    class FakePlan:
+        def __init__(self, op, sched):
+            pass
+
+        def workspace(self):
+            return None
+
+        def prepare(self, inputs, out, ws):
+            return FakePrepared(inputs[0])
+
+    class FakeTensor:
+        def __init__(self, tag):
+            self.tag = tag
+
+        def clone(self):
+            return FakeTensor(self.tag + "'")
+
+    class FakeInner:
+        warmup, repeat, out, torch = 1, 4, None, FakeTorch
+
+        def _inputs(self, sched):
+            return [FakeTensor("a")]
+
+    ev = tune.ParallelGpuEvaluator(op, time_fn=lambda s: {}, compile_fn=lambda job: 0, rotate=2)
+    ev.inner = FakeInner()
+    orig = tune.rc.Plan
+    tune.rc.Plan = FakePlan
+    try:
+        rec = ev._time(op.default())
+    finally:
+        tune.rc.Plan = orig
+    assert rec["valid"] and rec["ms"] > 0
+    tags = [t.tag for t in launched]
+    assert set(tags) == {"a", "a'"}                  # both copies were used
+    assert all(x != y for x, y in zip(tags[1:], tags[2:]))   # alternating within a timed run
+
+
 def test_campaign_timing_passes_the_flush_choice_to_the_timer():
     # the evaluator's own timer asks for the cache flush only in cold mode
     from paper_2506_01374_amd import tune
