@@ -6,6 +6,9 @@ seeded random legal transformation sequences of length 12 from P0 (the
 rollouts of Sec. 3.2), 40 per operator at the small shapes, whole outputs
 compared; and the best schedule of a short seeded UCT search per operator,
 measured on the GPU with the timing call, then compared with the oracle.
+The campaign evaluator's timing conditions (cold, warm, back-to-back
+through input copies) are run on a real plan per operator, and the output
+they leave is compared with the oracle too.
 """
 import os
 
@@ -75,3 +78,27 @@ def test_short_uct_search_best_matches_oracle(key):
         plan.time(dev, out, ws, warmup=1, repeat=2, flush=True)
         torch.cuda.synchronize()
         assert_parity(op, W.output_to_f64(op, out), host, label=f"{key} searched {text}")
+
+
+@pytest.mark.parametrize("key", cases.WALK_KEYS)
+@pytest.mark.parametrize("mode", ["cold", "warm", "rotated"])
+def test_campaign_timing_modes_time_a_real_plan_and_leave_its_output(key, mode):
+    """The campaign evaluator's three timing conditions (cache flushed before
+    each launch, warm, back-to-back steps through three input copies) time
+    a real plan, and the output buffer then holds the oracle's result."""
+    from paper_2506_01374_amd import tune
+    op = cases.small_op(key)
+    sched = op.default()
+    print(f"[gpu] campaign timing {mode} kind={op.kind} dims={op.dims} sched={sched}", flush=True)
+    # compile_fn: no worker pool; the plan compiles in this process
+    ev = tune.ParallelGpuEvaluator(op, repeat=3, warmup=1, compile_fn=lambda job: 0,
+                                   flush=(mode == "cold"), rotate=(3 if mode == "rotated" else 0))
+    try:
+        rec = ev.measure(sched)
+    finally:
+        ev.close()
+    assert rec["valid"] and rec["ms"] > 0 and rec["reward"] > 0, rec
+    if mode == "rotated":
+        assert len(ev._copies) == 1 and len(next(iter(ev._copies.values()))) == 3
+    torch.cuda.synchronize()
+    assert_parity(op, W.output_to_f64(op, ev.inner.out), ev.inner.host, label=f"{key} {mode} timing")
