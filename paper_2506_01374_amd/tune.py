@@ -276,6 +276,33 @@ class ParallelGpuEvaluator:
             self.pool.shutdown()
 
 
+def time_p0_and_tuned(op: rc.Op, name: str, tuned_text: str, repeat: int = 10, rounds: int = 2) -> dict:
+    """Cold times of the untransformed program P0 and of the tuned schedule
+    (cache flushed before each launch, median of `repeat` launches),
+    alternating `rounds` times in one process, and the tuned schedule's
+    speedup over P0: the factor that turns a search's best / tuned into its
+    best speedup over the untransformed program, the quantity of the
+    paper's best-speedup-against-samples table (Sec. 4.2, Table 3)."""
+    import statistics
+    ev = GpuEvaluator(op, repeat=repeat, warmup=1)
+    pair = (("p0", op.default()), ("tuned", op.from_string(tuned_text)))
+    times: Dict[str, List[float]] = {"p0": [], "tuned": []}
+    for _ in range(rounds):
+        for key, sched in pair:
+            ev.cache.pop(str(sched), None)       # time again, not from the cache
+            rec = ev.measure(sched)
+            if not rec.get("valid"):
+                raise RuntimeError(f"{key} schedule did not run: {rec.get('error')}")
+            times[key].append(rec["ms"] * 1e3)
+    p0_us, tuned_us = statistics.median(times["p0"]), statistics.median(times["tuned"])
+    return {"workload": name, "p0_schedule": str(pair[0][1]), "tuned_schedule": str(pair[1][1]),
+            "measurement": f"cold: a 512 MiB buffer overwritten before each timed launch; median of "
+                           f"{repeat} launches; P0 and the tuned schedule alternating {rounds} times",
+            "p0_us": times["p0"], "tuned_us": times["tuned"],
+            "p0_reward": reward_of(op, p0_us * 1e-3), "tuned_reward": reward_of(op, tuned_us * 1e-3),
+            "tuned_speedup_over_p0": p0_us / tuned_us}
+
+
 PAPER_AXES = (18, 36, 72, 150, 200)   # sample counts of the paper's best-vs-samples table
 
 
@@ -937,6 +964,9 @@ def main(argv=None):
     ap.add_argument("--warm", action="store_true",
                     help="campaign timing without the cache flush (back-to-back launches on the same inputs)")
     ap.add_argument("--jobs", type=int, default=12, help="compile worker processes (--campaign)")
+    ap.add_argument("--p0", action="store_true",
+                    help="time the untransformed program P0 and the tuned schedule cold in one process "
+                         "(the tuned schedule's speedup over P0)")
     ap.add_argument("--slow-ms", type=float, default=50.0,
                     help="a schedule slower than this on its first launch is timed once (--campaign)")
     args = ap.parse_args(argv)
@@ -961,6 +991,15 @@ def main(argv=None):
                 bad += sum(1 for x in st if x != 0)
                 print(f"compiled {min(i + chunk, len(space))}/{len(space)} ({bad} rejected) "
                       f"{time.time() - t0:.0f}s", flush=True)
+        return
+
+    if args.p0:
+        tuned = json.load(open(os.path.join(HERE, "tuned.json")))
+        rec = time_p0_and_tuned(op, args.workload, tuned[args.workload], repeat=args.repeat)
+        with open(os.path.join(args.out, f"{args.workload}.p0.json"), "w") as f:
+            json.dump(rec, f, indent=1)
+        print(json.dumps({k: rec[k] for k in ("workload", "p0_us", "tuned_us", "tuned_speedup_over_p0")}),
+              flush=True)
         return
 
     if args.campaign:

@@ -687,3 +687,33 @@ def test_campaign_timing_passes_the_flush_choice_to_the_timer():
             tune.rc.Plan = orig
         assert seen and all(f is flush for f in seen)
         seen.clear()
+
+
+def test_p0_timing_alternates_and_reports_the_tuned_speedup(monkeypatch):
+    # P0 and the tuned schedule are timed alternately, each again rather
+    # than from the evaluator's cache; the speedup is the ratio of medians
+    from paper_2506_01374_amd import tune
+    op = rc.Op(rc.RC_OP_GEMM_F32, (128, 128, 128))
+    tuned_text = "tile_m=32,tile_n=32,tile_k=32,waves_m=1,waves_n=2,vec=4,stages=2,unroll=1,layout=0"
+    assert op.from_string(tuned_text).validate() == ""
+    order = []
+
+    class FakeEvaluator:
+        def __init__(self, op, repeat=10, warmup=2, log=None):
+            self.cache = {}
+
+        def measure(self, sched):
+            text = str(sched)
+            assert text not in self.cache
+            order.append(text)
+            ms = 0.9 if text == str(op.default()) else 0.3
+            self.cache[text] = {"valid": True, "ms": ms + 0.01 * len(order)}
+            return self.cache[text]
+
+    monkeypatch.setattr(tune, "GpuEvaluator", FakeEvaluator)
+    rec = tune.time_p0_and_tuned(op, "gemm_f32_128", tuned_text, repeat=3, rounds=2)
+    p0, tuned = str(op.default()), str(op.from_string(tuned_text))
+    assert order == [p0, tuned, p0, tuned]
+    assert all(math.isclose(a, b) for a, b in zip(rec["p0_us"] + rec["tuned_us"], [910.0, 930.0, 320.0, 340.0]))
+    assert abs(rec["tuned_speedup_over_p0"] - 920.0 / 330.0) < 1e-9
+    assert rec["p0_reward"] < rec["tuned_reward"]
