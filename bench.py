@@ -153,6 +153,21 @@ def _search_headline(records):
     return best
 
 
+def _p0_speedup(name, op, sched):
+    """The tuned schedule's cold speedup over the untransformed program P0
+    (results/<workload>.p0.json, written by `tune.py --p0`), only if that
+    record was taken with this exact schedule; else null."""
+    path = os.path.join(ROOT, "results", f"{name}.p0.json")
+    try:
+        rec = json.load(open(path))
+        if str(op.from_string(rec["tuned_schedule"])) != str(sched):
+            return None
+        return {"source": os.path.relpath(path, ROOT), "value": round(rec["tuned_speedup_over_p0"], 3),
+                "p0_us": rec["p0_us"], "tuned_us": rec["tuned_us"], "measurement": rec.get("measurement")}
+    except Exception:      # no record, or one this version cannot read
+        return None
+
+
 def _kernel_source(name):
     from paper_2506_01374_amd import rc, workloads as W
     kind = W.workload_op(name).kind
@@ -351,6 +366,7 @@ def main():
         "roofline": roof, "cpu_baseline": cpu,
         "search": search,
         "search_headline": _search_headline(search),
+        "tuned_speedup_over_p0": _p0_speedup(name, op, sched),
     }
     print(json.dumps(rec), flush=True)
 

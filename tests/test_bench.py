@@ -47,3 +47,18 @@ def test_traffic_records_are_keyed_by_the_tuned_schedules():
         assert str(op.from_string(records[name]["key"])) == str(op.from_string(text)), name
         assert records[name]["bytes_per_launch"] > 0
         assert bench._load_traffic(name, op, op.default()) is None
+
+
+def test_p0_speedup_records_answer_only_for_their_tuned_schedule():
+    # Every workload has a P0 record taken with its tuned schedule; the
+    # record never answers for another schedule or a missing workload.
+    import bench
+    from paper_2506_01374_amd import workloads as W
+    tuned = json.load(open(os.path.join(ROOT, "paper_2506_01374_amd", "tuned.json")))
+    for name, text in tuned.items():
+        op = W.workload_op(name)
+        rec = bench._p0_speedup(name, op, op.from_string(text))
+        assert rec is not None and rec["value"] > 1.0, name
+        assert min(rec["p0_us"]) > max(rec["tuned_us"]), name
+        assert bench._p0_speedup(name, op, op.default()) is None
+    assert bench._p0_speedup("no_such_workload", op, op.default()) is None
